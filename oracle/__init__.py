@@ -1,0 +1,10 @@
+"""Plain fp64 CPU oracle of the SAO per-token loss pass.
+
+TEST INFRASTRUCTURE ONLY. Only the test suite, the smoke check and the CPU
+baseline leg of the benchmark may import this package. The product path (the
+HIP library and its Python binding) never imports it and has no CPU fallback.
+"""
+from .sao_oracle import (  # noqa: F401
+    token_logprob, token_logprob_loop, advantage, dis_loss,
+    loss_backward, loss_backward_loop, value_forward, value_loss, surrogate_S,
+)

@@ -1,0 +1,305 @@
+"""fp64 CPU oracle of the SAO per-token training-loss pass.
+
+TEST INFRASTRUCTURE ONLY: imported by the test suite, the smoke check and the
+benchmark's CPU-baseline leg, never by the product path.
+
+Every quantity of the pass is a closed-form function of its inputs, so each
+function below is the plain definition evaluated in float64, in the order the
+paper states it:
+
+* ``token_logprob``  -- log pi_theta(a_t|s_t) of the LM head at temperature 1
+  over the full vocabulary (Sec. 3.1, Eq. 1-2; evaluation settings of Sec. 4.1).
+* ``advantage``      -- skip-observation token-level GAE (Sec. 3.2, Eq. 4-5)
+  with the length-adaptive lambda_policy = 1 - 1/(alpha*l) and critic returns
+  at lambda_critic = 1 (Sec. 4.1, training details); textbook GAE of Sec. 2 is
+  the special case without observations.
+* ``dis_loss``       -- the direct double-sided importance-sampling objective:
+  ratio against the rollout log-probs (Eq. 2), calibration f with strict band
+  edges (Eq. 3), token-level mean of f(r) A log pi (Eq. 1).
+* ``loss_backward``  -- gradient of that objective into the hidden states and
+  the head weights through the log-softmax.
+* ``value_forward`` / ``value_loss`` -- a bias-free H->1 critic head and the
+  critic's squared-error loss against the returns (Sec. 2, PPO paragraph).
+
+Readings where the paper is silent (all listed in the design notes):
+  gamma defaults to 1; ``l`` in lambda_policy is the trajectory's token length
+  (observations included), lambda clamped at 0; rewards on observation tokens
+  fold into the preceding action, rewards before the first action are dropped;
+  the value after a trajectory's last action is 0; the token mean divides by
+  N = number of loss-mask tokens (clipped ones included); f(r) is a
+  stop-gradient weight; the library minimises -L; band edges are strict as in
+  Eq. 3 (equality is clipped); a NaN ratio is flagged non-finite and
+  contributes exactly 0.
+
+Large inputs are processed in blocks of rows only to bound memory: rows are
+independent in every definition here, so the blocking changes no arithmetic.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional, Sequence
+
+import numpy as np
+
+FLAG_MASKED, FLAG_USED, FLAG_LOW, FLAG_HIGH, FLAG_NONFINITE = 0, 1, 2, 3, 4
+
+
+def _f64(x):
+    return np.asarray(x, dtype=np.float64)
+
+
+def _active_rows(T: int, mask, rows):
+    if rows is not None:
+        return np.asarray(rows, dtype=np.int64)
+    if mask is None:
+        return np.arange(T, dtype=np.int64)
+    return np.nonzero(np.asarray(mask) != 0)[0].astype(np.int64)
+
+
+# --------------------------------------------------------------------------- #
+# Eq. (1)-(2): per-token log-probability under the current policy's LM head.
+# --------------------------------------------------------------------------- #
+def token_logprob(hidden, w_head, target, mask=None, rows: Optional[Sequence[int]] = None,
+                  block: int = 1024, w64: Optional[np.ndarray] = None):
+    """log pi(y_t | s_t) = z_{t,y_t} - log sum_v exp(z_{t,v}),  z_{t,v} = h_t . W_v.
+
+    Returns ``(logp, lse)`` as float64 arrays of length T. Rows outside the loss
+    mask (or outside ``rows`` when given) are 0, matching the library's
+    convention for rows it does not compute.
+    """
+    T = hidden.shape[0]
+    W = _f64(w_head) if w64 is None else w64
+    tgt = np.asarray(target, dtype=np.int64)
+    logp = np.zeros(T, dtype=np.float64)
+    lse = np.zeros(T, dtype=np.float64)
+    act = _active_rows(T, mask, rows)
+    for s in range(0, act.size, block):
+        r = act[s:s + block]
+        z = _f64(hidden[r]) @ W.T                              # z_{t,v} = sum_k h_{t,k} W_{v,k}
+        if np.abs(z).max(initial=0.0) > 700.0:
+            raise ValueError("logits beyond the range where exp() is finite in float64")
+        lse_r = np.log(np.exp(z).sum(axis=1))                  # log sum_v exp(z_{t,v})
+        lse[r] = lse_r
+        logp[r] = z[np.arange(r.size), tgt[r]] - lse_r         # z_{t,y_t} - lse_t
+    return logp, lse
+
+
+def token_logprob_loop(hidden, w_head, target, mask=None):
+    """The same definition as ``token_logprob`` written as scalar loops (tiny inputs)."""
+    T, H = hidden.shape
+    V = w_head.shape[0]
+    logp = [0.0] * T
+    lse = [0.0] * T
+    for t in range(T):
+        if mask is not None and not mask[t]:
+            continue
+        h = [float(x) for x in hidden[t]]
+        zs = []
+        for v in range(V):
+            w = w_head[v]
+            zs.append(math.fsum(h[k] * float(w[k]) for k in range(H)))
+        s = math.fsum(math.exp(z) for z in zs)
+        lse[t] = math.log(s)
+        logp[t] = zs[int(target[t])] - lse[t]
+    return np.array(logp), np.array(lse)
+
+
+# --------------------------------------------------------------------------- #
+# Eq. (4)-(5): skip-observation token-level GAE, with critic returns.
+# --------------------------------------------------------------------------- #
+def trajectory_lambda(L_tokens: int, n_actions: int, lam: float, alpha: float,
+                      length: str = "tokens") -> float:
+    """lambda_policy = 1 - 1/(alpha*l) (length-adaptive GAE, Sec. 4.1), clamped at 0.
+
+    ``alpha <= 0`` selects the fixed ``lam``. ``l`` is the trajectory's token
+    length by default; ``length="actions"`` uses the number of action tokens.
+    """
+    if alpha <= 0.0:
+        return float(lam)
+    l = L_tokens if length == "tokens" else n_actions
+    if l <= 0:
+        return 0.0
+    return max(0.0, 1.0 - 1.0 / (alpha * l))
+
+
+def advantage(values, rewards, mask, cu_seqlens, gamma: float = 1.0, lam: float = 1.0,
+              alpha: float = 0.0, length: str = "tokens"):
+    """Skip-observation GAE advantages and lambda=1 returns for a packed batch.
+
+    For trajectory b with action positions tau_0 < ... < tau_{n-1} (mask 1) in
+    [s_b, e_b), and tau_n := e_b:
+        r~_k   = sum of rewards at positions tau_k .. tau_{k+1}-1
+        delta_k = r~_k + gamma * V(tau_{k+1}) - V(tau_k)     (V after the last action = 0)
+        A_k     = delta_k + gamma * lambda_b * A_{k+1}        (A_n = 0)          Eq. (4)-(5)
+        G_k     = r~_k + gamma * G_{k+1}                      (G_n = 0, lambda_critic = 1)
+    Outputs are float64 arrays with 0 at mask-0 positions, and N = sum(mask).
+    """
+    vals, rew = _f64(values), _f64(rewards)
+    m = np.asarray(mask) != 0
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    T = vals.shape[0]
+    adv = np.zeros(T, dtype=np.float64)
+    ret = np.zeros(T, dtype=np.float64)
+    for b in range(cu.size - 1):
+        s, e = int(cu[b]), int(cu[b + 1])
+        tau = [t for t in range(s, e) if m[t]]
+        n = len(tau)
+        if n == 0:
+            continue
+        lam_b = trajectory_lambda(e - s, n, lam, alpha, length)
+        bounds = tau + [e]
+        r_fold = [math.fsum(rew[bounds[k]:bounds[k + 1]]) for k in range(n)]
+        v = [vals[t] for t in tau] + [0.0]
+        A_next, G_next = 0.0, 0.0
+        for k in range(n - 1, -1, -1):
+            delta = r_fold[k] + gamma * v[k + 1] - v[k]
+            A_k = delta + gamma * lam_b * A_next
+            G_k = r_fold[k] + gamma * G_next
+            adv[tau[k]], ret[tau[k]] = A_k, G_k
+            A_next, G_next = A_k, G_k
+    return adv, ret, int(m.sum())
+
+
+# --------------------------------------------------------------------------- #
+# Eq. (1)-(3): direct double-sided importance sampling and the token mean.
+# --------------------------------------------------------------------------- #
+def dis_loss(logp, logp_rollout, adv, mask, eps_low, eps_high, n_tokens: Optional[int] = None):
+    """DIS loss, its gradient w.r.t. log pi, per-token flags and counts.
+
+    eps_low/eps_high are the float32 values the library receives, widened to
+    float64. For each loss-mask token:
+        rho_t = exp(log pi_t - log pi_rollout_t)                         Eq. (2)
+        flag  = 4 if rho is NaN; 2 if rho <= 1-eps_low; 3 if rho >= 1+eps_high; else 1
+        c_t   = [flag == 1]                    (strict band of f, Eq. (3))
+    With N the token-mean denominator:
+        loss[0] = -(1/N) sum_t c_t rho_t A_t log pi_t    (minus Eq. (1))
+        loss[1] = -(1/N) sum_t c_t rho_t A_t             (same gradient, f as stop-gradient)
+        g_t     = -c_t rho_t A_t / N                     (d loss / d log pi_t; exactly 0 if c_t=0)
+    counts = [sum(mask), used, clipped-low, clipped-high, non-finite].
+    """
+    lp, lro, A = _f64(logp), _f64(logp_rollout), _f64(adv)
+    m = np.asarray(mask) != 0
+    lo_edge = 1.0 - float(np.float32(eps_low))
+    hi_edge = 1.0 + float(np.float32(eps_high))
+    N = int(m.sum()) if n_tokens is None else int(n_tokens)
+    with np.errstate(over="ignore", invalid="ignore"):
+        rho = np.exp(lp - lro)                                   # Eq. (2)
+    flags = np.where(np.isnan(rho), FLAG_NONFINITE,
+             np.where(rho <= lo_edge, FLAG_LOW,
+              np.where(rho >= hi_edge, FLAG_HIGH, FLAG_USED)))
+    flags = np.where(m, flags, FLAG_MASKED).astype(np.uint8)
+    used = flags == FLAG_USED                                    # 1 - eps_l < rho < 1 + eps_h
+    g = np.zeros(lp.shape[0], dtype=np.float64)
+    loss = np.zeros(2, dtype=np.float64)
+    if N > 0:
+        idx = np.nonzero(used)[0]
+        loss[0] = -math.fsum(rho[idx] * A[idx] * lp[idx]) / N
+        loss[1] = -math.fsum(rho[idx] * A[idx]) / N
+        g[idx] = -rho[idx] * A[idx] / N
+    counts = np.array([int(m.sum()), int(used.sum()), int((flags == FLAG_LOW).sum()),
+                       int((flags == FLAG_HIGH).sum()), int((flags == FLAG_NONFINITE).sum())],
+                      dtype=np.int64)
+    return loss, g, flags, counts
+
+
+# --------------------------------------------------------------------------- #
+# Backward through the log-softmax into hidden states and head weights.
+# --------------------------------------------------------------------------- #
+def loss_backward(hidden, w_head, target, lse, g, dh_rows: Optional[Sequence[int]] = None,
+                  dw_rows: Optional[Sequence[int]] = None, block: int = 1024,
+                  w64: Optional[np.ndarray] = None):
+    """dz_{t,v} = g_t (1[v = y_t] - exp(z_{t,v} - lse_t));  dH_t = sum_v dz_{t,v} W_v;
+    dW_v = sum_t dz_{t,v} h_t.
+
+    Only rows with g_t != 0 contribute; dH is exactly 0 elsewhere. ``dh_rows``
+    restricts dH to the given token rows (others 0) and ``dw_rows`` restricts dW
+    to the given vocabulary rows (others 0); both default to everything.
+    Returns float64 ``(dH [T,H], dW [V,H])``.
+    """
+    T, H = hidden.shape
+    V = w_head.shape[0]
+    W = _f64(w_head) if w64 is None else w64
+    gg, L = _f64(g), _f64(lse)
+    tgt = np.asarray(target, dtype=np.int64)
+    live = np.nonzero(gg != 0.0)[0]
+    dH = np.zeros((T, H), dtype=np.float64)
+    dW = np.zeros((V, H), dtype=np.float64)
+
+    want_dh = live if dh_rows is None else np.intersect1d(live, np.asarray(dh_rows, dtype=np.int64))
+    for s in range(0, want_dh.size, block):
+        r = want_dh[s:s + block]
+        z = _f64(hidden[r]) @ W.T
+        dz = -gg[r, None] * np.exp(z - L[r, None])
+        dz[np.arange(r.size), tgt[r]] += gg[r]
+        dH[r] = dz @ W
+
+    vrows = np.arange(V, dtype=np.int64) if dw_rows is None else np.asarray(dw_rows, dtype=np.int64)
+    Wv = W[vrows]
+    for s in range(0, live.size, block):
+        r = live[s:s + block]
+        h = _f64(hidden[r])
+        z = h @ Wv.T                                           # z_{t,v} for the requested v
+        dz = -gg[r, None] * np.exp(z - L[r, None])
+        onehot = tgt[r, None] == vrows[None, :]
+        dz += onehot * gg[r, None]
+        dW[vrows] += dz.T @ h
+    return dH, dW
+
+
+def loss_backward_loop(hidden, w_head, target, lse, g):
+    """``loss_backward`` as scalar loops (tiny inputs)."""
+    T, H = hidden.shape
+    V = w_head.shape[0]
+    dH = np.zeros((T, H))
+    dW = np.zeros((V, H))
+    for t in range(T):
+        if g[t] == 0.0:
+            continue
+        h = [float(x) for x in hidden[t]]
+        for v in range(V):
+            w = [float(x) for x in w_head[v]]
+            z = math.fsum(h[k] * w[k] for k in range(H))
+            dz = float(g[t]) * ((1.0 if v == int(target[t]) else 0.0) - math.exp(z - float(lse[t])))
+            for k in range(H):
+                dH[t, k] += dz * w[k]
+                dW[v, k] += dz * h[k]
+    return dH, dW
+
+
+def surrogate_S(hidden, w_head, target, logp_rollout, adv, used, n_tokens: int):
+    """S = -(1/N) sum_{used t} exp(log pi_t - log pi_rollout_t) A_t with the used set frozen.
+
+    Its gradient equals the gradient of -Eq. (1) with f(r) as a stop-gradient
+    weight; finite differences of S pin ``loss_backward``.
+    """
+    rows = np.nonzero(np.asarray(used))[0]
+    lp, _ = token_logprob(hidden, w_head, target, rows=rows)
+    rho = np.exp(lp[rows] - _f64(logp_rollout)[rows])
+    return -math.fsum(rho * _f64(adv)[rows]) / n_tokens
+
+
+# --------------------------------------------------------------------------- #
+# Critic head and its squared-error loss (Sec. 2, PPO paragraph).
+# --------------------------------------------------------------------------- #
+def value_forward(hidden, w_value):
+    """v_t = h_t . w_v (bias-free H->1 head)."""
+    return _f64(hidden) @ _f64(w_value)
+
+
+def value_loss(hidden, w_value, v, ret, mask, n_tokens: Optional[int] = None):
+    """L_V = (1/N) sum_t m_t (v_t - G_t)^2, with its gradients.
+
+    Returns ``(L_V, dH_v [T,H], dw_v [H])`` where dv_t = 2 m_t (v_t - G_t) / N,
+    dH_v = dv_t w_v and dw_v = sum_t dv_t h_t.
+    """
+    vv, G = _f64(v), _f64(ret)
+    m = (np.asarray(mask) != 0).astype(np.float64)
+    N = int(m.sum()) if n_tokens is None else int(n_tokens)
+    if N == 0:
+        return 0.0, np.zeros(hidden.shape), np.zeros(hidden.shape[1])
+    diff = vv - G
+    L = math.fsum(m * diff * diff) / N
+    dv = 2.0 * m * diff / N
+    dH = dv[:, None] * _f64(w_value)[None, :]
+    dw = _f64(hidden).T @ dv
+    return L, dH, dw
