@@ -1,0 +1,202 @@
+#!/usr/bin/env python3
+"""Throughput of the SAO per-token loss pass on one MI355X.
+
+One step is the whole hot path over one synthetic batch: skip-observation GAE
+(sao_advantage), LM-head log-probs (sao_token_logprob), the DIS loss
+(sao_clipped_loss) and the backward into hidden states and W_head
+(sao_loss_backward), with the zeroing of the accumulated outputs. Inputs are
+resident in HBM before the timed region.
+
+Default workload: 16 single rollouts, T = 65,536 tokens, H = 2048, V = 151,936,
+bf16 hidden/W_head, forward + backward, drift noise sigma 0.2.
+
+Prints one JSON line (rank 0, one GPU): tokens/s, the roofline figure of the
+head-forward MFMA kernel (timed live with HIP events around its launches) and
+the fp64 oracle timed on this host's cores over a bounded sample of the batch.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tokens/s SAO logprob+clipped-loss fwd+bwd (H2048,V152k); % bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA, TFLOP/s
+WORKLOAD_TEXT = {
+    "c2": "16 single rollouts, T=65536, H=2048, V=151936, bf16, fwd+bwd, ~30% observation tokens, "
+          "drift sigma 0.2, eps 0.2/0.2, gamma 1, alpha 1.5",
+}
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(batch, ref_logp, rows: int, seed: int = 0):
+    """The oracle on a bounded sample: `rows` loss-mask tokens through the head pass
+    (forward, and backward for those with g != 0), plus the whole-batch scan and
+    loss; scaled to the whole batch by the share of loss-mask tokens sampled."""
+    import oracle
+    from synth import rollout_logprobs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    cfg = batch.cfg
+    act = np.nonzero(batch.mask)[0]
+    rng = np.random.default_rng(seed)
+    sample = np.sort(rng.choice(act, size=min(rows, act.size), replace=False))
+    t0 = time.perf_counter()
+    w64 = batch.w_head.astype(np.float64)
+    adv, ret, N = oracle.advantage(batch.values, batch.rewards, batch.mask, batch.cu_seqlens, cfg.gamma,
+                                   cfg.lam, cfg.alpha)
+    t_scan = time.perf_counter() - t0
+    t1 = time.perf_counter()
+    lp, lse = oracle.token_logprob(batch.hidden, None, batch.target, rows=sample, w64=w64)
+    lro = rollout_logprobs(ref_logp, batch.xi)
+    sub = np.zeros_like(batch.mask)
+    sub[sample] = 1
+    _, g, _, _ = oracle.dis_loss(lp, lro, adv, sub, cfg.eps_low, cfg.eps_high, N)
+    oracle.loss_backward(batch.hidden, None, batch.target, lse, g, w64=w64)
+    t_head = time.perf_counter() - t1
+    est = t_scan + t_head * act.size / sample.size
+    return {"value": batch.T / est, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{sample.size} of {act.size} loss-mask tokens through the fp64 head forward+backward "
+                      f"({t_head:.1f} s, scaled by {act.size / sample.size:.1f}) plus the whole-batch "
+                      f"scan and loss ({t_scan:.1f} s); W_head widening to fp64 excluded"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--cpu-rows", type=int, default=256, help="loss-mask tokens in the oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_07508_amd as sao
+    from paper_2607_07508_amd import binding as B
+    from synth import CONFIGS, generate
+    from synth.device import to_device
+    from tests.golden.make_full_logprobs import load as load_golden
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        sys.exit(1)
+    cfg = CONFIGS[args.workload]
+    log(f"generating {args.workload}")
+    batch = generate(cfg)
+    ref_logp, _ = load_golden(args.workload, batch)
+    db = to_device(batch, ref_logp)
+    L = sao.lib()
+    T, H, V = batch.T, cfg.H, cfg.V
+    dev = db.hidden.device
+    st = torch.cuda.current_stream(dev).cuda_stream
+    f32 = dict(dtype=torch.float32, device=dev)
+
+    logp = torch.empty(T, **f32)
+    lse = torch.empty(T, **f32)
+    adv = torch.empty(T, **f32)
+    ret = torch.empty(T, **f32)
+    g = torch.empty(T, **f32)
+    flags = torch.empty(T, dtype=torch.uint8, device=dev)
+    n_tok = torch.zeros(1, dtype=torch.int64, device=dev)
+    loss = torch.zeros(2, dtype=torch.float64, device=dev)
+    counts = torch.zeros(5, dtype=torch.int64, device=dev)
+    dhid = torch.empty((T, H), dtype=db.hidden.dtype, device=dev)
+    dw = torch.zeros((V, H), **f32)
+    dt = B.SAO_BF16 if cfg.dtype == "bf16" else B.SAO_F32
+    ws_bytes = max(B.workspace_size(B.OP_LOGPROB, T, H, V, dt), B.workspace_size(B.OP_BACKWARD, T, H, V, dt),
+                   B.workspace_size(B.OP_LOSS, T, 1, 1, dt), B.workspace_size(B.OP_ADVANTAGE, T, 1, 1, dt))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    p = lambda t: t.data_ptr()  # noqa: E731
+
+    def step():
+        loss.zero_()
+        counts.zero_()
+        dw.zero_()
+        B._check(L.sao_advantage(p(db.values), p(db.rewards), p(db.mask), p(db.cu_seqlens), cfg.B, T,
+                                 cfg.gamma, cfg.lam, cfg.alpha, p(adv), p(ret), p(n_tok), None, p(ws), ws_bytes,
+                                 st))
+        B._check(L.sao_token_logprob(p(db.hidden), H, p(db.w_head), H, p(db.target), p(db.mask), T, H, V, dt,
+                                     p(logp), p(lse), None, p(ws), ws_bytes, st))
+        B._check(L.sao_clipped_loss(p(logp), p(db.logp_rollout), p(adv), p(db.mask), T, cfg.eps_low,
+                                    cfg.eps_high, p(n_tok), p(loss), p(g), p(flags), p(counts), p(ws),
+                                    ws_bytes, st))
+        B._check(L.sao_loss_backward(p(db.hidden), H, p(db.w_head), H, p(db.target), p(lse), p(g), T, H, V,
+                                     dt, p(dhid), p(dw), p(ws), ws_bytes, st))
+
+    log(f"warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    counts_h = counts.cpu().numpy()
+    t_act = int(counts_h[0])
+    t_grad = int(counts_h[1])
+
+    fwd_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    for a, b in fwd_ev:        # materialise the event handles
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        B.time_kernel(B.KERNEL_HEAD_FORWARD, *fwd_ev[i])
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    B.time_kernel(B.KERNEL_NONE, None, None)
+    ms = start.elapsed_time(stop) / args.steps
+    fwd_ms = float(np.mean([a.elapsed_time(b) for a, b in fwd_ev]))
+
+    fwd_flops = 2.0 * t_act * V * H
+    achieved = fwd_flops / (fwd_ms * 1e-3) / 1e12
+    algo_flops = (2.0 * t_act + 4.0 * t_grad) * V * H
+    out = {
+        "metric": METRIC,
+        "value": T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {WORKLOAD_TEXT[args.workload]}", "T": T, "H": H, "V": V,
+                   "B": cfg.B, "T_act": t_act, "T_grad": t_grad, "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "mfma", "kernel": "k_head_fwd (sao_token_logprob)", "achieved": achieved,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": None, "launch_ms": fwd_ms, "flops_per_launch": fwd_flops},
+        "algorithmic_mfma_frac": algo_flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+    }
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline over {args.cpu_rows} rows")
+        out["cpu_baseline"] = cpu_baseline(batch, ref_logp, args.cpu_rows)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

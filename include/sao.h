@@ -1,0 +1,197 @@
+/*
+ * sao.h -- C ABI of the SAO per-token training-loss pass on AMD MI355X (gfx950).
+ *
+ * The pass is the loss side of single-rollout asynchronous RL with direct
+ * double-sided importance sampling (DIS): per-token log-probs of the LM head,
+ * skip-observation GAE advantages, the DIS ratio against the rollout engine's
+ * log-probs with a strict two-sided token mask, a token-level mean, and the
+ * backward into the hidden states and the head weights.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.   Every array argument is a DEVICE pointer owned by the caller. The
+ *           library never allocates or frees caller-visible memory and keeps no
+ *           mutable global state. Scratch space is the caller's `ws` buffer of
+ *           `ws_bytes` bytes (device memory, 256-byte aligned), at least
+ *           sao_workspace_size(...) bytes; its contents on entry are ignored.
+ * Streams.  All work is enqueued on `stream` (a hipStream_t; NULL = the null
+ *           stream). Calls return before the device finishes and never
+ *           synchronise. Calls on one stream are ordered; the caller orders
+ *           calls on different streams. The library is reentrant.
+ * Layouts.  Token-major, row-major. `hidden` is T rows of H elements with row
+ *           stride `ld_hidden` elements; `w_head` is V rows of H elements with
+ *           row stride `ld_w`. Strides must be >= H and multiples of 8, H must
+ *           be a multiple of 8, and the two bases 16-byte aligned. Per-token
+ *           arrays are dense, length T, aligned so that hidden[t] predicts
+ *           target[t] and logp_rollout[t], values[t], rewards[t], mask[t]
+ *           describe the same action a_t.
+ * Dtypes.   SAO_BF16: hidden/w_head/dhidden are bfloat16 (bit patterns, 2 bytes),
+ *           products accumulate in fp32. SAO_F32: they are float32.
+ * Masks.    mask[t] = 1 marks a model-generated action token (the loss mask);
+ *           0 marks prompt/observation tokens.
+ * Errors.   Anything checkable on the host is returned synchronously before any
+ *           work is enqueued: SAO_ERR_NULL (required pointer NULL), SAO_ERR_SHAPE
+ *           (negative size, H or V < 1, bad stride/alignment, B < 1),
+ *           SAO_ERR_VALUE (epsilon negative or non-finite, gamma or lambda
+ *           outside [0,1], alpha non-finite), SAO_ERR_DTYPE, SAO_ERR_WORKSPACE
+ *           (ws too small or misaligned), SAO_ERR_DEVICE (a HIP launch failed).
+ *           sao_last_error_message() gives a thread-local detail string.
+ *           T == 0 is a no-op that returns SAO_OK.
+ *           Data errors visible only on the device (a target outside [0,V),
+ *           cu_seqlens not non-decreasing or not ending at T, a non-finite
+ *           log-sum-exp) OR bits into the optional device word `*status`
+ *           (SAO_STATUS_*) without a host synchronisation; the affected outputs
+ *           are NaN rather than silently valid.
+ * Accumulation.  Outputs documented as "+=" accumulate so that chunked calls sum
+ *           to the whole batch; the caller zeroes them. All other outputs are
+ *           overwritten.
+ *
+ * Citations name sections and equations of "Single-Rollout Asynchronous
+ * Optimization for Agentic Reinforcement Learning" (arXiv 2607.07508).
+ */
+#ifndef SAO_H
+#define SAO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* hipStream_t;
+
+typedef enum {
+  SAO_OK = 0,
+  SAO_ERR_NULL = 1,
+  SAO_ERR_SHAPE = 2,
+  SAO_ERR_VALUE = 3,
+  SAO_ERR_DTYPE = 4,
+  SAO_ERR_WORKSPACE = 5,
+  SAO_ERR_DEVICE = 6
+} sao_status_t;
+
+typedef enum { SAO_BF16 = 0, SAO_F32 = 1 } sao_dtype_t;
+
+typedef enum {
+  SAO_OP_LOGPROB = 0,
+  SAO_OP_ADVANTAGE = 1,
+  SAO_OP_LOSS = 2,
+  SAO_OP_BACKWARD = 3,
+  SAO_OP_VALUE = 4
+} sao_op_t;
+
+/* Bits of the optional device status word. */
+#define SAO_STATUS_TARGET_RANGE 1  /* a loss-mask token's target is outside [0, V)   */
+#define SAO_STATUS_SEGMENTS     2  /* cu_seqlens is not non-decreasing from 0 to T    */
+#define SAO_STATUS_NONFINITE    4  /* a log-sum-exp came out NaN or infinite          */
+
+/* Per-token flags written by sao_clipped_loss. */
+#define SAO_FLAG_MASKED    0  /* mask == 0                                       */
+#define SAO_FLAG_USED      1  /* 1 - eps_low < rho < 1 + eps_high                 */
+#define SAO_FLAG_LOW       2  /* rho <= 1 - eps_low                               */
+#define SAO_FLAG_HIGH      3  /* rho >= 1 + eps_high                              */
+#define SAO_FLAG_NONFINITE 4  /* rho is NaN                                       */
+
+const char* sao_status_string(sao_status_t status);
+const char* sao_last_error_message(void);
+/* Library version as "major.minor.patch". */
+const char* sao_version(void);
+
+/* Bytes of `ws` that `op` needs for T tokens, hidden size H and vocabulary V
+ * (0 if none). Returns 0 for invalid arguments as well. */
+size_t sao_workspace_size(sao_op_t op, int64_t T, int64_t H, int64_t V, sao_dtype_t dtype);
+
+/*
+ * Per-token log-probabilities of the current policy, Sec. 3.1, Eq. (1)-(2):
+ *   z_{t,v} = hidden[t] . w_head[v],  lse[t] = log sum_v exp(z_{t,v}),
+ *   logp[t] = z_{t,target[t]} - lse[t]            (temperature 1, full vocabulary).
+ * Rows with mask[t] == 0 are skipped and get logp = lse = 0; mask == NULL means
+ * every row. The T x V logits never reach memory: each tile of logits is reduced
+ * to a running (max, sum of exponentials) per token inside the kernel.
+ * Outputs: logp[T], lse[T] float32 (overwritten). lse is the input of
+ * sao_loss_backward.
+ */
+sao_status_t sao_token_logprob(const void* hidden, int64_t ld_hidden, const void* w_head,
+                               int64_t ld_w, const int32_t* target, const uint8_t* mask,
+                               int64_t T, int64_t H, int64_t V, sao_dtype_t dtype, float* logp,
+                               float* lse, int32_t* status, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/*
+ * Skip-observation token-level GAE, Sec. 3.2, Eq. (4)-(5), over B packed
+ * trajectories; trajectory b is tokens [cu_seqlens[b], cu_seqlens[b+1]).
+ * For its action tokens tau_0 < ... < tau_{n-1} (mask 1), with tau_n = end:
+ *   r~_k    = sum of rewards[tau_k .. tau_{k+1}-1]   (observation rewards fold into
+ *             the preceding action; rewards before the first action are dropped)
+ *   delta_k = r~_k + gamma * values[tau_{k+1}] - values[tau_k]   (0 after the last action)
+ *   adv[tau_k] = delta_k + gamma * lambda_b * adv[tau_{k+1}]
+ *   ret[tau_k] = r~_k + gamma * ret[tau_{k+1}]                   (critic lambda = 1)
+ * lambda_b = max(0, 1 - 1/(alpha * L_b)) with L_b the trajectory's token count
+ * when alpha > 0 (length-adaptive GAE, Sec. 4.1), else `lam`.
+ * Arithmetic is float64 inside; adv/ret are float32, 0 where mask == 0
+ * (overwritten). n_tokens (nullable, device int64) receives sum(mask), the
+ * token-mean denominator N of sao_clipped_loss (overwritten).
+ * values, rewards, mask are [T]; cu_seqlens is int32 [B+1]. If cu_seqlens does
+ * not rise from 0 to T without decreasing, every adv/ret is NaN and the status
+ * word gets SAO_STATUS_SEGMENTS. ws: sao_workspace_size(SAO_OP_ADVANTAGE, ...) bytes.
+ */
+sao_status_t sao_advantage(const float* values, const float* rewards, const uint8_t* mask,
+                           const int32_t* cu_seqlens, int32_t B, int64_t T, double gamma,
+                           double lam, double alpha, float* adv, float* ret, int64_t* n_tokens,
+                           int32_t* status, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Direct double-sided importance sampling and the token-level mean,
+ * Sec. 3.1, Eq. (1)-(3). For each token with mask 1 (in float64):
+ *   rho_t = exp(logp[t] - logp_rollout[t])                         Eq. (2)
+ *   flag  = NONFINITE if rho is NaN, LOW if rho <= 1-eps_low,
+ *           HIGH if rho >= 1+eps_high, else USED                   Eq. (3), strict
+ *   loss[0] += -(1/N) sum_{USED} rho_t adv_t logp_t    (minus Eq. (1))
+ *   loss[1] += -(1/N) sum_{USED} rho_t adv_t           (same gradient)
+ *   g[t]     = -[USED] rho_t adv_t / N                 (d loss / d logp[t]; exactly 0
+ *                                                       unless USED; overwritten)
+ * f(r) is treated as a stop-gradient weight. N = *n_tokens (device int64, the
+ * whole batch's loss-mask count, so chunked calls share one denominator); when
+ * n_tokens is NULL, N = sum(mask) of this call. N == 0 gives zero loss and g.
+ * flags[T] uint8 (overwritten), counts[5] int64 (+=): {sum(mask), USED, LOW,
+ * HIGH, NONFINITE}. loss[2] is float64 (+=). Reductions are deterministic.
+ */
+sao_status_t sao_clipped_loss(const float* logp, const float* logp_rollout, const float* adv,
+                              const uint8_t* mask, int64_t T, float eps_low, float eps_high,
+                              const int64_t* n_tokens, double* loss, float* g, uint8_t* flags,
+                              int64_t* counts, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Backward of the DIS loss through the log-softmax of Eq. (1)-(2):
+ *   dz_{t,v}   = g[t] * (1[v == target[t]] - exp(z_{t,v} - lse[t]))
+ *   dhidden[t] = sum_v dz_{t,v} w_head[v]      (dtype of hidden, dense [T][H]; rows with
+ *                                               g == 0 are exact zeros; overwritten)
+ *   dw_head[v] += sum_t dz_{t,v} hidden[t]     (float32, dense [V][H], +=)
+ * g and lse come from sao_clipped_loss and sao_token_logprob. Rows with g == 0
+ * cost no work. Logits are recomputed on the fly; their gradient is staged in
+ * `ws` one vocabulary block at a time (see sao_workspace_size).
+ */
+sao_status_t sao_loss_backward(const void* hidden, int64_t ld_hidden, const void* w_head,
+                               int64_t ld_w, const int32_t* target, const float* lse,
+                               const float* g, int64_t T, int64_t H, int64_t V, sao_dtype_t dtype,
+                               void* dhidden, float* dw_head, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/*
+ * Measurement hook, not part of the pass. For the calling thread, records the
+ * caller's HIP events `start_event` and `stop_event` (hipEvent_t, created by
+ * the caller with timing enabled) on the launch stream immediately before and
+ * after the next launches of kernel `kernel`; SAO_KERNEL_NONE (or NULL events)
+ * disables it. Each launch re-records the same pair, so the pair brackets the
+ * most recent launch. The library never creates, waits on or destroys these
+ * events.
+ */
+#define SAO_KERNEL_NONE         0
+#define SAO_KERNEL_HEAD_FORWARD 1  /* the MFMA head-forward kernel of sao_token_logprob */
+void sao_debug_time_kernel(int kernel, void* start_event, void* stop_event);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SAO_H */

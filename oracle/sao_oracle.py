@@ -217,8 +217,8 @@ def loss_backward(hidden, w_head, target, lse, g, dh_rows: Optional[Sequence[int
     Returns float64 ``(dH [T,H], dW [V,H])``.
     """
     T, H = hidden.shape
-    V = w_head.shape[0]
     W = _f64(w_head) if w64 is None else w64
+    V = W.shape[0]
     gg, L = _f64(g), _f64(lse)
     tgt = np.asarray(target, dtype=np.int64)
     live = np.nonzero(gg != 0.0)[0]

@@ -1,0 +1,192 @@
+"""ctypes binding of libsao (include/sao.h).
+
+Argument marshalling only: every step of the pass runs in the library's HIP
+kernels. torch supplies device memory (outputs and workspace) and the current
+stream. There is no CPU fallback: a missing library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsao.so")
+
+SAO_BF16, SAO_F32 = 0, 1
+OP_LOGPROB, OP_ADVANTAGE, OP_LOSS, OP_BACKWARD, OP_VALUE = 0, 1, 2, 3, 4
+STATUS_TARGET_RANGE, STATUS_SEGMENTS, STATUS_NONFINITE = 1, 2, 4
+FLAG_MASKED, FLAG_USED, FLAG_LOW, FLAG_HIGH, FLAG_NONFINITE = 0, 1, 2, 3, 4
+
+EXPORTS = ("sao_status_string", "sao_last_error_message", "sao_version", "sao_workspace_size",
+           "sao_token_logprob", "sao_advantage", "sao_clipped_loss", "sao_loss_backward",
+           "sao_debug_time_kernel")
+KERNEL_NONE, KERNEL_HEAD_FORWARD = 0, 1
+
+
+class SaoError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{message} (status {code})")
+        self.code = code
+
+
+_p = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_SIGS = {
+    "sao_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "sao_last_error_message": (ctypes.c_char_p, []),
+    "sao_version": (ctypes.c_char_p, []),
+    "sao_workspace_size": (ctypes.c_size_t, [ctypes.c_int, _i64, _i64, _i64, ctypes.c_int]),
+    "sao_token_logprob": (ctypes.c_int, [_p, _i64, _p, _i64, _p, _p, _i64, _i64, _i64, ctypes.c_int,
+                                         _p, _p, _p, _p, ctypes.c_size_t, _p]),
+    "sao_advantage": (ctypes.c_int, [_p, _p, _p, _p, ctypes.c_int32, _i64, ctypes.c_double,
+                                     ctypes.c_double, ctypes.c_double, _p, _p, _p, _p, _p,
+                                     ctypes.c_size_t, _p]),
+    "sao_clipped_loss": (ctypes.c_int, [_p, _p, _p, _p, _i64, ctypes.c_float, ctypes.c_float, _p, _p,
+                                        _p, _p, _p, _p, ctypes.c_size_t, _p]),
+    "sao_loss_backward": (ctypes.c_int, [_p, _i64, _p, _i64, _p, _p, _p, _i64, _i64, _i64,
+                                         ctypes.c_int, _p, _p, _p, ctypes.c_size_t, _p]),
+    "sao_debug_time_kernel": (None, [ctypes.c_int, _p, _p]),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libsao.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_07508_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(code: int) -> None:
+    if code != 0:
+        raise SaoError(code, lib().sao_last_error_message().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return SAO_BF16
+    if t.dtype == torch.float32:
+        return SAO_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _rows(t: torch.Tensor, name: str) -> int:
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError(f"{name} must be a row-major 2-D tensor with unit column stride")
+    return t.stride(0)
+
+
+def workspace_size(op: int, T: int, H: int, V: int, dtype: int) -> int:
+    return int(lib().sao_workspace_size(op, T, H, V, dtype))
+
+
+def _workspace(nbytes: int, device) -> Optional[torch.Tensor]:
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def token_logprob(hidden: torch.Tensor, w_head: torch.Tensor, target: torch.Tensor,
+                  mask: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None,
+                  out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None):
+    """Per-token (logp, lse) of the LM head; rows with mask 0 get 0."""
+    T, H = hidden.shape
+    V = w_head.shape[0]
+    dt = _dtype_code(hidden)
+    if _dtype_code(w_head) != dt:
+        raise TypeError("hidden and w_head must share a dtype")
+    dev = hidden.device
+    logp, lse = out if out is not None else (torch.empty(T, dtype=torch.float32, device=dev),
+                                             torch.empty(T, dtype=torch.float32, device=dev))
+    ws = _workspace(workspace_size(OP_LOGPROB, T, H, V, dt), dev)
+    _check(lib().sao_token_logprob(
+        _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_head), _rows(w_head, "w_head"), _ptr(target),
+        _ptr(mask), T, H, V, dt, _ptr(logp), _ptr(lse), _ptr(status), _ptr(ws),
+        0 if ws is None else ws.numel(), _stream(dev)))
+    return logp, lse
+
+
+def advantage(values: torch.Tensor, rewards: torch.Tensor, mask: torch.Tensor, cu_seqlens: torch.Tensor,
+              gamma: float = 1.0, lam: float = 1.0, alpha: float = 0.0,
+              status: Optional[torch.Tensor] = None, want_count: bool = True):
+    """Skip-observation GAE: (adv, ret, n_tokens) with n_tokens a device int64 scalar."""
+    T = values.shape[0]
+    B = cu_seqlens.shape[0] - 1
+    dev = values.device
+    adv = torch.empty(T, dtype=torch.float32, device=dev)
+    ret = torch.empty(T, dtype=torch.float32, device=dev)
+    n_tok = torch.empty(1, dtype=torch.int64, device=dev) if want_count else None
+    ws = _workspace(workspace_size(OP_ADVANTAGE, T, 1, 1, SAO_F32), dev)
+    _check(lib().sao_advantage(
+        _ptr(values), _ptr(rewards), _ptr(mask), _ptr(cu_seqlens), B, T, float(gamma), float(lam),
+        float(alpha), _ptr(adv), _ptr(ret), _ptr(n_tok), _ptr(status), _ptr(ws),
+        0 if ws is None else ws.numel(), _stream(dev)))
+    return adv, ret, n_tok
+
+
+def clipped_loss(logp: torch.Tensor, logp_rollout: torch.Tensor, adv: torch.Tensor, mask: torch.Tensor,
+                 eps_low: float, eps_high: float, n_tokens: Optional[torch.Tensor] = None,
+                 loss: Optional[torch.Tensor] = None, counts: Optional[torch.Tensor] = None):
+    """DIS loss: (loss[2] f64 +=, g, flags, counts[5] i64 +=). Zeroed accumulators are made if not given."""
+    T = logp.shape[0]
+    dev = logp.device
+    if loss is None:
+        loss = torch.zeros(2, dtype=torch.float64, device=dev)
+    if counts is None:
+        counts = torch.zeros(5, dtype=torch.int64, device=dev)
+    g = torch.empty(T, dtype=torch.float32, device=dev)
+    flags = torch.empty(T, dtype=torch.uint8, device=dev)
+    ws = _workspace(workspace_size(OP_LOSS, T, 1, 1, SAO_F32), dev)
+    _check(lib().sao_clipped_loss(
+        _ptr(logp), _ptr(logp_rollout), _ptr(adv), _ptr(mask), T, float(eps_low), float(eps_high),
+        _ptr(n_tokens), _ptr(loss), _ptr(g), _ptr(flags), _ptr(counts), _ptr(ws),
+        0 if ws is None else ws.numel(), _stream(dev)))
+    return loss, g, flags, counts
+
+
+def loss_backward(hidden: torch.Tensor, w_head: torch.Tensor, target: torch.Tensor, lse: torch.Tensor,
+                  g: torch.Tensor, dw_head: Optional[torch.Tensor] = None,
+                  dhidden: Optional[torch.Tensor] = None):
+    """(dhidden [T,H] in hidden's dtype, dw_head [V,H] f32 +=; zeroed if not given)."""
+    T, H = hidden.shape
+    V = w_head.shape[0]
+    dt = _dtype_code(hidden)
+    dev = hidden.device
+    if dhidden is None:
+        dhidden = torch.empty((T, H), dtype=hidden.dtype, device=dev)
+    if dw_head is None:
+        dw_head = torch.zeros((V, H), dtype=torch.float32, device=dev)
+    ws = _workspace(workspace_size(OP_BACKWARD, T, H, V, dt), dev)
+    _check(lib().sao_loss_backward(
+        _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_head), _rows(w_head, "w_head"), _ptr(target),
+        _ptr(lse), _ptr(g), T, H, V, dt, _ptr(dhidden), _ptr(dw_head), _ptr(ws),
+        0 if ws is None else ws.numel(), _stream(dev)))
+    return dhidden, dw_head
+
+
+def time_kernel(kernel: int, start: Optional[torch.cuda.Event], stop: Optional[torch.cuda.Event]) -> None:
+    """Bracket the next launches of `kernel` with two timing events (None disables)."""
+    if start is None or stop is None:
+        lib().sao_debug_time_kernel(KERNEL_NONE, None, None)
+        return
+    lib().sao_debug_time_kernel(kernel, start.cuda_event, stop.cuda_event)

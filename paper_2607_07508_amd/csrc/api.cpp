@@ -1,0 +1,183 @@
+// C ABI of the SAO loss pass: host-side validation, workspace sizing, launch.
+// Every check below runs before any HIP call, so argument errors never touch the device.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+
+#include "../../include/sao.h"
+#include "launch.hpp"
+#include "layout.hpp"
+
+namespace {
+
+thread_local char g_msg[512] = "";
+
+sao_status_t fail(sao_status_t s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_msg, sizeof(g_msg), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+sao_status_t ok() {
+  g_msg[0] = '\0';
+  return SAO_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t esize_of(sao_dtype_t d) { return d == SAO_BF16 ? 2 : 4; }
+
+constexpr int64_t kMaxRows = (int64_t{1} << 31) - 1024;
+
+sao_status_t check_head(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w, int64_t T,
+                        int64_t H, int64_t V, sao_dtype_t dtype) {
+  if (dtype != SAO_BF16 && dtype != SAO_F32) return fail(SAO_ERR_DTYPE, "unknown dtype %d", (int)dtype);
+  if (T < 0 || T > kMaxRows) return fail(SAO_ERR_SHAPE, "T=%lld out of range", (long long)T);
+  if (H < 8 || H % 8 != 0) return fail(SAO_ERR_SHAPE, "H=%lld must be a positive multiple of 8", (long long)H);
+  if (V < 1 || V > kMaxRows) return fail(SAO_ERR_SHAPE, "V=%lld out of range", (long long)V);
+  if (ld_hidden < H || ld_hidden % 8 != 0)
+    return fail(SAO_ERR_SHAPE, "ld_hidden=%lld must be >= H and a multiple of 8", (long long)ld_hidden);
+  if (ld_w < H || ld_w % 8 != 0)
+    return fail(SAO_ERR_SHAPE, "ld_w=%lld must be >= H and a multiple of 8", (long long)ld_w);
+  if (!aligned16(hidden) || !aligned16(w_head))
+    return fail(SAO_ERR_SHAPE, "hidden and w_head must be 16-byte aligned");
+  return SAO_OK;
+}
+
+sao_status_t check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return SAO_OK;
+  if (!ws) return fail(SAO_ERR_NULL, "workspace of %zu bytes required", need);
+  if (ws_bytes < need) return fail(SAO_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, need);
+  if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return fail(SAO_ERR_WORKSPACE, "workspace not 256-byte aligned");
+  return SAO_OK;
+}
+
+sao_status_t device(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(SAO_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+namespace sao {
+KernelTimer& kernel_timer() {
+  thread_local KernelTimer t;
+  return t;
+}
+}  // namespace sao
+
+extern "C" {
+
+const char* sao_status_string(sao_status_t s) {
+  switch (s) {
+    case SAO_OK: return "ok";
+    case SAO_ERR_NULL: return "null pointer";
+    case SAO_ERR_SHAPE: return "bad shape";
+    case SAO_ERR_VALUE: return "bad value";
+    case SAO_ERR_DTYPE: return "bad dtype";
+    case SAO_ERR_WORKSPACE: return "workspace too small";
+    case SAO_ERR_DEVICE: return "device error";
+  }
+  return "unknown status";
+}
+
+const char* sao_last_error_message(void) { return g_msg; }
+
+const char* sao_version(void) { return "0.1.0"; }
+
+void sao_debug_time_kernel(int kernel, void* start_event, void* stop_event) {
+  sao::KernelTimer& t = sao::kernel_timer();
+  t.kernel = (start_event && stop_event) ? kernel : SAO_KERNEL_NONE;
+  t.start = static_cast<hipEvent_t>(start_event);
+  t.stop = static_cast<hipEvent_t>(stop_event);
+}
+
+size_t sao_workspace_size(sao_op_t op, int64_t T, int64_t H, int64_t V, sao_dtype_t dtype) {
+  if (T < 0 || (dtype != SAO_BF16 && dtype != SAO_F32)) return 0;
+  if (T == 0) return 0;
+  switch (op) {
+    case SAO_OP_LOGPROB:
+      if (H < 1 || V < 1) return 0;
+      return sao::logprob_layout(T, H, V, esize_of(dtype)).total;
+    case SAO_OP_BACKWARD:
+      if (H < 1 || V < 1) return 0;
+      return sao::backward_layout(T, H, V, esize_of(dtype)).total;
+    case SAO_OP_LOSS:
+      return sao::loss_layout(T).total;
+    case SAO_OP_ADVANTAGE:
+      return sao::kAdvantageWorkspace;
+    case SAO_OP_VALUE:
+      return 0;
+  }
+  return 0;
+}
+
+sao_status_t sao_token_logprob(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
+                               const int32_t* target, const uint8_t* mask, int64_t T, int64_t H, int64_t V,
+                               sao_dtype_t dtype, float* logp, float* lse, int32_t* status, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  if (!hidden || !w_head || !target || !logp || !lse)
+    return fail(SAO_ERR_NULL, "hidden, w_head, target, logp and lse are required");
+  if (sao_status_t s = check_head(hidden, ld_hidden, w_head, ld_w, T, H, V, dtype)) return s;
+  if (T == 0) return ok();
+  if (sao_status_t s = check_ws(ws, ws_bytes, sao_workspace_size(SAO_OP_LOGPROB, T, H, V, dtype))) return s;
+  return device(sao::launch_logprob(hidden, ld_hidden, w_head, ld_w, target, mask, T, H, V, dtype == SAO_BF16,
+                                    logp, lse, status, ws, stream),
+                "sao_token_logprob launch");
+}
+
+sao_status_t sao_advantage(const float* values, const float* rewards, const uint8_t* mask,
+                           const int32_t* cu_seqlens, int32_t B, int64_t T, double gamma, double lam,
+                           double alpha, float* adv, float* ret, int64_t* n_tokens, int32_t* status, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  if (!values || !rewards || !mask || !cu_seqlens || !adv || !ret)
+    return fail(SAO_ERR_NULL, "values, rewards, mask, cu_seqlens, adv and ret are required");
+  if (B < 1) return fail(SAO_ERR_SHAPE, "B=%d must be >= 1", (int)B);
+  if (T < 0 || T > kMaxRows) return fail(SAO_ERR_SHAPE, "T=%lld out of range", (long long)T);
+  if (!(gamma >= 0.0 && gamma <= 1.0)) return fail(SAO_ERR_VALUE, "gamma=%g outside [0,1]", gamma);
+  if (!(lam >= 0.0 && lam <= 1.0)) return fail(SAO_ERR_VALUE, "lam=%g outside [0,1]", lam);
+  if (!std::isfinite(alpha)) return fail(SAO_ERR_VALUE, "alpha must be finite");
+  if (T == 0) return ok();
+  if (sao_status_t s = check_ws(ws, ws_bytes, sao_workspace_size(SAO_OP_ADVANTAGE, T, 1, 1, SAO_F32))) return s;
+  return device(sao::launch_advantage(values, rewards, mask, cu_seqlens, B, T, gamma, lam, alpha, adv, ret,
+                                      n_tokens, status, ws, stream),
+                "sao_advantage launch");
+}
+
+sao_status_t sao_clipped_loss(const float* logp, const float* logp_rollout, const float* adv,
+                              const uint8_t* mask, int64_t T, float eps_low, float eps_high,
+                              const int64_t* n_tokens, double* loss, float* g, uint8_t* flags, int64_t* counts,
+                              void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!logp || !logp_rollout || !adv || !mask || !loss || !g || !flags || !counts)
+    return fail(SAO_ERR_NULL, "logp, logp_rollout, adv, mask, loss, g, flags and counts are required");
+  if (T < 0 || T > kMaxRows) return fail(SAO_ERR_SHAPE, "T=%lld out of range", (long long)T);
+  if (!(eps_low >= 0.0f) || !std::isfinite(eps_low) || !(eps_high >= 0.0f) || !std::isfinite(eps_high))
+    return fail(SAO_ERR_VALUE, "eps_low=%g, eps_high=%g must be finite and >= 0", eps_low, eps_high);
+  if (T == 0) return ok();
+  if (sao_status_t s = check_ws(ws, ws_bytes, sao_workspace_size(SAO_OP_LOSS, T, 1, 1, SAO_F32))) return s;
+  return device(sao::launch_loss(logp, logp_rollout, adv, mask, T, eps_low, eps_high, n_tokens, loss, g, flags,
+                                 counts, ws, stream),
+                "sao_clipped_loss launch");
+}
+
+sao_status_t sao_loss_backward(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
+                               const int32_t* target, const float* lse, const float* g, int64_t T, int64_t H,
+                               int64_t V, sao_dtype_t dtype, void* dhidden, float* dw_head, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  if (!hidden || !w_head || !target || !lse || !g || !dhidden || !dw_head)
+    return fail(SAO_ERR_NULL, "hidden, w_head, target, lse, g, dhidden and dw_head are required");
+  if (sao_status_t s = check_head(hidden, ld_hidden, w_head, ld_w, T, H, V, dtype)) return s;
+  if (!aligned16(dhidden) || !aligned16(dw_head))
+    return fail(SAO_ERR_SHAPE, "dhidden and dw_head must be 16-byte aligned");
+  if (T == 0) return ok();
+  if (sao_status_t s = check_ws(ws, ws_bytes, sao_workspace_size(SAO_OP_BACKWARD, T, H, V, dtype))) return s;
+  return device(sao::launch_backward(hidden, ld_hidden, w_head, ld_w, target, lse, g, T, H, V,
+                                     dtype == SAO_BF16, dhidden, dw_head, ws, stream),
+                "sao_loss_backward launch");
+}
+
+}  // extern "C"

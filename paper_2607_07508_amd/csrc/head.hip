@@ -1,0 +1,556 @@
+// LM-head kernels of the SAO loss pass: per-token log-probs (forward) and the
+// backward into hidden states and head weights, both on bf16 (or fp32) MFMA.
+//
+// Forward (Sec. 3.1, Eq. 1-2): rows with mask 1 are compacted, then
+//   z = W_head . h_t over 256 x 128 tiles (vocabulary x tokens); each tile is
+//   reduced in registers to a running (max, sum exp) per token, so the logits
+//   never leave the chip; partials over vocabulary groups are merged per token
+//   and the target logit z_{t,y_t} is a separate dot product.
+// Backward: rows with g != 0 are compacted; for each vocabulary block of Vc rows
+//   (A) recompute z and write dz = g (onehot - exp(z - lse)) to a [T x Vc] scratch,
+//   (B) dH += dz . W_block, (C) dW_block += dz^T . H, all on MFMA.
+#include "common.hpp"
+#include "gemm.hpp"
+#include "launch.hpp"
+#include "layout.hpp"
+#include "../../include/sao.h"
+
+namespace sao {
+
+// Compacted row buffers are zero-filled up to a multiple of this many rows.
+constexpr int64_t kRowPad = 256;
+
+// ------------------------------------------------------------------------- //
+// Row compaction
+// ------------------------------------------------------------------------- //
+__device__ __forceinline__ bool row_selected(const uint8_t* mask, const float* g, int64_t t) {
+  if (mask) return mask[t] != 0;
+  if (g) return g[t] != 0.0f;
+  return true;
+}
+
+template <typename T>
+__device__ __forceinline__ T block_sum_256(T v, T* sh) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) sh[wave] = v;
+  __syncthreads();
+  return sh[0] + sh[1] + sh[2] + sh[3];
+}
+
+__global__ __launch_bounds__(256) void k_count_rows(const uint8_t* mask, const float* g, int64_t T,
+                                                    int32_t* blk_counts) {
+  __shared__ int32_t sh[4];
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kRowsPerCountBlock + threadIdx.x * 4;
+  int32_t c = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t t = base + j;
+    if (t < T && row_selected(mask, g, t)) ++c;
+  }
+  c = block_sum_256(c, sh);
+  if (threadIdx.x == 0) blk_counts[blockIdx.x] = c;
+}
+
+// Writes idx[c] = t for the c-th selected row (ascending t), pos[t] = c or -1,
+// the total to *count, and zeroes zero_a[t], zero_b[t] on unselected rows.
+__global__ __launch_bounds__(256) void k_compact_rows(const uint8_t* mask, const float* g, int64_t T,
+                                                      const int32_t* blk_counts, int32_t* idx,
+                                                      int32_t* pos, int32_t* count, float* zero_a,
+                                                      float* zero_b) {
+  __shared__ int32_t sh[4];
+  __shared__ int32_t s_wave[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int32_t before = 0;
+  for (int i = tid; i < static_cast<int>(blockIdx.x); i += 256) before += blk_counts[i];
+  before = block_sum_256(before, sh);
+
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kRowsPerCountBlock + tid * 4;
+  bool sel[4];
+  int32_t c = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t t = base + j;
+    sel[j] = t < T && row_selected(mask, g, t);
+    c += sel[j] ? 1 : 0;
+  }
+  int32_t incl = c;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int32_t o = __shfl_up(incl, d, 64);
+    if (lane >= d) incl += o;
+  }
+  if (lane == 63) s_wave[wave] = incl;
+  __syncthreads();
+  int32_t woff = 0;
+  for (int w = 0; w < wave; ++w) woff += s_wave[w];
+  int32_t p = before + woff + incl - c;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t t = base + j;
+    if (t >= T) break;
+    if (sel[j]) {
+      idx[p] = static_cast<int32_t>(t);
+      if (pos) pos[t] = p;
+      ++p;
+    } else {
+      if (pos) pos[t] = -1;
+      if (zero_a) zero_a[t] = 0.0f;
+      if (zero_b) zero_b[t] = 0.0f;
+    }
+  }
+  if (blockIdx.x == gridDim.x - 1 && tid == 255) *count = p;
+}
+
+// Copies the selected rows into a dense [rows][H] buffer and zero-fills up to the
+// next multiple of 256 rows; gathers per-row extras alongside.
+template <class E>
+__global__ __launch_bounds__(256) void k_gather_rows(const typename E::storage* src, int64_t ld_src,
+                                                     int64_t H, const int32_t* idx,
+                                                     const int32_t* count,
+                                                     typename E::storage* dst,
+                                                     const int32_t* target, int32_t* y_c,
+                                                     const float* g, float* g_c, const float* lse,
+                                                     float* lse_c) {
+  const int lane = threadIdx.x & 63;
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  const int64_t n = *count;
+  if (c >= round_up_dev(n, kRowPad)) return;
+  const int64_t chunks = H / E::kPerChunk;
+  uint4* d = reinterpret_cast<uint4*>(dst + c * H);
+  if (c < n) {
+    const int64_t t = idx[c];
+    const uint4* s = reinterpret_cast<const uint4*>(src + t * ld_src);
+    for (int64_t k = lane; k < chunks; k += 64) d[k] = s[k];
+    if (lane == 0) {
+      if (y_c) y_c[c] = target[t];
+      if (g_c) g_c[c] = g[t];
+      if (lse_c) lse_c[c] = lse[t];
+    }
+  } else {
+    for (int64_t k = lane; k < chunks; k += 64) d[k] = zero4();
+    if (lane == 0) {
+      if (y_c) y_c[c] = -1;
+      if (g_c) g_c[c] = 0.0f;
+      if (lse_c) lse_c[c] = 0.0f;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------- //
+// Forward: online log-sum-exp epilogue
+// ------------------------------------------------------------------------- //
+struct EpiLse {
+  float2* part;   // [m_groups][ldp] running (max, sum exp) per token
+  int64_t ldp;
+  int64_t M;      // vocabulary size
+  float rm[kNI], rs[kNI];
+
+  __device__ __forceinline__ void begin(int64_t, int, int, int) {
+#pragma unroll
+    for (int i = 0; i < kNI; ++i) {
+      rm[i] = -__builtin_inff();
+      rs[i] = 0.0f;
+    }
+  }
+
+  __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t, int wm, int,
+                                       int lane) {
+    if (m0 + kBM > M) {
+#pragma unroll
+      for (int mi = 0; mi < kMI; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (m0 + acc_row(wm, mi, r, lane) >= M)
+#pragma unroll
+            for (int ni = 0; ni < kNI; ++ni) acc[mi][ni][r] = -__builtin_inff();
+    }
+#pragma unroll
+    for (int ni = 0; ni < kNI; ++ni) {
+      float tmax = -__builtin_inff();
+#pragma unroll
+      for (int mi = 0; mi < kMI; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc[mi][ni][r]);
+      const float mn = fmaxf(rm[ni], tmax);
+      if (mn == -__builtin_inff()) continue;
+      const float sc = mn * kLog2e;
+      float s = rs[ni] * fast_exp2(fmaf(rm[ni], kLog2e, -sc));
+#pragma unroll
+      for (int mi = 0; mi < kMI; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s += fast_exp2(fmaf(acc[mi][ni][r], kLog2e, -sc));
+      rm[ni] = mn;
+      rs[ni] = s;
+    }
+  }
+
+  __device__ __forceinline__ void finish(int mg, int64_t n0, int wm, int wn, int lane, void* smem) {
+#pragma unroll
+    for (int ni = 0; ni < kNI; ++ni) {
+      const float m2 = __shfl_xor(rm[ni], 32, 64);
+      const float s2 = __shfl_xor(rs[ni], 32, 64);
+      lse_merge(rm[ni], rs[ni], m2, s2);
+    }
+    float2* sh = static_cast<float2*>(smem);
+    __syncthreads();
+    if (wm == 1 && lane < 32)
+#pragma unroll
+      for (int ni = 0; ni < kNI; ++ni) sh[acc_col(wn, ni, lane)] = make_float2(rm[ni], rs[ni]);
+    __syncthreads();
+    if (wm == 0 && lane < 32) {
+#pragma unroll
+      for (int ni = 0; ni < kNI; ++ni) {
+        const float2 o = sh[acc_col(wn, ni, lane)];
+        lse_merge(rm[ni], rs[ni], o.x, o.y);
+        part[static_cast<int64_t>(mg) * ldp + n0 + acc_col(wn, ni, lane)] = make_float2(rm[ni], rs[ni]);
+      }
+    }
+  }
+};
+
+template <class E>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t V) {
+  __shared__ uint4 lds[2][kStageChunks];
+  EpiLse epi;
+  epi.part = part;
+  epi.ldp = ldp;
+  epi.M = V;
+  gemm_body<E, true, true>(s, epi, lds);
+}
+
+template <class E>
+__device__ __forceinline__ float dot_chunk(const uint4& a, const uint4& b);
+
+template <>
+__device__ __forceinline__ float dot_chunk<BF16>(const uint4& a, const uint4& b) {
+  const uint32_t* x = reinterpret_cast<const uint32_t*>(&a);
+  const uint32_t* y = reinterpret_cast<const uint32_t*>(&b);
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    s = fmaf(__uint_as_float(x[i] << 16), __uint_as_float(y[i] << 16), s);
+    s = fmaf(__uint_as_float(x[i] & 0xffff0000u), __uint_as_float(y[i] & 0xffff0000u), s);
+  }
+  return s;
+}
+
+template <>
+__device__ __forceinline__ float dot_chunk<F32>(const uint4& a, const uint4& b) {
+  float s = __uint_as_float(a.x) * __uint_as_float(b.x);
+  s = fmaf(__uint_as_float(a.y), __uint_as_float(b.y), s);
+  s = fmaf(__uint_as_float(a.z), __uint_as_float(b.z), s);
+  s = fmaf(__uint_as_float(a.w), __uint_as_float(b.w), s);
+  return s;
+}
+
+// One wave per compacted row: merge the vocabulary-group partials into lse, take
+// the target logit as a dot product, and write logp = z_y - lse at the row's position.
+template <class E>
+__global__ __launch_bounds__(256) void k_fwd_finalize(const float2* part, int64_t ldp, int m_groups,
+                                                      const typename E::storage* hc, int64_t H,
+                                                      const typename E::storage* w, int64_t ld_w,
+                                                      int64_t V, const int32_t* idx,
+                                                      const int32_t* target, const int32_t* count,
+                                                      float* logp, float* lse, int32_t* status) {
+  const int lane = threadIdx.x & 63;
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (c >= *count) return;
+  float m = -__builtin_inff(), s = 0.0f;
+  for (int gi = lane; gi < m_groups; gi += 64) {
+    const float2 p = part[static_cast<int64_t>(gi) * ldp + c];
+    lse_merge(m, s, p.x, p.y);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, 64);
+    const float s2 = __shfl_xor(s, o, 64);
+    lse_merge(m, s, m2, s2);
+  }
+  const int64_t t = idx[c];
+  const int32_t y = target[t];
+  const bool yok = y >= 0 && static_cast<int64_t>(y) < V;
+  float z = 0.0f;
+  if (yok) {
+    const uint4* hr = reinterpret_cast<const uint4*>(hc + c * H);
+    const uint4* wr = reinterpret_cast<const uint4*>(w + static_cast<int64_t>(y) * ld_w);
+    const int64_t chunks = H / E::kPerChunk;
+    for (int64_t k = lane; k < chunks; k += 64) z += dot_chunk<E>(hr[k], wr[k]);
+  }
+  z = wave_sum(z);
+  if (lane == 0) {
+    const float l = m + logf(s);
+    const bool finite = __builtin_isfinite(l);
+    if (status && !yok) atomicOr(status, SAO_STATUS_TARGET_RANGE);
+    if (status && !finite) atomicOr(status, SAO_STATUS_NONFINITE);
+    lse[t] = l;
+    logp[t] = yok ? z - l : __builtin_nanf("");
+  }
+}
+
+// ------------------------------------------------------------------------- //
+// Backward
+// ------------------------------------------------------------------------- //
+template <class E>
+__device__ __forceinline__ void store4(typename E::storage* p, const float (&d)[4]);
+
+template <>
+__device__ __forceinline__ void store4<BF16>(uint16_t* p, const float (&d)[4]) {
+  const uint32_t lo = static_cast<uint32_t>(f32_to_bf16(d[0])) | (static_cast<uint32_t>(f32_to_bf16(d[1])) << 16);
+  const uint32_t hi = static_cast<uint32_t>(f32_to_bf16(d[2])) | (static_cast<uint32_t>(f32_to_bf16(d[3])) << 16);
+  *reinterpret_cast<uint2*>(p) = make_uint2(lo, hi);
+}
+
+template <>
+__device__ __forceinline__ void store4<F32>(float* p, const float (&d)[4]) {
+  *reinterpret_cast<float4*>(p) = make_float4(d[0], d[1], d[2], d[3]);
+}
+
+// dz_{t,v} = g_t (1[v = y_t] - exp(z_{t,v} - lse_t)) for one vocabulary block,
+// stored token-major: dz[c][v - v0] (row stride ldz).
+template <class E>
+struct EpiDz {
+  typename E::storage* dz;
+  int64_t ldz;
+  int64_t m_valid;   // vocabulary rows of this block
+  int64_t v_base;    // vocabulary index of block row 0
+  const float* g_c;
+  const float* lse_c;
+  const int32_t* y_c;
+  float gl[kNI], ll[kNI];
+  int64_t yl[kNI];
+
+  __device__ __forceinline__ void begin(int64_t n0, int, int wn, int lane) {
+#pragma unroll
+    for (int ni = 0; ni < kNI; ++ni) {
+      const int64_t c = n0 + acc_col(wn, ni, lane);
+      gl[ni] = g_c[c];
+      ll[ni] = lse_c[c] * kLog2e;
+      yl[ni] = static_cast<int64_t>(y_c[c]) - v_base;
+    }
+  }
+
+  __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t n0, int wm, int wn,
+                                       int lane) {
+#pragma unroll
+    for (int ni = 0; ni < kNI; ++ni) {
+      typename E::storage* row = dz + (n0 + acc_col(wn, ni, lane)) * ldz;
+#pragma unroll
+      for (int mi = 0; mi < kMI; ++mi) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int64_t v = m0 + acc_row(wm, mi, 4 * j, lane);
+          float d[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float p = fast_exp2(fmaf(acc[mi][ni][4 * j + e], kLog2e, -ll[ni]));
+            const float oh = (v + e == yl[ni]) ? 1.0f : 0.0f;
+            d[e] = (v + e < m_valid) ? gl[ni] * (oh - p) : 0.0f;
+          }
+          store4<E>(row + v, d);
+        }
+      }
+    }
+  }
+
+  __device__ __forceinline__ void finish(int, int64_t, int, int, int, void*) {}
+};
+
+// out[m][n] += acc (fp32), rows < m_valid and columns < n_valid. Each element has
+// one writer per launch and launches on a stream are ordered, so the no-return
+// atomic add below is an ordinary deterministic accumulate that needs no
+// result registers.
+struct EpiAcc {
+  float* out;
+  int64_t ldo;
+  int64_t m_valid;
+  int64_t n_valid;
+
+  __device__ __forceinline__ void begin(int64_t, int, int, int) {}
+
+  __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t n0, int wm, int wn,
+                                       int lane) {
+#pragma unroll
+    for (int ni = 0; ni < kNI; ++ni) {
+      const int64_t n = n0 + acc_col(wn, ni, lane);
+      if (n >= n_valid) continue;
+#pragma unroll
+      for (int mi = 0; mi < kMI; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t m = m0 + acc_row(wm, mi, r, lane);
+          if (m < m_valid) unsafeAtomicAdd(out + m * ldo + n, acc[mi][ni][r]);
+        }
+    }
+  }
+
+  __device__ __forceinline__ void finish(int, int64_t, int, int, int, void*) {}
+};
+
+template <class E>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_bwd_dz(GemmShape s, EpiDz<E> epi) {
+  __shared__ uint4 lds[2][kStageChunks];
+  gemm_body<E, true, true>(s, epi, lds);
+}
+
+template <class E, bool AKC, bool BKC>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_bwd_acc(GemmShape s, EpiAcc epi) {
+  __shared__ uint4 lds[2][kStageChunks];
+  gemm_body<E, AKC, BKC>(s, epi, lds);
+}
+
+// Zero rows [0, round_up(*count, 256)) of a [rows][H] fp32 buffer.
+__global__ __launch_bounds__(256) void k_zero_rows(float* p, int64_t H, const int32_t* count) {
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (c >= round_up_dev(*count, kRowPad)) return;
+  float4* r = reinterpret_cast<float4*>(p + c * H);
+  for (int64_t k = threadIdx.x & 63; k < H / 4; k += 64) r[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+// dhidden[t] = dH[pos[t]] rounded to the element type, or zeros when pos[t] < 0.
+template <class E>
+__global__ __launch_bounds__(256) void k_dh_scatter(const float* dh, int64_t H, const int32_t* pos,
+                                                    int64_t T, typename E::storage* dhid) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const int32_t c = pos[t];
+  typename E::storage* out = dhid + t * H;
+  const float4* src = reinterpret_cast<const float4*>(dh + static_cast<int64_t>(c < 0 ? 0 : c) * H);
+  for (int64_t k = threadIdx.x & 63; k < H / 4; k += 64) {
+    float d[4] = {0.f, 0.f, 0.f, 0.f};
+    if (c >= 0) {
+      const float4 v = src[k];
+      d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+    }
+    store4<E>(out + 4 * k, d);
+  }
+}
+
+// ------------------------------------------------------------------------- //
+// Launchers
+// ------------------------------------------------------------------------- //
+static GemmShape make_shape(const void* a, int64_t lda, int64_t m, const void* b, int64_t ldb, int64_t n,
+                            int64_t k, int m_per_wg) {
+  GemmShape s{};
+  s.a = a; s.lda = lda; s.m = m;
+  s.b = b; s.ldb = ldb; s.n = n;
+  s.k = k;
+  s.m_tiles = static_cast<int>(ceil_div(m, kBM));
+  s.n_tiles = static_cast<int>(ceil_div(n, kBN));
+  s.m_per_wg = m_per_wg;
+  s.m_groups = static_cast<int>(ceil_div(s.m_tiles, m_per_wg));
+  s.sn = pick_sn(s.n_tiles);
+  return s;
+}
+
+template <class E>
+static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
+                               const int32_t* target, const uint8_t* mask, int64_t T, int64_t H,
+                               int64_t V, float* logp, float* lse, int32_t* status, void* ws,
+                               hipStream_t st) {
+  using S = typename E::storage;
+  const LogprobLayout L = logprob_layout(T, H, V, sizeof(S));
+  char* w8 = static_cast<char*>(ws);
+  int32_t* blk = reinterpret_cast<int32_t*>(w8 + L.blk_counts);
+  int32_t* count = reinterpret_cast<int32_t*>(w8 + L.count);
+  int32_t* idx = reinterpret_cast<int32_t*>(w8 + L.idx);
+  S* hc = reinterpret_cast<S*>(w8 + L.hc);
+  float2* part = reinterpret_cast<float2*>(w8 + L.part);
+
+  const int nb = static_cast<int>(L.n_count_blocks);
+  hipLaunchKernelGGL(k_count_rows, dim3(nb), dim3(256), 0, st, mask, nullptr, T, blk);
+  hipLaunchKernelGGL(k_compact_rows, dim3(nb), dim3(256), 0, st, mask, nullptr, T, blk, idx,
+                     nullptr, count, logp, lse);
+  const int rows4 = static_cast<int>(L.t_pad / 4);
+  hipLaunchKernelGGL(k_gather_rows<E>, dim3(rows4), dim3(256), 0, st, static_cast<const S*>(hidden),
+                     ld_hidden, H, idx, count, hc, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+  GemmShape s = make_shape(w_head, ld_w, V, hc, H, T, H, kFwdMTilesPerWg);
+  s.n_dev = count;
+  const KernelTimer& tm = kernel_timer();
+  const bool timed = tm.kernel == SAO_KERNEL_HEAD_FORWARD && tm.start && tm.stop;
+  if (timed) hipEventRecord(tm.start, st);
+  hipLaunchKernelGGL(k_head_fwd<E>, dim3(gemm_grid(s)), dim3(256), 0, st, s, part, L.t_pad, V);
+  if (timed) hipEventRecord(tm.stop, st);
+  hipLaunchKernelGGL(k_fwd_finalize<E>, dim3(rows4), dim3(256), 0, st, part, L.t_pad,
+                     static_cast<int>(L.m_groups), hc, H, static_cast<const S*>(w_head), ld_w, V, idx,
+                     target, count, logp, lse, status);
+  return hipGetLastError();
+}
+
+template <class E>
+static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
+                                const int32_t* target, const float* lse, const float* g, int64_t T,
+                                int64_t H, int64_t V, void* dhidden, float* dw, void* ws,
+                                hipStream_t st) {
+  using S = typename E::storage;
+  const BackwardLayout L = backward_layout(T, H, V, sizeof(S));
+  char* w8 = static_cast<char*>(ws);
+  int32_t* blk = reinterpret_cast<int32_t*>(w8 + L.blk_counts);
+  int32_t* count = reinterpret_cast<int32_t*>(w8 + L.count);
+  int32_t* idx = reinterpret_cast<int32_t*>(w8 + L.idx);
+  int32_t* pos = reinterpret_cast<int32_t*>(w8 + L.pos);
+  float* g_c = reinterpret_cast<float*>(w8 + L.g_c);
+  float* lse_c = reinterpret_cast<float*>(w8 + L.lse_c);
+  int32_t* y_c = reinterpret_cast<int32_t*>(w8 + L.y_c);
+  S* hg = reinterpret_cast<S*>(w8 + L.hg);
+  float* dh = reinterpret_cast<float*>(w8 + L.dh);
+  S* dz = reinterpret_cast<S*>(w8 + L.dz);
+  const S* w = static_cast<const S*>(w_head);
+
+  const int nb = static_cast<int>(L.n_count_blocks);
+  hipLaunchKernelGGL(k_count_rows, dim3(nb), dim3(256), 0, st, nullptr, g, T, blk);
+  hipLaunchKernelGGL(k_compact_rows, dim3(nb), dim3(256), 0, st, nullptr, g, T, blk, idx, pos, count,
+                     nullptr, nullptr);
+  const int rows4 = static_cast<int>(L.t_pad / 4);
+  hipLaunchKernelGGL(k_gather_rows<E>, dim3(rows4), dim3(256), 0, st, static_cast<const S*>(hidden),
+                     ld_hidden, H, idx, count, hg, target, y_c, g, g_c, lse, lse_c);
+  hipLaunchKernelGGL(k_zero_rows, dim3(rows4), dim3(256), 0, st, dh, H, count);
+
+  for (int64_t vb = 0; vb < L.n_vblocks; ++vb) {
+    const int64_t v0 = vb * L.vc;
+    const int64_t vlen = (V - v0) < L.vc ? (V - v0) : L.vc;
+    const S* wb = w + v0 * ld_w;
+    // (A) dz for this vocabulary block
+    GemmShape sa = make_shape(wb, ld_w, vlen, hg, H, T, H, 1);
+    sa.n_dev = count;
+    EpiDz<E> ez{dz, L.vc, vlen, v0, g_c, lse_c, y_c, {}, {}, {}};
+    hipLaunchKernelGGL(k_bwd_dz<E>, dim3(gemm_grid(sa)), dim3(256), 0, st, sa, ez);
+    // (B) dH[t][h] += sum_v dz[t][v] W[v0 + v][h]
+    GemmShape sb = make_shape(dz, L.vc, T, wb, ld_w, H, vlen, 1);
+    sb.m_dev = count;
+    EpiAcc eb{dh, H, L.t_pad, H};
+    hipLaunchKernelGGL((k_bwd_acc<E, true, false>), dim3(gemm_grid(sb)), dim3(256), 0, st, sb, eb);
+    // (C) dW[v0 + v][h] += sum_t dz[t][v] Hg[t][h]
+    GemmShape sc = make_shape(dz, L.vc, vlen, hg, H, H, T, 1);
+    sc.k_dev = count;
+    EpiAcc ec{dw + v0 * H, H, vlen, H};
+    hipLaunchKernelGGL((k_bwd_acc<E, false, false>), dim3(gemm_grid(sc)), dim3(256), 0, st, sc, ec);
+  }
+  const int t4 = static_cast<int>(ceil_div(T, 4));
+  hipLaunchKernelGGL(k_dh_scatter<E>, dim3(t4), dim3(256), 0, st, dh, H, pos, T, static_cast<S*>(dhidden));
+  return hipGetLastError();
+}
+
+hipError_t launch_logprob(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
+                          const int32_t* target, const uint8_t* mask, int64_t T, int64_t H, int64_t V,
+                          bool bf16, float* logp, float* lse, int32_t* status, void* ws, hipStream_t st) {
+  return bf16 ? logprob_impl<BF16>(hidden, ld_hidden, w_head, ld_w, target, mask, T, H, V, logp, lse,
+                                   status, ws, st)
+              : logprob_impl<F32>(hidden, ld_hidden, w_head, ld_w, target, mask, T, H, V, logp, lse,
+                                  status, ws, st);
+}
+
+hipError_t launch_backward(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
+                           const int32_t* target, const float* lse, const float* g, int64_t T, int64_t H,
+                           int64_t V, bool bf16, void* dhidden, float* dw, void* ws, hipStream_t st) {
+  return bf16 ? backward_impl<BF16>(hidden, ld_hidden, w_head, ld_w, target, lse, g, T, H, V, dhidden, dw,
+                                    ws, st)
+              : backward_impl<F32>(hidden, ld_hidden, w_head, ld_w, target, lse, g, T, H, V, dhidden, dw,
+                                   ws, st);
+}
+
+}  // namespace sao

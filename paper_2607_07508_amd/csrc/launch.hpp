@@ -1,0 +1,34 @@
+// Internal launch entry points behind the C ABI (device pointers, caller's stream).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sao {
+
+hipError_t launch_logprob(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
+                          const int32_t* target, const uint8_t* mask, int64_t T, int64_t H, int64_t V,
+                          bool bf16, float* logp, float* lse, int32_t* status, void* ws, hipStream_t st);
+
+hipError_t launch_backward(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
+                           const int32_t* target, const float* lse, const float* g, int64_t T, int64_t H,
+                           int64_t V, bool bf16, void* dhidden, float* dw, void* ws, hipStream_t st);
+
+hipError_t launch_advantage(const float* values, const float* rewards, const uint8_t* mask,
+                            const int32_t* cu_seqlens, int32_t B, int64_t T, double gamma, double lam,
+                            double alpha, float* adv, float* ret, int64_t* n_tokens, int32_t* status,
+                            void* ws, hipStream_t st);
+
+hipError_t launch_loss(const float* logp, const float* logp_rollout, const float* adv, const uint8_t* mask,
+                       int64_t T, float eps_low, float eps_high, const int64_t* n_tokens, double* loss,
+                       float* g, uint8_t* flags, int64_t* counts, void* ws, hipStream_t st);
+
+// Thread-local measurement hook (see sao_debug_time_kernel).
+struct KernelTimer {
+  int kernel = 0;
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+KernelTimer& kernel_timer();
+
+}  // namespace sao

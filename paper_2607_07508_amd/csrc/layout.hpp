@@ -1,0 +1,103 @@
+// Host-side workspace layouts shared by sao_workspace_size and the launchers.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sao {
+
+constexpr int64_t kTile = 256;
+constexpr int64_t kRowsPerCountBlock = 1024;  // rows per block of the compaction count
+constexpr int kFwdMTilesPerWg = 8;            // vocabulary tiles one forward workgroup walks
+constexpr int64_t kVocabBlock = 16384;        // vocabulary rows per backward dZ block
+constexpr int kLossThreads = 256;
+constexpr int kLossPerThread = 8;
+constexpr int kLossMaxBlocks = 2048;
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
+inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+struct Carve {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    const size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  }
+};
+
+// sao_token_logprob
+struct LogprobLayout {
+  int64_t t_pad, n_count_blocks, m_tiles, m_groups;
+  size_t blk_counts, count, idx, hc, part, total;
+};
+
+inline LogprobLayout logprob_layout(int64_t T, int64_t H, int64_t V, size_t esize) {
+  LogprobLayout L{};
+  L.t_pad = round_up(T, kTile);
+  L.n_count_blocks = ceil_div(T, kRowsPerCountBlock);
+  L.m_tiles = ceil_div(V, kTile);
+  L.m_groups = ceil_div(L.m_tiles, kFwdMTilesPerWg);
+  Carve c;
+  L.blk_counts = c.take(4 * static_cast<size_t>(L.n_count_blocks));
+  L.count = c.take(4);
+  L.idx = c.take(4 * static_cast<size_t>(L.t_pad));
+  L.hc = c.take(esize * static_cast<size_t>(L.t_pad) * static_cast<size_t>(H));
+  L.part = c.take(8 * static_cast<size_t>(L.m_groups) * static_cast<size_t>(L.t_pad));
+  L.total = c.off;
+  return L;
+}
+
+// sao_loss_backward
+struct BackwardLayout {
+  int64_t t_pad, n_count_blocks, vc, n_vblocks;
+  size_t blk_counts, count, idx, pos, g_c, lse_c, y_c, hg, dh, dz, total;
+};
+
+inline BackwardLayout backward_layout(int64_t T, int64_t H, int64_t V, size_t esize) {
+  BackwardLayout L{};
+  L.t_pad = round_up(T, kTile);
+  L.n_count_blocks = ceil_div(T, kRowsPerCountBlock);
+  L.vc = round_up(V, kTile) < kVocabBlock ? round_up(V, kTile) : kVocabBlock;
+  L.n_vblocks = ceil_div(V, L.vc);
+  Carve c;
+  const size_t tp = static_cast<size_t>(L.t_pad);
+  L.blk_counts = c.take(4 * static_cast<size_t>(L.n_count_blocks));
+  L.count = c.take(4);
+  L.idx = c.take(4 * tp);
+  L.pos = c.take(4 * static_cast<size_t>(T));
+  L.g_c = c.take(4 * tp);
+  L.lse_c = c.take(4 * tp);
+  L.y_c = c.take(4 * tp);
+  L.hg = c.take(esize * tp * static_cast<size_t>(H));
+  L.dh = c.take(4 * tp * static_cast<size_t>(H));
+  L.dz = c.take(esize * tp * static_cast<size_t>(L.vc));
+  L.total = c.off;
+  return L;
+}
+
+// sao_advantage: one int32 flag (segments malformed)
+constexpr size_t kAdvantageWorkspace = 256;
+
+// sao_clipped_loss
+struct LossLayout {
+  int64_t blocks;
+  size_t part_f, part_i, n_count, total;
+};
+
+inline LossLayout loss_layout(int64_t T) {
+  LossLayout L{};
+  int64_t blocks = ceil_div(T, static_cast<int64_t>(kLossThreads) * kLossPerThread);
+  if (blocks > kLossMaxBlocks) blocks = kLossMaxBlocks;
+  if (blocks < 1) blocks = 1;
+  L.blocks = blocks;
+  Carve c;
+  L.part_f = c.take(16 * static_cast<size_t>(blocks));   // two doubles per block
+  L.part_i = c.take(40 * static_cast<size_t>(blocks));   // five int64 per block
+  L.n_count = c.take(8);
+  L.total = c.off;
+  return L;
+}
+
+}  // namespace sao

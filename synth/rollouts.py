@@ -120,17 +120,25 @@ class Batch:
 
 
 def bf16_round(x: np.ndarray) -> np.ndarray:
-    """Round float32 values to the nearest bfloat16 (ties to even); returns float32."""
+    """Round float32 values to the nearest bfloat16 (ties to even); returns float32.
+
+    Finite inputs only: for them the 32-bit sum below cannot wrap.
+    """
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32)
-    out = np.empty_like(u)
-    step = 1 << 22
-    flat_u, flat_o = u.reshape(-1), out.reshape(-1)
-    for s in range(0, flat_u.size, step):
-        v = flat_u[s:s + step].astype(np.uint64)
-        v = (v + 0x7FFF + ((v >> 16) & 1)) & 0xFFFF0000
-        flat_o[s:s + step] = v.astype(np.uint32)
-    return out.view(np.float32)
+    out = np.empty_like(x)
+    flat_x, flat_o = x.reshape(-1).view(np.uint32), out.reshape(-1).view(np.uint32)
+    step = 1 << 20
+    lsb = np.empty(min(step, flat_x.size), dtype=np.uint32)
+    for s in range(0, flat_x.size, step):
+        v = flat_x[s:s + step]
+        o = flat_o[s:s + step]
+        b = lsb[:v.size]
+        np.right_shift(v, 16, out=b)
+        np.bitwise_and(b, 1, out=b)
+        np.add(v, 0x7FFF, out=o)
+        np.add(o, b, out=o)
+        np.bitwise_and(o, 0xFFFF0000, out=o)
+    return out
 
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:

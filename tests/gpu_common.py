@@ -1,0 +1,117 @@
+"""Shared helpers of the GPU parity tests: run the HIP path and the oracle, compare.
+
+Tolerances (the GPU side computes in fp32 from bf16/fp32 inputs; the oracle in fp64):
+  log-probs and lse: max abs <= 2e-3 (expected ~1e-5)
+  flags, counts, N: bit-exact (the drift noise keeps every ratio >= 4e-3 in
+      log space from a band edge, far beyond the ~1e-5 log-prob error)
+  loss values: |d| <= 1e-3 * max(|ref|, (1/N) sum |terms|)
+  g: |d| <= 1e-3 * |ref| + 1e-12 (g = -rho A / N inherits the log-prob error ~1e-5)
+  advantages/returns: |d| <= 1e-6 * max(1, |ref|) (fp64 inside, rounded to fp32)
+  dH, dW: Frobenius relative <= 1e-2, per-row relative <= 1e-2 on rows whose norm
+      exceeds 1e-3 of the largest row, rows with g = 0 exactly zero
+"""
+from __future__ import annotations
+
+import sys
+import time
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2607_07508_amd as sao
+from synth import rollout_logprobs
+from synth.device import to_device
+
+TOL_LOGP = 2e-3
+TOL_LOSS = 1e-3
+TOL_G = 1e-3
+TOL_ADV = 1e-6
+TOL_GRAD = 1e-2
+
+
+def say(msg: str) -> None:
+    print(f"[{time.strftime('%H:%M:%S')}] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def gpu_pass(batch, ref_logp, gamma, lam, alpha, backward=True, n_tokens_global=True):
+    """The whole hot path on the GPU through the C ABI; returns host numpy results."""
+    cfg = batch.cfg
+    db = to_device(batch, ref_logp)
+    logp, lse = sao.token_logprob(db.hidden, db.w_head, db.target, db.mask)
+    adv, ret, n_tok = sao.advantage(db.values, db.rewards, db.mask, db.cu_seqlens, gamma, lam, alpha)
+    loss, g, flags, counts = sao.clipped_loss(logp, db.logp_rollout, adv, db.mask, cfg.eps_low, cfg.eps_high,
+                                              n_tok if n_tokens_global else None)
+    out = dict(logp=logp, lse=lse, adv=adv, ret=ret, n=n_tok, loss=loss, g=g, flags=flags, counts=counts)
+    if backward:
+        dh, dw = sao.loss_backward(db.hidden, db.w_head, db.target, lse, g)
+        out.update(dh=dh, dw=dw)
+    torch.cuda.synchronize()
+    res = {}
+    for k, v in out.items():
+        if v.dtype == torch.bfloat16:
+            v = v.float()
+        res[k] = v.cpu().numpy()
+    return res
+
+
+def oracle_pass(batch, gamma, lam, alpha, backward=True):
+    cfg = batch.cfg
+    lp, lse = oracle.token_logprob(batch.hidden, batch.w_head, batch.target, batch.mask)
+    adv, ret, N = oracle.advantage(batch.values, batch.rewards, batch.mask, batch.cu_seqlens, gamma, lam, alpha)
+    lro = rollout_logprobs(lp, batch.xi)
+    loss, g, flags, counts = oracle.dis_loss(lp, lro, adv, batch.mask, cfg.eps_low, cfg.eps_high, N)
+    res = dict(logp=lp, lse=lse, adv=adv, ret=ret, n=N, loss=loss, g=g, flags=flags, counts=counts, lro=lro)
+    if backward:
+        dh, dw = oracle.loss_backward(batch.hidden, batch.w_head, batch.target, lse, g)
+        res.update(dh=dh, dw=dw)
+    return res
+
+
+def check_loss(got, ref, lp, lro, adv, mask, N):
+    """Loss values against the oracle, guarded against cancellation."""
+    rho = np.exp(lp - lro)
+    used = (ref["flags"] == 1)
+    scale0 = np.abs(rho * adv * lp)[used].sum() / max(N, 1)
+    scale1 = np.abs(rho * adv)[used].sum() / max(N, 1)
+    for k, sc in ((0, scale0), (1, scale1)):
+        tol = TOL_LOSS * max(abs(ref["loss"][k]), sc, 1e-300)
+        assert abs(got["loss"][k] - ref["loss"][k]) <= tol, (k, got["loss"][k], ref["loss"][k], tol)
+
+
+def check_grad(got, ref, rows_zero=None, name="grad"):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    nr = np.linalg.norm(ref)
+    if nr == 0:
+        assert np.abs(got).max() == 0, name
+        return
+    assert np.linalg.norm(got - ref) <= TOL_GRAD * nr, (name, np.linalg.norm(got - ref) / nr)
+    rn = np.linalg.norm(ref, axis=1)
+    big = rn > 1e-3 * rn.max()
+    rel = np.linalg.norm(got - ref, axis=1)[big] / rn[big]
+    assert rel.max() <= TOL_GRAD, (name, rel.max())
+    if rows_zero is not None:
+        assert (got[rows_zero] == 0).all(), name
+
+
+def compare_all(got, ref, batch, backward=True):
+    m = batch.mask == 1
+    assert np.abs(got["logp"][m] - ref["logp"][m]).max() <= TOL_LOGP
+    assert np.abs(got["lse"][m] - ref["lse"][m]).max() <= TOL_LOGP
+    assert (got["logp"][~m] == 0).all() and (got["lse"][~m] == 0).all()
+    assert int(got["n"][0]) == ref["n"]
+    scale = np.maximum(1.0, np.abs(ref["adv"]))
+    assert (np.abs(got["adv"] - ref["adv"]) <= TOL_ADV * scale).all()
+    scale = np.maximum(1.0, np.abs(ref["ret"]))
+    assert (np.abs(got["ret"] - ref["ret"]) <= TOL_ADV * scale).all()
+    assert np.array_equal(got["flags"], ref["flags"])
+    assert np.array_equal(got["counts"], ref["counts"])
+    check_loss(got, ref, ref["logp"], ref["lro"], ref["adv"], batch.mask, ref["n"])
+    assert (np.abs(got["g"] - ref["g"]) <= TOL_G * np.abs(ref["g"]) + 1e-12).all()
+    assert (got["g"][ref["flags"] != 1] == 0).all()
+    if backward:
+        zero_rows = np.nonzero(ref["g"] == 0)[0]
+        check_grad(got["dh"], ref["dh"], zero_rows, "dhidden")
+        check_grad(got["dw"], ref["dw"], None, "dw_head")

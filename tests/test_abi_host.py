@@ -1,0 +1,122 @@
+"""The C ABI on the host: the library loads, exports what include/sao.h declares,
+and rejects invalid arguments synchronously before any device work.
+
+No call here reaches a kernel launch: every case fails validation or is the
+T == 0 no-op, so the pointers passed are never dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_07508_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sao.h")
+
+OK, ERR_NULL, ERR_SHAPE, ERR_VALUE, ERR_DTYPE, ERR_WORKSPACE = 0, 1, 2, 3, 4, 5
+FAKE = 0x10000          # 16- and 256-byte aligned, never dereferenced
+FAKE_ODD = 0x10008      # 8 mod 16
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(sao_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(binding.LIB_PATH):
+        pytest.skip("libsao.so not built")
+    return binding.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert set(names) >= {"sao_token_logprob", "sao_advantage", "sao_clipped_loss", "sao_loss_backward"}
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(binding.EXPORTS)
+
+
+def test_version_and_strings(L):
+    assert L.sao_version().decode().count(".") == 2
+    for code in range(7):
+        assert L.sao_status_string(code)
+
+
+def logprob(L, hidden=FAKE, ldh=64, w=FAKE, ldw=64, tgt=FAKE, mask=None, T=16, H=64, V=1000, dt=0,
+            logp=FAKE, lse=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    return L.sao_token_logprob(hidden, ldh, w, ldw, tgt, mask, T, H, V, dt, logp, lse, None, ws, ws_bytes, None)
+
+
+def test_logprob_validation(L):
+    assert logprob(L, hidden=None) == ERR_NULL
+    assert logprob(L, lse=None) == ERR_NULL
+    assert logprob(L, T=-1) == ERR_SHAPE
+    assert logprob(L, H=12, ldh=16, ldw=16) == ERR_SHAPE            # H not a multiple of 8
+    assert logprob(L, V=0) == ERR_SHAPE
+    assert logprob(L, ldh=32) == ERR_SHAPE                          # ld < H
+    assert logprob(L, ldw=68) == ERR_SHAPE                          # ld not a multiple of 8
+    assert logprob(L, hidden=FAKE_ODD) == ERR_SHAPE                 # misaligned
+    assert logprob(L, dt=7) == ERR_DTYPE
+    assert logprob(L, ws_bytes=16) == ERR_WORKSPACE
+    assert logprob(L, ws=None) == ERR_NULL
+    assert logprob(L, ws=FAKE + 16) == ERR_WORKSPACE               # not 256-byte aligned
+    assert logprob(L, T=0) == OK                                    # no-op
+    assert b"workspace" in L.sao_last_error_message() or L.sao_last_error_message() == b""
+
+
+def test_advantage_validation(L):
+    def adv(vals=FAKE, B=2, T=10, gamma=1.0, lam=1.0, alpha=0.0, adv_out=FAKE, ws=FAKE, ws_bytes=256):
+        return L.sao_advantage(vals, FAKE, FAKE, FAKE, B, T, gamma, lam, alpha, adv_out, FAKE, None, None,
+                               ws, ws_bytes, None)
+    assert adv(vals=None) == ERR_NULL
+    assert adv(adv_out=None) == ERR_NULL
+    assert adv(B=0) == ERR_SHAPE
+    assert adv(T=-3) == ERR_SHAPE
+    assert adv(gamma=1.5) == ERR_VALUE
+    assert adv(gamma=float("nan")) == ERR_VALUE
+    assert adv(lam=-0.1) == ERR_VALUE
+    assert adv(alpha=float("inf")) == ERR_VALUE
+    assert adv(ws=None) == ERR_NULL
+    assert adv(ws_bytes=4) == ERR_WORKSPACE
+    assert adv(T=0) == OK
+
+
+def test_loss_validation(L):
+    def loss(T=10, el=0.2, eh=0.2, g=FAKE, ws=FAKE, ws_bytes=1 << 30):
+        return L.sao_clipped_loss(FAKE, FAKE, FAKE, FAKE, T, el, eh, None, FAKE, g, FAKE, FAKE, ws, ws_bytes,
+                                  None)
+    assert loss(g=None) == ERR_NULL
+    assert loss(el=-0.1) == ERR_VALUE
+    assert loss(eh=float("inf")) == ERR_VALUE
+    assert loss(eh=float("nan")) == ERR_VALUE
+    assert loss(ws_bytes=8) == ERR_WORKSPACE
+    assert loss(T=0) == OK
+
+
+def test_backward_validation(L):
+    def bwd(dh=FAKE, dw=FAKE, T=16, H=64, V=100, dt=0, ws_bytes=1 << 40):
+        return L.sao_loss_backward(FAKE, H, FAKE, H, FAKE, FAKE, FAKE, T, H, V, dt, dh, dw, FAKE, ws_bytes,
+                                   None)
+    assert bwd(dh=None) == ERR_NULL
+    assert bwd(dw=FAKE_ODD) == ERR_SHAPE
+    assert bwd(H=0) == ERR_SHAPE
+    assert bwd(dt=2) == ERR_DTYPE
+    assert bwd(ws_bytes=100) == ERR_WORKSPACE
+    assert bwd(T=0) == OK
+
+
+def test_workspace_sizes(L):
+    ws = binding.workspace_size
+    assert ws(binding.OP_ADVANTAGE, 1000, 1, 1, 0) == 256
+    assert ws(binding.OP_LOGPROB, 0, 2048, 151936, 0) == 0
+    assert ws(binding.OP_LOGPROB, -1, 2048, 151936, 0) == 0
+    small = ws(binding.OP_LOGPROB, 1000, 64, 1000, 1)
+    assert small > 1000 * 64 * 4
+    # the backward dz scratch is one vocabulary block, not T x V
+    big = ws(binding.OP_BACKWARD, 65536, 2048, 151936, 0)
+    assert big < 65536 * 151936 * 2 // 4
+    assert ws(binding.OP_LOSS, 1 << 26, 1, 1, 1) < 1 << 20

@@ -1,0 +1,76 @@
+"""Full-size parity in the launch configuration the benchmark times.
+
+Log-probs and lse are compared on every loss-mask row against the oracle values
+stored by tests/golden/make_full_logprobs.py; advantages, flags, counts, loss
+and g on every token (the oracle scan and loss are cheap); dhidden and dW_head
+on sampled rows that the oracle computes one by one, plus exact zeros on every
+row with g = 0.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import CONFIGS, generate, rollout_logprobs
+from tests.gpu_common import TOL_ADV, TOL_G, TOL_LOGP, check_grad, check_loss, gpu_pass, say
+from tests.golden.make_full_logprobs import load as load_golden, path_for
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+
+
+def _full(name, backward, n_rows=24, seed=0):
+    cfg = CONFIGS[name]
+    say(f"{name}: generating T={cfg.T} H={cfg.H} V={cfg.V}")
+    b = generate(cfg)
+    ref_lp, ref_lse = load_golden(name, b)
+    say(f"{name}: GPU pass")
+    got = gpu_pass(b, ref_lp, cfg.gamma, cfg.lam, cfg.alpha, backward)
+    m = b.mask == 1
+    say(f"{name}: compare logp on {int(m.sum())} rows")
+    assert np.abs(got["logp"][m] - ref_lp[m]).max() <= TOL_LOGP
+    assert np.abs(got["lse"][m] - ref_lse[m]).max() <= TOL_LOGP
+    assert (got["logp"][~m] == 0).all()
+    adv, ret, N = oracle.advantage(b.values, b.rewards, b.mask, b.cu_seqlens, cfg.gamma, cfg.lam, cfg.alpha)
+    assert int(got["n"][0]) == N
+    assert (np.abs(got["adv"] - adv) <= TOL_ADV * np.maximum(1, np.abs(adv))).all()
+    assert (np.abs(got["ret"] - ret) <= TOL_ADV * np.maximum(1, np.abs(ret))).all()
+    lro = rollout_logprobs(ref_lp, b.xi)
+    loss, g, flags, counts = oracle.dis_loss(ref_lp, lro, adv, b.mask, cfg.eps_low, cfg.eps_high, N)
+    assert np.array_equal(got["flags"], flags)
+    assert np.array_equal(got["counts"], counts)
+    check_loss(got, dict(loss=loss, flags=flags), ref_lp, lro, adv, b.mask, N)
+    assert (np.abs(got["g"] - g) <= TOL_G * np.abs(g) + 1e-12).all()
+    say(f"{name}: forward ok, clipped {counts[2] + counts[3]} of {counts[0]}")
+    if not backward:
+        return
+    rng = np.random.default_rng(seed)
+    live = np.nonzero(g)[0]
+    rows = np.sort(rng.choice(live, size=n_rows, replace=False))
+    vrows = np.unique(np.concatenate([b.target[rows[:n_rows // 2]], rng.choice(cfg.V, n_rows, replace=False),
+                                      [0, cfg.V - 1]]))
+    say(f"{name}: oracle backward on {rows.size} token rows and {vrows.size} vocabulary rows")
+    w64 = b.w_head.astype(np.float64)
+    dH, dW = oracle.loss_backward(b.hidden, None, b.target, ref_lse, g, dh_rows=rows, dw_rows=vrows, w64=w64)
+    check_grad(got["dh"][rows], dH[rows], None, "dhidden rows")
+    assert (got["dh"][g == 0] == 0).all()
+    check_grad(got["dw"][vrows], dW[vrows], None, "dw_head rows")
+    # the vocabulary sum of dz is 0 for every token, so sum_v dW_v = 0 up to rounding
+    col = got["dw"].astype(np.float64).sum(axis=0)
+    assert np.abs(col).max() <= 1e-2 * np.abs(got["dw"]).sum(axis=0).max()
+    say(f"{name}: backward ok")
+
+
+@pytest.mark.skipif(not __import__("os").path.exists(path_for("c2")), reason="stored oracle values missing")
+def test_c2_full_forward_backward():
+    _full("c2", backward=True)
+
+
+@pytest.mark.skipif(not __import__("os").path.exists(path_for("c1")), reason="stored oracle values missing")
+def test_c1_full_forward():
+    _full("c1", backward=False)

@@ -1,0 +1,162 @@
+"""GPU parity of the whole hot path (through the C ABI) against the fp64 oracle.
+
+Sizes span several tiles with ragged tails, several vocabulary blocks of the
+backward, fp32 and bf16, and the degenerate cases (single token, all masked,
+minimum H, target out of range, malformed segments).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_07508_amd as sao
+from synth import CONFIGS, generate, rollout_logprobs, small_config, with_overrides
+from synth.device import to_device
+from tests.gpu_common import (TOL_LOGP, check_grad, compare_all, gpu_pass, oracle_pass, say)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    sao.lib()
+
+
+def _roundtrip(cfg, gamma=1.0, lam=1.0, alpha=0.0, backward=True):
+    say(f"case {cfg.name}: T={cfg.T} H={cfg.H} V={cfg.V} {cfg.dtype} gamma={gamma} lam={lam} alpha={alpha}")
+    b = generate(cfg)
+    ref = oracle_pass(b, gamma, lam, alpha, backward)
+    got = gpu_pass(b, ref["logp"], gamma, lam, alpha, backward)
+    compare_all(got, ref, b, backward)
+    say(f"case {cfg.name}: ok (clipped {ref['counts'][2] + ref['counts'][3]} of {ref['counts'][0]})")
+    return got, ref
+
+
+def test_c0_fp32_fixed_lambda():
+    _roundtrip(CONFIGS["c0"], 1.0, 1.0, 0.0)
+
+
+def test_c0_fp32_length_adaptive():
+    _roundtrip(CONFIGS["c0"], 1.0, 1.0, 1.5)
+
+
+def test_c0_as_bf16():
+    _roundtrip(with_overrides(CONFIGS["c0"], name="c0-bf16", dtype="bf16"), 0.99, 0.95, 0.0)
+
+
+@pytest.mark.parametrize("case", [
+    dict(name="m1", seed=11, B=5, T=700, H=192, V=2000),            # 8 vocab tiles, ragged tails
+    dict(name="m2", seed=12, B=3, T=300, H=64, V=1001),             # V not a multiple of 8
+    dict(name="m3", seed=13, B=4, T=640, H=64, V=40000),            # three backward vocab blocks
+    dict(name="m4", seed=14, B=2, T=50, H=8, V=300),                # minimum H
+    dict(name="m5", seed=15, B=6, T=1100, H=320, V=520, dtype="f32"),
+])
+def test_mid_sizes(case):
+    cfg = small_config(**case)
+    _roundtrip(cfg, 1.0, 1.0, 1.5)
+
+
+def test_single_token():
+    cfg = small_config("one", 21, B=1, T=1, H=16, V=77, act_span=(1, 1), obs_span=(1, 1))
+    _roundtrip(cfg)
+
+
+def test_peaked_logits():
+    # hidden and W ~ N(0, 1) at H = 64: logits of std 8, near one-hot softmax
+    cfg = small_config("peaked", 22, B=3, T=400, H=64, V=3000, init_std=1.0, dtype="f32")
+    _roundtrip(cfg, 0.99, 0.9)
+    cfg = small_config("peaked-bf16", 23, B=3, T=400, H=64, V=3000, init_std=1.0)
+    _roundtrip(cfg, 0.99, 0.9)
+
+
+def test_all_masked_and_zero_gradient():
+    b = generate(small_config("masked", 24, B=2, T=300, H=64, V=500))
+    b.mask[:] = 0
+    db = to_device(b, np.zeros(b.T))
+    logp, lse = sao.token_logprob(db.hidden, db.w_head, db.target, db.mask)
+    adv, ret, n = sao.advantage(db.values, db.rewards, db.mask, db.cu_seqlens, 1.0, 1.0, 0.0)
+    loss, g, flags, counts = sao.clipped_loss(logp, db.logp_rollout, adv, db.mask, 0.2, 0.2, n)
+    dw0 = torch.full((b.cfg.V, b.cfg.H), 0.5, dtype=torch.float32, device="cuda")
+    dh, dw = sao.loss_backward(db.hidden, db.w_head, db.target, lse, g, dw_head=dw0)
+    torch.cuda.synchronize()
+    assert (logp == 0).all() and (lse == 0).all() and (adv == 0).all() and int(n) == 0
+    assert (loss == 0).all() and (counts == 0).all() and (g == 0).all() and (flags == 0).all()
+    assert (dh == 0).all() and (dw == 0.5).all()
+
+
+def test_accumulation_and_determinism():
+    b = generate(small_config("acc", 25, B=4, T=900, H=128, V=1500))
+    ref = oracle_pass(b, 1.0, 1.0, 1.5)
+    db = to_device(b, ref["logp"])
+    runs = []
+    for _ in range(2):
+        logp, lse = sao.token_logprob(db.hidden, db.w_head, db.target, db.mask)
+        adv, ret, n = sao.advantage(db.values, db.rewards, db.mask, db.cu_seqlens, 1.0, 1.0, 1.5)
+        loss, g, flags, counts = sao.clipped_loss(logp, db.logp_rollout, adv, db.mask, 0.2, 0.2, n)
+        # a second call accumulates into loss / counts
+        sao.clipped_loss(logp, db.logp_rollout, adv, db.mask, 0.2, 0.2, n, loss=loss, counts=counts)
+        dh, dw = sao.loss_backward(db.hidden, db.w_head, db.target, lse, g)
+        sao.loss_backward(db.hidden, db.w_head, db.target, lse, g, dw_head=dw)
+        torch.cuda.synchronize()
+        runs.append([x.cpu().float().numpy() for x in (logp, loss, flags, counts, dh, dw)])
+    for a, c in zip(runs[0], runs[1]):
+        assert np.array_equal(a, c)
+    logp, loss, flags, counts, dh, dw = runs[0]
+    assert np.array_equal(counts, 2 * ref["counts"])
+    assert np.allclose(loss, 2 * ref["loss"], rtol=1e-3, atol=0)
+    check_grad(dw, 2 * ref["dw"], None, "dw x2")
+
+
+def test_chunked_equals_whole():
+    """Token chunks with the global N: losses, counts and dW sum to the whole-batch values."""
+    b = generate(small_config("chunks", 26, B=3, T=1200, H=64, V=900))
+    ref = oracle_pass(b, 1.0, 1.0, 1.5)
+    db = to_device(b, ref["logp"])
+    adv, ret, n = sao.advantage(db.values, db.rewards, db.mask, db.cu_seqlens, 1.0, 1.0, 1.5)
+    loss = torch.zeros(2, dtype=torch.float64, device="cuda")
+    counts = torch.zeros(5, dtype=torch.int64, device="cuda")
+    dw = torch.zeros((b.cfg.V, b.cfg.H), dtype=torch.float32, device="cuda")
+    dh = torch.empty_like(db.hidden)
+    for s in range(0, b.T, 256):
+        e = min(s + 256, b.T)
+        lp, lse = sao.token_logprob(db.hidden[s:e], db.w_head, db.target[s:e], db.mask[s:e])
+        _, g, _, _ = sao.clipped_loss(lp, db.logp_rollout[s:e], adv[s:e], db.mask[s:e], 0.2, 0.2, n,
+                                      loss=loss, counts=counts)
+        sao.loss_backward(db.hidden[s:e], db.w_head, db.target[s:e], lse, g, dw_head=dw, dhidden=dh[s:e])
+    torch.cuda.synchronize()
+    assert np.array_equal(counts.cpu().numpy(), ref["counts"])
+    assert np.allclose(loss.cpu().numpy(), ref["loss"], rtol=1e-3, atol=1e-12)
+    check_grad(dw.cpu().numpy(), ref["dw"], None, "chunked dw")
+    check_grad(dh.float().cpu().numpy(), ref["dh"], np.nonzero(ref["g"] == 0)[0], "chunked dh")
+
+
+def test_target_out_of_range_sets_status():
+    b = generate(small_config("badtgt", 27, B=2, T=200, H=64, V=400))
+    t_bad = int(np.nonzero(b.mask)[0][3])
+    b.target[t_bad] = b.cfg.V
+    db = to_device(b)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    logp, lse = sao.token_logprob(db.hidden, db.w_head, db.target, db.mask, status=status)
+    torch.cuda.synchronize()
+    assert int(status) & sao.binding.STATUS_TARGET_RANGE
+    lp = logp.cpu().numpy()
+    assert np.isnan(lp[t_bad])
+    ok = (b.mask == 1) & (np.arange(b.T) != t_bad)
+    ref, _ = oracle.token_logprob(b.hidden, b.w_head, np.minimum(b.target, b.cfg.V - 1), b.mask)
+    assert np.abs(lp[ok] - ref[ok]).max() <= TOL_LOGP
+
+
+def test_malformed_segments_set_status():
+    b = generate(small_config("badcu", 28, B=3, T=120, H=8, V=16))
+    db = to_device(b)
+    cu_np = b.cu_seqlens.copy()
+    cu_np[1], cu_np[2] = cu_np[2], cu_np[1]       # a decreasing boundary
+    assert cu_np[2] < cu_np[1]
+    cu = torch.from_numpy(cu_np).cuda()
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    adv, ret, n = sao.advantage(db.values, db.rewards, db.mask, cu, 1.0, 1.0, 0.0, status=status)
+    torch.cuda.synchronize()
+    assert int(status) & sao.binding.STATUS_SEGMENTS
+    assert np.isnan(adv.cpu().numpy()).any()
