@@ -13,6 +13,9 @@ constexpr float kLn2 = 0.6931471805599453f;
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+// 16-byte chunk as a native vector: copies lower to plain vector loads/stores
+// (HIP's uint4 is a struct whose copies become memcpy through private memory).
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
 // Storage type tags for the head operands.
 struct BF16 {

@@ -5,14 +5,16 @@
 // A workgroup of 256 threads (4 waves as 2 x 2) owns a 256 x 128 tile of C;
 // each wave owns 128 x 64 as 4 x 2 MFMA 32x32 blocks held in 128 accumulator
 // registers per lane. K advances in slabs of 128 bytes per row (64 bf16 or 32
-// fp32 elements), double-buffered in LDS (2 stages x (32 KB of A + 16 KB of B)).
+// fp32 elements) through a 3-stage LDS ring (3 x (32 KB of A + 16 KB of B)).
+// Slabs are copied global -> LDS directly (global_load_lds_dwordx4: no staging
+// registers, no LDS store instructions) two slabs ahead of the MFMAs.
 //
-// Each operand is stored either K-contiguous ([mn][k], row stride ld) or
-// MN-contiguous ([k][mn], row stride ld). LDS always holds [mn][k] rows of
-// eight 16-byte chunks with chunk c of row r at position c ^ (r & 7), so that
-// the 16-byte fragment reads of eight consecutive lanes touch all 32 banks.
-// MN-contiguous operands are transposed in registers (8 x 8 bf16 or 4 x 4 fp32
-// blocks) between the global load and the LDS store.
+// Both operands are stored K-contiguous ([mn][k], row stride ld). LDS holds
+// [mn][k] rows of eight 16-byte chunks with chunk c of row r at position
+// c ^ ((r >> 1) & 7), so that the 16-byte fragment reads of sixteen
+// consecutive lanes touch all 64 banks. The next slab is loaded into registers while the current
+// one feeds the MFMAs, and fragments of K step s+1 are read from LDS while
+// step s multiplies.
 //
 // Accumulator layout of v_mfma_f32_32x32x{16_bf16,2_f32} (block of 32 x 32):
 // lane l, register r holds row (r & 3) + 8 * (r >> 2) + 4 * (l >> 5), column l & 31.
@@ -35,10 +37,12 @@ constexpr int kBM = 256;                        // rows of A per tile
 constexpr int kBN = 128;                        // rows of B per tile
 constexpr int kMI = 4;                          // 32-row MFMA blocks per wave along M
 constexpr int kNI = 2;                          // 32-column MFMA blocks per wave along N
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;                   // 4 waves: 2 along M x 2 along N
+constexpr int kWavesN = 2;
 constexpr int kRowChunks = 8;                   // 16-byte chunks per LDS row (128 bytes of K)
 constexpr int kAChunks = kBM * kRowChunks;      // 32 KB
 constexpr int kBChunks = kBN * kRowChunks;      // 16 KB
+constexpr int kStages = 3;                      // LDS ring depth
 constexpr int kStageChunks = kAChunks + kBChunks;
 
 struct GemmShape {
@@ -78,7 +82,7 @@ struct Mma;
 
 template <>
 struct Mma<BF16> {
-  __device__ __forceinline__ static void run(f32x16_t& acc, const uint4& a, const uint4& b) {
+  __device__ __forceinline__ static void run(f32x16_t& acc, const v4u& a, const v4u& b) {
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                   __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
   }
@@ -86,7 +90,7 @@ struct Mma<BF16> {
 
 template <>
 struct Mma<F32> {
-  __device__ __forceinline__ static void run(f32x16_t& acc, const uint4& a, const uint4& b) {
+  __device__ __forceinline__ static void run(f32x16_t& acc, const v4u& a, const v4u& b) {
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
     acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
@@ -94,199 +98,98 @@ struct Mma<F32> {
   }
 };
 
-__device__ __forceinline__ uint4 zero4() { return make_uint4(0u, 0u, 0u, 0u); }
+__device__ __forceinline__ v4u zero4() { return v4u{0u, 0u, 0u, 0u}; }
 
-// Transpose of an 8 x 8 block of 16-bit values held as 8 rows of 16 bytes.
-__device__ __forceinline__ void transpose8x8_b16(const uint4 (&in)[8], uint4 (&out)[8]) {
-  const uint32_t* r[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) r[j] = reinterpret_cast<const uint32_t*>(&in[j]);
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    uint32_t w[4];
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-      const uint32_t lo = r[2 * d][i >> 1];
-      const uint32_t hi = r[2 * d + 1][i >> 1];
-      w[d] = (i & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
-    }
-    out[i] = make_uint4(w[0], w[1], w[2], w[3]);
-  }
+// LDS position of 16-byte chunk c of tile row r. The LDS serves 16 lanes of a
+// 16-byte access per cycle across 64 banks (256 bytes, two 128-byte rows), so
+// the 16 rows read by lanes 0-15 (and the 2 rows written by them) must land on
+// 16 distinct (row parity, chunk) pairs: XOR with (r >> 1) & 7 does that.
+__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
+
+// Direct copy of 16 bytes per lane from global memory (uniform base `g` plus the
+// lane's byte offset `off`) into LDS: lane l writes LDS bytes [m0 + 16 l, +16),
+// m0 being the wave-uniform LDS byte address `lds_addr`. Issued as inline
+// assembly so that the compiler does not insert its conservative full waits
+// before every LDS read; completion is tracked with explicit vmcnt waits.
+__device__ __forceinline__ void dma16(const void* g, uint32_t off, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(g), "s"(lds_addr)
+               : "memory", "m0");
 }
 
-// Transpose of a 4 x 4 block of 32-bit values held as 4 rows of 16 bytes.
-__device__ __forceinline__ void transpose4x4_b32(const uint4 (&in)[4], uint4 (&out)[4]) {
-  out[0] = make_uint4(in[0].x, in[1].x, in[2].x, in[3].x);
-  out[1] = make_uint4(in[0].y, in[1].y, in[2].y, in[3].y);
-  out[2] = make_uint4(in[0].z, in[1].z, in[2].z, in[3].z);
-  out[3] = make_uint4(in[0].w, in[1].w, in[2].w, in[3].w);
+// This wave's copies except the 12 most recent have landed in LDS, its LDS
+// reads have returned, then the workgroup barrier: afterwards every wave's
+// copies of the next slab are visible and the stage read before is free.
+__device__ __forceinline__ void wait_vm12_barrier() {
+  asm volatile("s_waitcnt vmcnt(12) lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
-// Staging registers for one operand tile of R rows: 16-byte chunks per thread.
-// K-contiguous tiles spread R * 8 chunks over 256 threads; MN-contiguous tiles
-// give each thread whole kPerChunk x kPerChunk blocks.
-template <class E, bool KC, int R>
-constexpr int stage_chunks() {
-  return KC ? R / 32 : ((R / E::kPerChunk + 31) / 32) * E::kPerChunk;
-}
-
-template <int N>
-struct Stage {
-  uint4 v[N];
+// Fragments of one K16 step (bf16; K8 for fp32): kMI rows of A, kNI rows of B.
+struct Frags {
+  v4u a[kMI];
+  v4u b[kNI];
 };
 
-// Global -> registers for one R-row operand tile at (mn0, k0), K-contiguous layout.
-template <class E, int R>
-__device__ __forceinline__ void load_kc(Stage<R / 32>& st, const typename E::storage* base, int64_t ld,
-                                        int64_t mn0, int64_t mn_valid, int64_t k0, int64_t k_valid,
-                                        int tid) {
-  const int c = tid & 7;
-  const int64_t kk = k0 + c * E::kPerChunk;
-  const bool kin = kk < k_valid;
-#pragma unroll
-  for (int i = 0; i < R / 32; ++i) {
-    int64_t row = mn0 + i * 32 + (tid >> 3);
-    row = row < mn_valid ? row : mn_valid - 1;
-    const uint4* p = reinterpret_cast<const uint4*>(base + row * ld + kk);
-    st.v[i] = kin ? *p : zero4();
-  }
-}
-
-template <int R>
-__device__ __forceinline__ void store_kc(const Stage<R / 32>& st, uint4* lds, int tid) {
-  const int c = tid & 7;
-#pragma unroll
-  for (int i = 0; i < R / 32; ++i) {
-    const int row = i * 32 + (tid >> 3);
-    lds[row * kRowChunks + (c ^ (row & 7))] = st.v[i];
-  }
-}
-
-// Global -> registers for one R-row operand tile at (mn0, k0), MN-contiguous layout
-// ([k][mn], row stride ld). The tile is 8 K chunks x R / kPerChunk MN chunks of
-// kPerChunk x kPerChunk blocks; thread tid owns K chunk (tid & 7) and MN chunks
-// (tid >> 3) + 32 j, each loaded as kPerChunk 16-byte rows. Rows k >= k_valid
-// read as zero; MN chunks past mn_valid are clamped to the last valid chunk
-// (their results are unused). Threads without a block (R = 128, bf16) idle.
-template <class E, int R>
-__device__ __forceinline__ void load_mc(Stage<stage_chunks<E, false, R>()>& st, const typename E::storage* base, int64_t ld,
-                                        int64_t mn0, int64_t mn_valid, int64_t k0, int64_t k_valid,
-                                        int tid) {
-  constexpr int P = E::kPerChunk;
-  constexpr int NMC = R / P;                         // MN chunks in the tile
-  constexpr int NB = (NMC + 31) / 32;                // blocks per thread
-  const int kc = tid & 7;
-#pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    const int mc = (tid >> 3) + 32 * j;
-    if (NMC < 32 && mc >= NMC) break;
-    int64_t mn = mn0 + mc * P;
-    mn = mn < mn_valid ? mn : ((mn_valid - 1) / P) * P;
-#pragma unroll
-    for (int e = 0; e < P; ++e) {
-      const int64_t kk = k0 + kc * P + e;
-      const uint4* p = reinterpret_cast<const uint4*>(base + kk * ld + mn);
-      st.v[j * P + e] = kk < k_valid ? *p : zero4();
-    }
-  }
-}
-
-template <class E, int R>
-__device__ __forceinline__ void store_mc(const Stage<stage_chunks<E, false, R>()>& st, uint4* lds, int tid) {
-  constexpr int P = E::kPerChunk;
-  constexpr int NMC = R / P;
-  constexpr int NB = (NMC + 31) / 32;
-  const int kc = tid & 7;
-#pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    const int mc = (tid >> 3) + 32 * j;
-    if (NMC < 32 && mc >= NMC) break;
-    if constexpr (P == 8) {
-      uint4 in[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) in[e] = st.v[e];
-      uint4 out[8];
-      transpose8x8_b16(in, out);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int row = mc * 8 + i;
-        lds[row * kRowChunks + (kc ^ (row & 7))] = out[i];
-      }
-    } else {
-      uint4 in[4] = {st.v[j * 4 + 0], st.v[j * 4 + 1], st.v[j * 4 + 2], st.v[j * 4 + 3]};
-      uint4 out[4];
-      transpose4x4_b32(in, out);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = mc * 4 + i;
-        lds[row * kRowChunks + (kc ^ (row & 7))] = out[i];
-      }
-    }
-  }
-}
-
-template <class E, bool KC, int R>
-__device__ __forceinline__ void load_op(Stage<stage_chunks<E, KC, R>()>& st, const void* base, int64_t ld, int64_t mn0,
-                                        int64_t mn_valid, int64_t k0, int64_t k_valid, int tid) {
-  const auto* p = static_cast<const typename E::storage*>(base);
-  if constexpr (KC)
-    load_kc<E, R>(st, p, ld, mn0, mn_valid, k0, k_valid, tid);
-  else
-    load_mc<E, R>(st, p, ld, mn0, mn_valid, k0, k_valid, tid);
-}
-
-template <class E, bool KC, int R>
-__device__ __forceinline__ void store_op(const Stage<stage_chunks<E, KC, R>()>& st, uint4* lds, int tid) {
-  if constexpr (KC)
-    store_kc<R>(st, lds, tid);
-  else
-    store_mc<E, R>(st, lds, tid);
-}
-
-// One 128-byte K slab of MFMA work for this wave from LDS.
-template <class E>
-__device__ __forceinline__ void mma_slab(f32x16_t (&acc)[kMI][kNI], const uint4* la, const uint4* lb,
-                                         int wm, int wn, int lane) {
+// Rows read by a lane differ by multiples of 32, which leaves (row >> 1) & 7 and
+// hence the swizzle unchanged: one LDS address per operand and K step, the
+// blocks at immediate offsets.
+__device__ __forceinline__ void read_frags(Frags& f, const v4u* la, const v4u* lb, int s, int wm, int wn,
+                                           int lane, int c_valid) {
   const int r32 = lane & 31;
-  const int hf = lane >> 5;
+  const int c = 2 * s + (lane >> 5);
+  const int pc = c ^ ((r32 >> 1) & 7);
+  const v4u* pa = la + (wm * (kBM / 2) + r32) * kRowChunks + pc;
+  const v4u* pb = lb + (wn * (kBN / kWavesN) + r32) * kRowChunks + pc;
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    const int c = 2 * s + hf;
-    uint4 fa[kMI], fb[kNI];
+  for (int i = 0; i < kMI; ++i) f.a[i] = pa[i * 32 * kRowChunks];
 #pragma unroll
-    for (int i = 0; i < kMI; ++i) {
-      const int ra = wm * (kBM / 2) + i * 32 + r32;
-      fa[i] = la[ra * kRowChunks + (c ^ (ra & 7))];
-    }
+  for (int j = 0; j < kNI; ++j) f.b[j] = pb[j * 32 * kRowChunks];
+  if (c >= c_valid) {  // K tail of the last slab: chunk beyond K contributes nothing
 #pragma unroll
-    for (int j = 0; j < kNI; ++j) {
-      const int rb = wn * (kBN / 2) + j * 32 + r32;
-      fb[j] = lb[rb * kRowChunks + (c ^ (rb & 7))];
-    }
+    for (int i = 0; i < kMI; ++i) f.a[i] = zero4();
 #pragma unroll
-    for (int i = 0; i < kMI; ++i)
-#pragma unroll
-      for (int j = 0; j < kNI; ++j) Mma<E>::run(acc[i][j], fa[i], fb[j]);
+    for (int j = 0; j < kNI; ++j) f.b[j] = zero4();
   }
+}
+
+template <class E>
+__device__ __forceinline__ void mma_step(f32x16_t (&acc)[kMI][kNI], const Frags& f) {
+#pragma unroll
+  for (int i = 0; i < kMI; ++i)
+#pragma unroll
+    for (int j = 0; j < kNI; ++j) Mma<E>::run(acc[i][j], f.a[i], f.b[j]);
+}
+
+// LDS writes of this thread are complete, then the workgroup barrier. Unlike
+// __syncthreads() this does not wait for outstanding global loads, which keeps
+// the next slab's prefetch in flight across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // Row index inside the 256-row tile of accumulator (mi, register r) for this lane.
 __device__ __forceinline__ int acc_row(int wm, int mi, int r, int lane) {
   return wm * (kBM / 2) + mi * 32 + (r & 3) + 8 * (r >> 2) + 4 * (lane >> 5);
 }
-__device__ __forceinline__ int acc_col(int wn, int ni, int lane) { return wn * (kBN / 2) + ni * 32 + (lane & 31); }
+__device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
+  return wn * (kBN / kWavesN) + ni * 32 + (lane & 31);
+}
 
 // The generic kernel body. Epi provides:
-//   begin(n0, wm, wn, lane)          once, before the first tile
-//   tile(acc, m0, n0, wm, wn, lane)  after each finished 256 x 256 tile
+//   begin(n0, wm, wn, lane)           once, before the first tile
+//   tile(acc, m0, n0, wm, wn, lane)   after each finished 256 x 128 tile
 //   finish(mg, n0, wm, wn, lane, lds) once, after the last tile (LDS is free)
-template <class E, bool AKC, bool BKC, class Epi>
-__device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, uint4 (*lds)[kStageChunks]) {
+// Both operands are K-contiguous.
+template <class E, class Epi>
+__device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*lds)[kStageChunks]) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1;
-  const int wn = wave & 1;
+  const int wm = wave / kWavesN;
+  const int wn = wave % kWavesN;
 
   // Raster: block -> (N tile, M group).
   const int b = blockIdx.x;
@@ -310,9 +213,10 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, uint4 (*
   const int mt_end = min(mt_begin + s.m_per_wg, min(s.m_tiles, m_tiles_live));
   if (mt_begin >= mt_end) return;
 
-  constexpr int kSlab = 8 * E::kPerChunk;  // K elements per slab
-  const int nk = static_cast<int>((k_valid + kSlab - 1) / kSlab);
-  const int total = (mt_end - mt_begin) * nk;
+  constexpr int P = E::kPerChunk;
+  const int64_t k_chunks = (k_valid + P - 1) / P;          // valid 16-byte chunks per row
+  const int nk = static_cast<int>((k_chunks + 7) / 8);     // slabs of 8 chunks
+  const int c_last = static_cast<int>(k_chunks - static_cast<int64_t>(nk - 1) * 8);  // 1..8
 
   epi.begin(n0, wm, wn, lane);
 
@@ -322,40 +226,107 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, uint4 (*
 #pragma unroll
     for (int j = 0; j < kNI; ++j) acc[i][j] = f32x16_t{};
 
-  Stage<stage_chunks<E, AKC, kBM>()> sa;
-  Stage<stage_chunks<E, BKC, kBN>()> sb;
-  load_op<E, AKC, kBM>(sa, s.a, s.lda, static_cast<int64_t>(mt_begin) * kBM, m_valid, 0, k_valid, tid);
-  load_op<E, BKC, kBN>(sb, s.b, s.ldb, n0, n_valid, 0, k_valid, tid);
-  store_op<E, AKC, kBM>(sa, lds[0], tid);
-  store_op<E, BKC, kBN>(sb, lds[0] + kAChunks, tid);
-  __syncthreads();
+  auto c_valid_of = [&](int kt) -> int { return kt < nk - 1 ? 8 : c_last; };
+  const int esz = static_cast<int>(sizeof(typename E::storage));
+  const char* a_base = static_cast<const char*>(s.a);
+  const char* b_base = static_cast<const char*>(s.b);
+  // Copy instruction q of this wave covers tile rows (wave * QA + q) * 8 + lane / 8
+  // (QA = 8 for A, 4 for B); lane l lands on physical chunk l & 7 of its row,
+  // so it fetches the logical chunk that the swizzle maps there.
+  constexpr int QA = kBM * kRowChunks / 64 / 4;  // copies per wave per A slab
+  constexpr int QB = kBN * kRowChunks / 64 / 4;  // copies per wave per B slab
+  uint32_t offa[QA], offb[QB];   // byte offsets of the rows (this tile) from the operand base
+  int lca[QA], lcb[QB];          // logical chunk fetched by this lane per copy
+#pragma unroll
+  for (int q = 0; q < QA; ++q) {
+    const int r = (wave * QA + q) * 8 + (lane >> 3);
+    lca[q] = swz(r, lane & 7);
+  }
+#pragma unroll
+  for (int q = 0; q < QB; ++q) {
+    const int r = (wave * QB + q) * 8 + (lane >> 3);
+    lcb[q] = swz(r, lane & 7);
+    int64_t row = n0 + r;
+    row = row < n_valid ? row : n_valid - 1;
+    offb[q] = static_cast<uint32_t>(row * s.ldb * esz);
+  }
+  auto set_tile = [&](int mt) {
+#pragma unroll
+    for (int q = 0; q < QA; ++q) {
+      int64_t row = static_cast<int64_t>(mt) * kBM + (wave * QA + q) * 8 + (lane >> 3);
+      row = row < m_valid ? row : m_valid - 1;
+      offa[q] = static_cast<uint32_t>(row * s.lda * esz);
+    }
+  };
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0]));
+  // Issue the copies of slab kt (A rows of the tile set by set_tile) into `stage`.
+  auto copy_slab = [&](int kt, int stage) {
+    const uint32_t sbase = lds0 + static_cast<uint32_t>(stage) * kStageChunks * 16;
+#pragma unroll
+    for (int q = 0; q < QA; ++q) {
+      int64_t c = static_cast<int64_t>(kt) * 8 + lca[q];
+      c = c < k_chunks ? c : k_chunks - 1;
+      dma16(a_base, offa[q] + static_cast<uint32_t>(c * P * esz),
+            __builtin_amdgcn_readfirstlane(sbase + (wave * QA + q) * 1024));
+    }
+#pragma unroll
+    for (int q = 0; q < QB; ++q) {
+      int64_t c = static_cast<int64_t>(kt) * 8 + lcb[q];
+      c = c < k_chunks ? c : k_chunks - 1;
+      dma16(b_base, offb[q] + static_cast<uint32_t>(c * P * esz),
+            __builtin_amdgcn_readfirstlane(sbase + kAChunks * 16 + (wave * QB + q) * 1024));
+    }
+  };
+  static_assert(QA + QB == 12, "the wait counts below assume 12 copies per wave per slab");
 
-  int f = 0;
+  // Slab j (tile-major over this workgroup's tiles) is multiplied from stage
+  // j % 3 while slab j+2 is being copied into stage (j+2) % 3. Copies past the
+  // end read clamped, in-bounds addresses so that every slab issues exactly 12
+  // copies per wave and the wait counts stay exact.
+  int tile_of_copy = mt_begin;
+  int kt_of_copy = 0;
+  auto copy_next = [&](int stage) {
+    if (kt_of_copy == 0) set_tile(tile_of_copy < mt_end ? tile_of_copy : mt_end - 1);
+    copy_slab(kt_of_copy, stage);
+    if (++kt_of_copy == nk) {
+      kt_of_copy = 0;
+      ++tile_of_copy;
+    }
+  };
+  copy_next(0);
+  copy_next(1);
+  wait_vm12_barrier();
+
+  int j = 0;
   for (int mt = mt_begin; mt < mt_end; ++mt) {
-    for (int kt = 0; kt < nk; ++kt, ++f) {
-      const int buf = f & 1;
-      const bool last_k = kt + 1 == nk;
-      const bool more = (f + 1) < total;
-      if (more) {
-        const int nmt = last_k ? mt + 1 : mt;
-        const int nkt = last_k ? 0 : kt + 1;
-        load_op<E, AKC, kBM>(sa, s.a, s.lda, static_cast<int64_t>(nmt) * kBM, m_valid,
-                        static_cast<int64_t>(nkt) * kSlab, k_valid, tid);
-        load_op<E, BKC, kBN>(sb, s.b, s.ldb, n0, n_valid, static_cast<int64_t>(nkt) * kSlab, k_valid, tid);
-      }
-      mma_slab<E>(acc, lds[buf], lds[buf] + kAChunks, wm, wn, lane);
-      if (more) {
-        store_op<E, AKC, kBM>(sa, lds[buf ^ 1], tid);
-        store_op<E, BKC, kBN>(sb, lds[buf ^ 1] + kAChunks, tid);
-      }
-      __syncthreads();
+    for (int kt = 0; kt < nk; ++kt, ++j) {
+      const int stage = j % kStages;
+      copy_next((j + 2) % kStages);
+      const v4u* la = lds[stage];
+      const v4u* lb = lds[stage] + kAChunks;
+      const int c_valid = c_valid_of(kt);
+      // Four K16 steps; the fragments of step s+1 are read while step s multiplies.
+      Frags f0, f1;
+      read_frags(f0, la, lb, 0, wm, wn, lane, c_valid);
+      read_frags(f1, la, lb, 1, wm, wn, lane, c_valid);
+      mma_step<E>(acc, f0);
+      read_frags(f0, la, lb, 2, wm, wn, lane, c_valid);
+      mma_step<E>(acc, f1);
+      read_frags(f1, la, lb, 3, wm, wn, lane, c_valid);
+      mma_step<E>(acc, f0);
+      mma_step<E>(acc, f1);
+      wait_vm12_barrier();
     }
     epi.tile(acc, static_cast<int64_t>(mt) * kBM, n0, wm, wn, lane);
 #pragma unroll
     for (int i = 0; i < kMI; ++i)
 #pragma unroll
-      for (int j = 0; j < kNI; ++j) acc[i][j] = f32x16_t{};
+      for (int jj = 0; jj < kNI; ++jj) acc[i][jj] = f32x16_t{};
   }
+  // Drain the copies issued past the end before LDS is reused.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
   epi.finish(mg, n0, wm, wn, lane, reinterpret_cast<void*>(&lds[0][0]));
 }
 

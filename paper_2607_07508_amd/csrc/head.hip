@@ -6,9 +6,11 @@
 //   reduced in registers to a running (max, sum exp) per token, so the logits
 //   never leave the chip; partials over vocabulary groups are merged per token
 //   and the target logit z_{t,y_t} is a separate dot product.
-// Backward: rows with g != 0 are compacted; for each vocabulary block of Vc rows
-//   (A) recompute z and write dz = g (onehot - exp(z - lse)) to a [T x Vc] scratch,
-//   (B) dH += dz . W_block, (C) dW_block += dz^T . H, all on MFMA.
+// Backward: rows with g != 0 are compacted (Hg, and its transpose Hg^T), W is
+//   transposed once per call (W^T); for each vocabulary block of Vc rows
+//   (A) recompute z and write dz = g (onehot - exp(z - lse)) to [T x Vc] and
+//       [Vc x T] scratch, (B) dH += dz . W_block, (C) dW_block += dz^T . Hg,
+//   all three on MFMA with K-contiguous operands.
 #include "common.hpp"
 #include "gemm.hpp"
 #include "launch.hpp"
@@ -118,10 +120,10 @@ __global__ __launch_bounds__(256) void k_gather_rows(const typename E::storage* 
   const int64_t n = *count;
   if (c >= round_up_dev(n, kRowPad)) return;
   const int64_t chunks = H / E::kPerChunk;
-  uint4* d = reinterpret_cast<uint4*>(dst + c * H);
+  v4u* d = reinterpret_cast<v4u*>(dst + c * H);
   if (c < n) {
     const int64_t t = idx[c];
-    const uint4* s = reinterpret_cast<const uint4*>(src + t * ld_src);
+    const v4u* s = reinterpret_cast<const v4u*>(src + t * ld_src);
     for (int64_t k = lane; k < chunks; k += 64) d[k] = s[k];
     if (lane == 0) {
       if (y_c) y_c[c] = target[t];
@@ -211,21 +213,21 @@ struct EpiLse {
 };
 
 template <class E>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t V) {
-  __shared__ uint4 lds[2][kStageChunks];
+  __shared__ v4u lds[kStages][kStageChunks];
   EpiLse epi;
   epi.part = part;
   epi.ldp = ldp;
   epi.M = V;
-  gemm_body<E, true, true>(s, epi, lds);
+  gemm_body<E>(s, epi, lds);
 }
 
 template <class E>
-__device__ __forceinline__ float dot_chunk(const uint4& a, const uint4& b);
+__device__ __forceinline__ float dot_chunk(const v4u& a, const v4u& b);
 
 template <>
-__device__ __forceinline__ float dot_chunk<BF16>(const uint4& a, const uint4& b) {
+__device__ __forceinline__ float dot_chunk<BF16>(const v4u& a, const v4u& b) {
   const uint32_t* x = reinterpret_cast<const uint32_t*>(&a);
   const uint32_t* y = reinterpret_cast<const uint32_t*>(&b);
   float s = 0.0f;
@@ -238,7 +240,7 @@ __device__ __forceinline__ float dot_chunk<BF16>(const uint4& a, const uint4& b)
 }
 
 template <>
-__device__ __forceinline__ float dot_chunk<F32>(const uint4& a, const uint4& b) {
+__device__ __forceinline__ float dot_chunk<F32>(const v4u& a, const v4u& b) {
   float s = __uint_as_float(a.x) * __uint_as_float(b.x);
   s = fmaf(__uint_as_float(a.y), __uint_as_float(b.y), s);
   s = fmaf(__uint_as_float(a.z), __uint_as_float(b.z), s);
@@ -274,8 +276,8 @@ __global__ __launch_bounds__(256) void k_fwd_finalize(const float2* part, int64_
   const bool yok = y >= 0 && static_cast<int64_t>(y) < V;
   float z = 0.0f;
   if (yok) {
-    const uint4* hr = reinterpret_cast<const uint4*>(hc + c * H);
-    const uint4* wr = reinterpret_cast<const uint4*>(w + static_cast<int64_t>(y) * ld_w);
+    const v4u* hr = reinterpret_cast<const v4u*>(hc + c * H);
+    const v4u* wr = reinterpret_cast<const v4u*>(w + static_cast<int64_t>(y) * ld_w);
     const int64_t chunks = H / E::kPerChunk;
     for (int64_t k = lane; k < chunks; k += 64) z += dot_chunk<E>(hr[k], wr[k]);
   }
@@ -308,12 +310,22 @@ __device__ __forceinline__ void store4<F32>(float* p, const float (&d)[4]) {
   *reinterpret_cast<float4*>(p) = make_float4(d[0], d[1], d[2], d[3]);
 }
 
-// dz_{t,v} = g_t (1[v = y_t] - exp(z_{t,v} - lse_t)) for one vocabulary block,
-// stored token-major: dz[c][v - v0] (row stride ldz).
+template <class E>
+__device__ __forceinline__ typename E::storage to_storage(float x);
+template <>
+__device__ __forceinline__ uint16_t to_storage<BF16>(float x) { return f32_to_bf16(x); }
+template <>
+__device__ __forceinline__ float to_storage<F32>(float x) { return x; }
+
+// dz_{t,v} = g_t (1[v = y_t] - exp(z_{t,v} - lse_t)) for one vocabulary block, stored
+// token-major dz[c][v - v0] (row stride ldz) for the dH product and vocabulary-major
+// dzt[v - v0][c] (row stride ldzt) for the dW product.
 template <class E>
 struct EpiDz {
   typename E::storage* dz;
   int64_t ldz;
+  typename E::storage* dzt;
+  int64_t ldzt;
   int64_t m_valid;   // vocabulary rows of this block
   int64_t v_base;    // vocabulary index of block row 0
   const float* g_c;
@@ -336,7 +348,8 @@ struct EpiDz {
                                        int lane) {
 #pragma unroll
     for (int ni = 0; ni < kNI; ++ni) {
-      typename E::storage* row = dz + (n0 + acc_col(wn, ni, lane)) * ldz;
+      const int64_t c = n0 + acc_col(wn, ni, lane);
+      typename E::storage* row = dz + c * ldz;
 #pragma unroll
       for (int mi = 0; mi < kMI; ++mi) {
 #pragma unroll
@@ -350,6 +363,8 @@ struct EpiDz {
             d[e] = (v + e < m_valid) ? gl[ni] * (oh - p) : 0.0f;
           }
           store4<E>(row + v, d);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dzt[(v + e) * ldzt + c] = to_storage<E>(d[e]);
         }
       }
     }
@@ -390,17 +405,44 @@ struct EpiAcc {
 };
 
 template <class E>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_bwd_dz(GemmShape s, EpiDz<E> epi) {
-  __shared__ uint4 lds[2][kStageChunks];
-  gemm_body<E, true, true>(s, epi, lds);
+  __shared__ v4u lds[kStages][kStageChunks];
+  gemm_body<E>(s, epi, lds);
 }
 
-template <class E, bool AKC, bool BKC>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+template <class E>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_bwd_acc(GemmShape s, EpiAcc epi) {
-  __shared__ uint4 lds[2][kStageChunks];
-  gemm_body<E, AKC, BKC>(s, epi, lds);
+  __shared__ v4u lds[kStages][kStageChunks];
+  gemm_body<E>(s, epi, lds);
+}
+
+// dst[c][r] = src[r][c] for r < rows (rows = *rows_dev when given), zero for
+// rows <= r < round_up(rows, kRowPad); one 64 x 64 tile per block through LDS.
+template <typename S>
+__global__ __launch_bounds__(256) void k_transpose(const S* src, int64_t ld_s, int64_t rows_host,
+                                                   const int32_t* rows_dev, int64_t cols, S* dst,
+                                                   int64_t ld_d) {
+  __shared__ S tile[64][65];
+  const int64_t rows = rows_dev ? static_cast<int64_t>(*rows_dev) : rows_host;
+  const int64_t fill = round_up_dev(rows, kRowPad);
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * 64, c0 = static_cast<int64_t>(blockIdx.x) * 64;
+  if (r0 >= fill) return;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int r = i * 4 + ty;
+    const int64_t gr = r0 + r, gc = c0 + tx;
+    tile[r][tx] = (gr < rows && gc < cols) ? src[gr * ld_s + gc] : S(0);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int oc = i * 4 + ty;
+    const int64_t gc = c0 + oc, gr = r0 + tx;
+    if (gc < cols && gr < fill) dst[gc * ld_d + gr] = tile[tx][oc];
+  }
 }
 
 // Zero rows [0, round_up(*count, 256)) of a [rows][H] fp32 buffer.
@@ -473,7 +515,7 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
   const KernelTimer& tm = kernel_timer();
   const bool timed = tm.kernel == SAO_KERNEL_HEAD_FORWARD && tm.start && tm.stop;
   if (timed) hipEventRecord(tm.start, st);
-  hipLaunchKernelGGL(k_head_fwd<E>, dim3(gemm_grid(s)), dim3(256), 0, st, s, part, L.t_pad, V);
+  hipLaunchKernelGGL(k_head_fwd<E>, dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad, V);
   if (timed) hipEventRecord(tm.stop, st);
   hipLaunchKernelGGL(k_fwd_finalize<E>, dim3(rows4), dim3(256), 0, st, part, L.t_pad,
                      static_cast<int>(L.m_groups), hc, H, static_cast<const S*>(w_head), ld_w, V, idx,
@@ -499,6 +541,9 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
   S* hg = reinterpret_cast<S*>(w8 + L.hg);
   float* dh = reinterpret_cast<float*>(w8 + L.dh);
   S* dz = reinterpret_cast<S*>(w8 + L.dz);
+  S* dzt = reinterpret_cast<S*>(w8 + L.dzt);
+  S* hgt = reinterpret_cast<S*>(w8 + L.hgt);
+  S* wt = reinterpret_cast<S*>(w8 + L.wt);
   const S* w = static_cast<const S*>(w_head);
 
   const int nb = static_cast<int>(L.n_count_blocks);
@@ -508,27 +553,32 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
   const int rows4 = static_cast<int>(L.t_pad / 4);
   hipLaunchKernelGGL(k_gather_rows<E>, dim3(rows4), dim3(256), 0, st, static_cast<const S*>(hidden),
                      ld_hidden, H, idx, count, hg, target, y_c, g, g_c, lse, lse_c);
+  const int hb = static_cast<int>(ceil_div(H, 64));
+  // Hg^T [H][t_pad] and W^T [H][v_pad]: K-contiguous operands of the dW and dH products.
+  hipLaunchKernelGGL(k_transpose<S>, dim3(hb, static_cast<int>(L.t_pad / 64)), dim3(256), 0, st,
+                     static_cast<const S*>(hg), H, L.t_pad, count, H, hgt, L.t_pad);
+  hipLaunchKernelGGL(k_transpose<S>, dim3(hb, static_cast<int>(L.v_pad / 64)), dim3(256), 0, st, w, ld_w, V,
+                     nullptr, H, wt, L.v_pad);
   hipLaunchKernelGGL(k_zero_rows, dim3(rows4), dim3(256), 0, st, dh, H, count);
 
   for (int64_t vb = 0; vb < L.n_vblocks; ++vb) {
     const int64_t v0 = vb * L.vc;
     const int64_t vlen = (V - v0) < L.vc ? (V - v0) : L.vc;
-    const S* wb = w + v0 * ld_w;
-    // (A) dz for this vocabulary block
-    GemmShape sa = make_shape(wb, ld_w, vlen, hg, H, T, H, 1);
+    // (A) z^T[v][t] = W[v0 + v] . Hg[t] -> dz in both layouts
+    GemmShape sa = make_shape(w + v0 * ld_w, ld_w, vlen, hg, H, T, H, 1);
     sa.n_dev = count;
-    EpiDz<E> ez{dz, L.vc, vlen, v0, g_c, lse_c, y_c, {}, {}, {}};
-    hipLaunchKernelGGL(k_bwd_dz<E>, dim3(gemm_grid(sa)), dim3(256), 0, st, sa, ez);
-    // (B) dH[t][h] += sum_v dz[t][v] W[v0 + v][h]
-    GemmShape sb = make_shape(dz, L.vc, T, wb, ld_w, H, vlen, 1);
+    EpiDz<E> ez{dz, L.vc, dzt, L.t_pad, vlen, v0, g_c, lse_c, y_c, {}, {}, {}};
+    hipLaunchKernelGGL(k_bwd_dz<E>, dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez);
+    // (B) dH[t][h] += sum_v dz[t][v] W^T[h][v0 + v]
+    GemmShape sb = make_shape(dz, L.vc, T, wt + v0, L.v_pad, H, vlen, 1);
     sb.m_dev = count;
     EpiAcc eb{dh, H, L.t_pad, H};
-    hipLaunchKernelGGL((k_bwd_acc<E, true, false>), dim3(gemm_grid(sb)), dim3(256), 0, st, sb, eb);
-    // (C) dW[v0 + v][h] += sum_t dz[t][v] Hg[t][h]
-    GemmShape sc = make_shape(dz, L.vc, vlen, hg, H, H, T, 1);
+    hipLaunchKernelGGL(k_bwd_acc<E>, dim3(gemm_grid(sb)), dim3(kThreads), 0, st, sb, eb);
+    // (C) dW[v0 + v][h] += sum_t dz^T[v][t] Hg^T[h][t]
+    GemmShape sc = make_shape(dzt, L.t_pad, vlen, hgt, L.t_pad, H, T, 1);
     sc.k_dev = count;
     EpiAcc ec{dw + v0 * H, H, vlen, H};
-    hipLaunchKernelGGL((k_bwd_acc<E, false, false>), dim3(gemm_grid(sc)), dim3(256), 0, st, sc, ec);
+    hipLaunchKernelGGL(k_bwd_acc<E>, dim3(gemm_grid(sc)), dim3(kThreads), 0, st, sc, ec);
   }
   const int t4 = static_cast<int>(ceil_div(T, 4));
   hipLaunchKernelGGL(k_dh_scatter<E>, dim3(t4), dim3(256), 0, st, dh, H, pos, T, static_cast<S*>(dhidden));
