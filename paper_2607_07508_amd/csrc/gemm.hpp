@@ -2,12 +2,12 @@
 //
 //   C[m][n] = sum_k A[m][k] * B[n][k]      (fp32 accumulation)
 //
-// A workgroup of 256 threads (4 waves as 2 x 2) owns a 256 x 128 tile of C;
-// each wave owns 128 x 64 as 4 x 2 MFMA 32x32 blocks held in 128 accumulator
+// A workgroup of 256 threads (4 waves as 2 x 2) owns a 256 x 256 tile of C;
+// each wave owns 128 x 128 as 4 x 4 MFMA 32x32 blocks held in 256 accumulator
 // registers per lane. K advances in slabs of 128 bytes per row (64 bf16 or 32
-// fp32 elements) through a 3-stage LDS ring (3 x (32 KB of A + 16 KB of B)).
+// fp32 elements) through an LDS ring of kStages x (32 KB of A + 32 KB of B).
 // Slabs are copied global -> LDS directly (global_load_lds_dwordx4: no staging
-// registers, no LDS store instructions) two slabs ahead of the MFMAs.
+// registers, no LDS store instructions) kAhead slabs ahead of the MFMAs.
 //
 // Both operands are stored K-contiguous ([mn][k], row stride ld). LDS holds
 // [mn][k] rows of eight 16-byte chunks with chunk c of row r at position
@@ -22,11 +22,13 @@
 // contributes the same k indices to A and B and the product is exact for any
 // hardware ordering of k inside the instruction.
 //
-// Tile raster: blocks are dispatched round-robin over the 8 XCDs (block b runs
-// on XCD b % 8). Every 256 consecutive blocks form one "wave" covering
-// (8 * SN) N-tiles x (32 / SN) M-groups; the 32 blocks of one XCD take SN
-// N-tiles x (32/SN) M-groups, so blocks sharing an XCD's L2 share operand
-// panels, and all XCDs work on the same M-groups at once.
+// Tile raster: one tile per workgroup. Blocks are dispatched round-robin over
+// the 8 XCDs (block b runs on XCD b % 8). Every 256 consecutive blocks form one
+// "wave"; the 32 blocks of one XCD take SN N-tiles x (32 / SN) M-tiles, so
+// blocks sharing an XCD's L2 share operand panels. In N-split mode the XCDs of
+// a wave take different N-tiles of the same M-tiles (the wave covers 8 SN x
+// 32/SN tiles); in M-split mode they take different M-tiles of the same N-tiles
+// (SN x 256/SN), so an M-tile's rows are fetched by one XCD only.
 #pragma once
 
 #include "common.hpp"
@@ -34,15 +36,16 @@
 namespace sao {
 
 constexpr int kBM = 256;                        // rows of A per tile
-constexpr int kBN = 128;                        // rows of B per tile
+constexpr int kBN = 256;                        // rows of B per tile
 constexpr int kMI = 4;                          // 32-row MFMA blocks per wave along M
-constexpr int kNI = 2;                          // 32-column MFMA blocks per wave along N
+constexpr int kNI = 4;                          // 32-column MFMA blocks per wave along N
 constexpr int kThreads = 256;                   // 4 waves: 2 along M x 2 along N
 constexpr int kWavesN = 2;
 constexpr int kRowChunks = 8;                   // 16-byte chunks per LDS row (128 bytes of K)
 constexpr int kAChunks = kBM * kRowChunks;      // 32 KB
-constexpr int kBChunks = kBN * kRowChunks;      // 16 KB
-constexpr int kStages = 3;                      // LDS ring depth
+constexpr int kBChunks = kBN * kRowChunks;      // 32 KB
+constexpr int kStages = 2;                      // LDS ring depth
+constexpr int kAhead = kStages - 1;             // slabs copied ahead of the MFMAs
 constexpr int kStageChunks = kAChunks + kBChunks;
 
 struct GemmShape {
@@ -58,23 +61,31 @@ struct GemmShape {
   const int32_t* k_dev;    // optional device count overriding k
   int m_tiles;             // ceil(m / kBM) with the host bound
   int n_tiles;             // ceil(n / kBN) with the host bound
-  int m_per_wg;            // consecutive M tiles one workgroup walks (N tile fixed)
-  int m_groups;            // ceil(m_tiles / m_per_wg)
-  int sn;                  // N tiles per XCD per raster wave (1, 2 or 4)
+  int sn;                  // N tiles per XCD per raster wave (1, 2, 4 or 8)
+  int msplit;              // 0: XCDs split the wave's N tiles; 1: XCDs split its M tiles
 };
+
+// Tiles of one raster wave (256 blocks) along N and along M.
+__host__ __device__ inline int wave_n(const GemmShape& s) { return s.msplit ? s.sn : 8 * s.sn; }
+__host__ __device__ inline int wave_m(const GemmShape& s) { return s.msplit ? 256 / s.sn : 32 / s.sn; }
 
 // Number of 256-block raster waves times 256.
 inline int gemm_grid(const GemmShape& s) {
-  const int nw = (s.n_tiles + 8 * s.sn - 1) / (8 * s.sn);
-  const int sm = 32 / s.sn;
-  const int mw = (s.m_groups + sm - 1) / sm;
+  const int nw = (s.n_tiles + wave_n(s) - 1) / wave_n(s);
+  const int mw = (s.m_tiles + wave_m(s) - 1) / wave_m(s);
   return nw * mw * 256;
 }
 
+// N-split: SN so that 8 SN N-tiles fill the N range with little waste.
 inline int pick_sn(int n_tiles) {
   if (n_tiles % 32 == 0 || n_tiles > 96) return 4;
   if (n_tiles % 16 == 0) return 2;
   return 1;
+}
+
+// M-split: all of a narrow N range per XCD (up to 8 tiles).
+inline int pick_sn_msplit(int n_tiles) {
+  return n_tiles >= 8 ? 8 : (n_tiles >= 4 ? 4 : (n_tiles >= 2 ? 2 : 1));
 }
 
 template <class E>
@@ -116,11 +127,15 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t off, uint32_t lds_
                : "memory", "m0");
 }
 
-// This wave's copies except the 12 most recent have landed in LDS, its LDS
+// This wave's copies except the N most recent have landed in LDS, its LDS
 // reads have returned, then the workgroup barrier: afterwards every wave's
 // copies of the next slab are visible and the stage read before is free.
-__device__ __forceinline__ void wait_vm12_barrier() {
-  asm volatile("s_waitcnt vmcnt(12) lgkmcnt(0)" ::: "memory");
+template <int N>
+__device__ __forceinline__ void wait_copies_barrier() {
+  if constexpr (N == 0)
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+  else
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(N) : "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
@@ -178,10 +193,10 @@ __device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
   return wn * (kBN / kWavesN) + ni * 32 + (lane & 31);
 }
 
-// The generic kernel body. Epi provides:
-//   begin(n0, wm, wn, lane)           once, before the first tile
-//   tile(acc, m0, n0, wm, wn, lane)   after each finished 256 x 128 tile
-//   finish(mg, n0, wm, wn, lane, lds) once, after the last tile (LDS is free)
+// The generic kernel body: one 256 x 256 tile per workgroup. Epi provides:
+//   begin(n0, wm, wn, lane)                 before the K loop
+//   tile(acc, m0, n0, wm, wn, lane, lds)    after it (LDS is free)
+//   finish(mt, n0, wm, wn, lane, lds)  last (LDS is free)
 // Both operands are K-contiguous.
 template <class E, class Epi>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*lds)[kStageChunks]) {
@@ -191,27 +206,29 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   const int wm = wave / kWavesN;
   const int wn = wave % kWavesN;
 
-  // Raster: block -> (N tile, M group).
+  // Raster: block -> (N tile, M tile).
   const int b = blockIdx.x;
   const int sn = s.sn;
-  const int sm = 32 / sn;
-  const int nw = (s.n_tiles + 8 * sn - 1) / (8 * sn);
+  const int nw = (s.n_tiles + wave_n(s) - 1) / wave_n(s);
   const int w = b >> 8;
   const int xcd = b & 7;
   const int slot = (b >> 3) & 31;
-  const int n_tile = (w % nw) * 8 * sn + xcd * sn + (slot % sn);
-  const int mg = (w / nw) * sm + slot / sn;
+  int n_tile, mt;
+  if (s.msplit) {
+    n_tile = (w % nw) * sn + slot % sn;
+    mt = (w / nw) * (256 / sn) + xcd * (32 / sn) + slot / sn;
+  } else {
+    n_tile = (w % nw) * 8 * sn + xcd * sn + slot % sn;
+    mt = (w / nw) * (32 / sn) + slot / sn;
+  }
 
   const int64_t n_valid = s.n_dev ? static_cast<int64_t>(*s.n_dev) : s.n;
   const int64_t m_valid = s.m_dev ? static_cast<int64_t>(*s.m_dev) : s.m;
   const int64_t k_valid = s.k_dev ? static_cast<int64_t>(*s.k_dev) : s.k;
-  if (n_tile >= s.n_tiles || mg >= s.m_groups) return;
+  if (n_tile >= s.n_tiles || mt >= s.m_tiles) return;
   const int64_t n0 = static_cast<int64_t>(n_tile) * kBN;
-  if (n0 >= n_valid || k_valid <= 0 || m_valid <= 0) return;
-  const int m_tiles_live = static_cast<int>((m_valid + kBM - 1) / kBM);
-  const int mt_begin = mg * s.m_per_wg;
-  const int mt_end = min(mt_begin + s.m_per_wg, min(s.m_tiles, m_tiles_live));
-  if (mt_begin >= mt_end) return;
+  const int64_t m0 = static_cast<int64_t>(mt) * kBM;
+  if (n0 >= n_valid || m0 >= m_valid || k_valid <= 0) return;
 
   constexpr int P = E::kPerChunk;
   const int64_t k_chunks = (k_valid + P - 1) / P;          // valid 16-byte chunks per row
@@ -226,21 +243,24 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
 #pragma unroll
     for (int j = 0; j < kNI; ++j) acc[i][j] = f32x16_t{};
 
-  auto c_valid_of = [&](int kt) -> int { return kt < nk - 1 ? 8 : c_last; };
   const int esz = static_cast<int>(sizeof(typename E::storage));
   const char* a_base = static_cast<const char*>(s.a);
   const char* b_base = static_cast<const char*>(s.b);
-  // Copy instruction q of this wave covers tile rows (wave * QA + q) * 8 + lane / 8
-  // (QA = 8 for A, 4 for B); lane l lands on physical chunk l & 7 of its row,
-  // so it fetches the logical chunk that the swizzle maps there.
+  // Copy instruction q of this wave covers tile rows (wave * Q + q) * 8 + lane / 8;
+  // lane l lands on physical chunk l & 7 of its row, so it fetches the logical
+  // chunk that the swizzle maps there. Row offsets are 32-bit: operands are
+  // limited to 2^31 elements on the host.
   constexpr int QA = kBM * kRowChunks / 64 / 4;  // copies per wave per A slab
   constexpr int QB = kBN * kRowChunks / 64 / 4;  // copies per wave per B slab
-  uint32_t offa[QA], offb[QB];   // byte offsets of the rows (this tile) from the operand base
-  int lca[QA], lcb[QB];          // logical chunk fetched by this lane per copy
+  uint32_t offa[QA], offb[QB];
+  int lca[QA], lcb[QB];
 #pragma unroll
   for (int q = 0; q < QA; ++q) {
     const int r = (wave * QA + q) * 8 + (lane >> 3);
     lca[q] = swz(r, lane & 7);
+    int64_t row = m0 + r;
+    row = row < m_valid ? row : m_valid - 1;
+    offa[q] = static_cast<uint32_t>(row * s.lda * esz);
   }
 #pragma unroll
   for (int q = 0; q < QB; ++q) {
@@ -250,16 +270,9 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
     row = row < n_valid ? row : n_valid - 1;
     offb[q] = static_cast<uint32_t>(row * s.ldb * esz);
   }
-  auto set_tile = [&](int mt) {
-#pragma unroll
-    for (int q = 0; q < QA; ++q) {
-      int64_t row = static_cast<int64_t>(mt) * kBM + (wave * QA + q) * 8 + (lane >> 3);
-      row = row < m_valid ? row : m_valid - 1;
-      offa[q] = static_cast<uint32_t>(row * s.lda * esz);
-    }
-  };
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0]));
-  // Issue the copies of slab kt (A rows of the tile set by set_tile) into `stage`.
+  // Issue the copies of slab kt into `stage` (chunks past K are clamped to the
+  // last valid chunk; their fragments are zeroed in read_frags).
   auto copy_slab = [&](int kt, int stage) {
     const uint32_t sbase = lds0 + static_cast<uint32_t>(stage) * kStageChunks * 16;
 #pragma unroll
@@ -277,57 +290,36 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
             __builtin_amdgcn_readfirstlane(sbase + kAChunks * 16 + (wave * QB + q) * 1024));
     }
   };
-  static_assert(QA + QB == 12, "the wait counts below assume 12 copies per wave per slab");
 
-  // Slab j (tile-major over this workgroup's tiles) is multiplied from stage
-  // j % 3 while slab j+2 is being copied into stage (j+2) % 3. Copies past the
-  // end read clamped, in-bounds addresses so that every slab issues exactly 12
-  // copies per wave and the wait counts stay exact.
-  int tile_of_copy = mt_begin;
-  int kt_of_copy = 0;
-  auto copy_next = [&](int stage) {
-    if (kt_of_copy == 0) set_tile(tile_of_copy < mt_end ? tile_of_copy : mt_end - 1);
-    copy_slab(kt_of_copy, stage);
-    if (++kt_of_copy == nk) {
-      kt_of_copy = 0;
-      ++tile_of_copy;
-    }
-  };
-  copy_next(0);
-  copy_next(1);
-  wait_vm12_barrier();
-
-  int j = 0;
-  for (int mt = mt_begin; mt < mt_end; ++mt) {
-    for (int kt = 0; kt < nk; ++kt, ++j) {
-      const int stage = j % kStages;
-      copy_next((j + 2) % kStages);
-      const v4u* la = lds[stage];
-      const v4u* lb = lds[stage] + kAChunks;
-      const int c_valid = c_valid_of(kt);
-      // Four K16 steps; the fragments of step s+1 are read while step s multiplies.
-      Frags f0, f1;
-      read_frags(f0, la, lb, 0, wm, wn, lane, c_valid);
-      read_frags(f1, la, lb, 1, wm, wn, lane, c_valid);
-      mma_step<E>(acc, f0);
-      read_frags(f0, la, lb, 2, wm, wn, lane, c_valid);
-      mma_step<E>(acc, f1);
-      read_frags(f1, la, lb, 3, wm, wn, lane, c_valid);
-      mma_step<E>(acc, f0);
-      mma_step<E>(acc, f1);
-      wait_vm12_barrier();
-    }
-    epi.tile(acc, static_cast<int64_t>(mt) * kBM, n0, wm, wn, lane);
-#pragma unroll
-    for (int i = 0; i < kMI; ++i)
-#pragma unroll
-      for (int jj = 0; jj < kNI; ++jj) acc[i][jj] = f32x16_t{};
+  // Slab kt is multiplied from stage kt % kStages while slab kt + kAhead is
+  // copied into stage (kt + kAhead) % kStages. With one slab ahead, nothing is
+  // in flight behind the slab waited for, so the wait is a full drain and the
+  // copy past the last slab is simply skipped.
+  static_assert(kAhead == 1, "wait counts below assume one slab ahead");
+  copy_slab(0, 0);
+  wait_copies_barrier<0>();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int stage = kt & 1;
+    if (kt + 1 < nk) copy_slab(kt + 1, stage ^ 1);
+    const v4u* la = lds[stage];
+    const v4u* lb = lds[stage] + kAChunks;
+    const int c_valid = kt + 1 < nk ? 8 : c_last;
+    // Four K16 steps; the fragments of step s+1 are read while step s multiplies.
+    Frags f0, f1;
+    read_frags(f0, la, lb, 0, wm, wn, lane, c_valid);
+    read_frags(f1, la, lb, 1, wm, wn, lane, c_valid);
+    mma_step<E>(acc, f0);
+    read_frags(f0, la, lb, 2, wm, wn, lane, c_valid);
+    mma_step<E>(acc, f1);
+    read_frags(f1, la, lb, 3, wm, wn, lane, c_valid);
+    mma_step<E>(acc, f0);
+    mma_step<E>(acc, f1);
+    wait_copies_barrier<0>();
   }
-  // Drain the copies issued past the end before LDS is reused.
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-  epi.finish(mg, n0, wm, wn, lane, reinterpret_cast<void*>(&lds[0][0]));
+  // After the final drain no copy is in flight and every LDS read has returned:
+  // the epilogue may use LDS as scratch.
+  epi.tile(acc, m0, n0, wm, wn, lane, reinterpret_cast<void*>(&lds[0][0]));
+  epi.finish(mt, n0, wm, wn, lane, reinterpret_cast<void*>(&lds[0][0]));
 }
 
 }  // namespace sao

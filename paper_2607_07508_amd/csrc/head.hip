@@ -144,7 +144,7 @@ __global__ __launch_bounds__(256) void k_gather_rows(const typename E::storage* 
 // Forward: online log-sum-exp epilogue
 // ------------------------------------------------------------------------- //
 struct EpiLse {
-  float2* part;   // [m_groups][ldp] running (max, sum exp) per token
+  float2* part;   // [m_tiles][ldp] (max, sum exp) per token and vocabulary tile
   int64_t ldp;
   int64_t M;      // vocabulary size
   float rm[kNI], rs[kNI];
@@ -158,23 +158,22 @@ struct EpiLse {
   }
 
   __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t, int wm, int,
-                                       int lane) {
-    if (m0 + kBM > M) {
-#pragma unroll
-      for (int mi = 0; mi < kMI; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (m0 + acc_row(wm, mi, r, lane) >= M)
-#pragma unroll
-            for (int ni = 0; ni < kNI; ++ni) acc[mi][ni][r] = -__builtin_inff();
-    }
+                                       int lane, void*) {
+    // Rows at or past the vocabulary end (last tile only) read as -inf; the
+    // accumulators themselves are left untouched so they can stay in AGPRs.
+    const int64_t lim64 = M - m0 - wm * (kBM / 2) - 4 * (lane >> 5);
+    const int lim = lim64 > kBM ? kBM : static_cast<int>(lim64);
+    auto z_at = [&](int mi, int ni, int r) -> float {
+      const int off = mi * 32 + (r & 3) + 8 * (r >> 2);
+      return off < lim ? acc[mi][ni][r] : -__builtin_inff();
+    };
 #pragma unroll
     for (int ni = 0; ni < kNI; ++ni) {
       float tmax = -__builtin_inff();
 #pragma unroll
       for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc[mi][ni][r]);
+        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, z_at(mi, ni, r));
       const float mn = fmaxf(rm[ni], tmax);
       if (mn == -__builtin_inff()) continue;
       const float sc = mn * kLog2e;
@@ -182,7 +181,7 @@ struct EpiLse {
 #pragma unroll
       for (int mi = 0; mi < kMI; ++mi)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s += fast_exp2(fmaf(acc[mi][ni][r], kLog2e, -sc));
+        for (int r = 0; r < 16; ++r) s += fast_exp2(fmaf(z_at(mi, ni, r), kLog2e, -sc));
       rm[ni] = mn;
       rs[ni] = s;
     }
@@ -310,6 +309,21 @@ __device__ __forceinline__ void store4<F32>(float* p, const float (&d)[4]) {
   *reinterpret_cast<float4*>(p) = make_float4(d[0], d[1], d[2], d[3]);
 }
 
+// Transpose of an 8 x 8 block of 16-bit values held as 8 rows of 16 bytes.
+__device__ __forceinline__ void transpose8x8_b16(const v4u (&in)[8], v4u (&out)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    v4u o;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const uint32_t lo = in[2 * d][i >> 1];
+      const uint32_t hi = in[2 * d + 1][i >> 1];
+      o[d] = (i & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+    }
+    out[i] = o;
+  }
+}
+
 template <class E>
 __device__ __forceinline__ typename E::storage to_storage(float x);
 template <>
@@ -344,27 +358,87 @@ struct EpiDz {
     }
   }
 
+  // dz of accumulator (mi, ni, registers 4j .. 4j+3): four consecutive vocabulary rows v..v+3.
+  __device__ __forceinline__ void dz4(const f32x16_t (&acc)[kMI][kNI], int mi, int ni, int j, int64_t v,
+                                      float (&d)[4]) const {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float p = fast_exp2(fmaf(acc[mi][ni][4 * j + e], kLog2e, -ll[ni]));
+      const float oh = (v + e == yl[ni]) ? 1.0f : 0.0f;
+      d[e] = (v + e < m_valid) ? gl[ni] * (oh - p) : 0.0f;
+    }
+  }
+
+  // LDS chunk position of 16-byte chunk c (8 vocabulary entries) of token row t
+  // in the staged bf16 tile: conflict-free for the accumulator writes (32
+  // consecutive rows, one chunk), the row reads and the 8-row block reads.
+  static __device__ __forceinline__ int tswz(int t, int c) { return c ^ ((t ^ (t >> 3)) & 15); }
+
   __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t n0, int wm, int wn,
-                                       int lane) {
+                                       int lane, void* smem) {
+    if constexpr (sizeof(typename E::storage) == 2) {
+      // Stage the 256 x 256 bf16 tile in LDS as [t][v] (128 KB), then write both
+      // global layouts with 16-byte stores.
+      v4u* tile16 = static_cast<v4u*>(smem);       // [256 rows][32 chunks]
 #pragma unroll
-    for (int ni = 0; ni < kNI; ++ni) {
-      const int64_t c = n0 + acc_col(wn, ni, lane);
-      typename E::storage* row = dz + c * ldz;
+      for (int ni = 0; ni < kNI; ++ni) {
+        const int t = acc_col(wn, ni, lane);
 #pragma unroll
-      for (int mi = 0; mi < kMI; ++mi) {
+        for (int mi = 0; mi < kMI; ++mi) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int64_t v = m0 + acc_row(wm, mi, 4 * j, lane);
-          float d[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float p = fast_exp2(fmaf(acc[mi][ni][4 * j + e], kLog2e, -ll[ni]));
-            const float oh = (v + e == yl[ni]) ? 1.0f : 0.0f;
-            d[e] = (v + e < m_valid) ? gl[ni] * (oh - p) : 0.0f;
+          for (int j = 0; j < 4; ++j) {
+            const int vl = acc_row(wm, mi, 4 * j, lane);   // multiple of 4
+            float d[4];
+            dz4(acc, mi, ni, j, m0 + vl, d);
+            const uint32_t lo = static_cast<uint32_t>(f32_to_bf16(d[0])) |
+                                (static_cast<uint32_t>(f32_to_bf16(d[1])) << 16);
+            const uint32_t hi = static_cast<uint32_t>(f32_to_bf16(d[2])) |
+                                (static_cast<uint32_t>(f32_to_bf16(d[3])) << 16);
+            uint2* p = reinterpret_cast<uint2*>(tile16 + t * 32 + tswz(t, vl >> 3)) + ((vl >> 2) & 1);
+            *p = make_uint2(lo, hi);
           }
-          store4<E>(row + v, d);
+        }
+      }
+      __syncthreads();
+      const int tid = threadIdx.x;
+      // [t][v]: thread takes chunk c of row t for 32 (t, c) pairs.
+#pragma unroll 4
+      for (int k = 0; k < 32; ++k) {
+        const int id = k * kThreads + tid;
+        const int t = id >> 5, c = id & 31;
+        const v4u x = tile16[t * 32 + tswz(t, c)];
+        *reinterpret_cast<v4u*>(dz + (n0 + t) * ldz + m0 + c * 8) = x;
+      }
+      // [v][t]: thread takes 8 x 8 blocks (8 tokens x 8 vocabulary entries), transposes them
+      // in registers and writes 8 rows of 8 tokens.
+#pragma unroll 1
+      for (int k = 0; k < 4; ++k) {
+        const int id = k * kThreads + tid;
+        const int c = id >> 5, t0 = (id & 31) * 8;
+        v4u in[8], out[8];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) dzt[(v + e) * ldzt + c] = to_storage<E>(d[e]);
+        for (int e = 0; e < 8; ++e) in[e] = tile16[(t0 + e) * 32 + tswz(t0 + e, c)];
+        transpose8x8_b16(in, out);
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          *reinterpret_cast<v4u*>(dzt + (m0 + c * 8 + i) * ldzt + n0 + t0) = out[i];
+      }
+    } else {
+#pragma unroll
+      for (int ni = 0; ni < kNI; ++ni) {
+        const int64_t c = n0 + acc_col(wn, ni, lane);
+        typename E::storage* row = dz + c * ldz;
+#pragma unroll
+        for (int mi = 0; mi < kMI; ++mi) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int64_t v = m0 + acc_row(wm, mi, 4 * j, lane);
+            float d[4];
+            dz4(acc, mi, ni, j, v, d);
+            store4<E>(row + v, d);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) dzt[(v + e) * ldzt + c] = to_storage<E>(d[e]);
+          }
         }
       }
     }
@@ -386,7 +460,7 @@ struct EpiAcc {
   __device__ __forceinline__ void begin(int64_t, int, int, int) {}
 
   __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t n0, int wm, int wn,
-                                       int lane) {
+                                       int lane, void*) {
 #pragma unroll
     for (int ni = 0; ni < kNI; ++ni) {
       const int64_t n = n0 + acc_col(wn, ni, lane);
@@ -476,15 +550,13 @@ __global__ __launch_bounds__(256) void k_dh_scatter(const float* dh, int64_t H, 
 // Launchers
 // ------------------------------------------------------------------------- //
 static GemmShape make_shape(const void* a, int64_t lda, int64_t m, const void* b, int64_t ldb, int64_t n,
-                            int64_t k, int m_per_wg) {
+                            int64_t k) {
   GemmShape s{};
   s.a = a; s.lda = lda; s.m = m;
   s.b = b; s.ldb = ldb; s.n = n;
   s.k = k;
   s.m_tiles = static_cast<int>(ceil_div(m, kBM));
   s.n_tiles = static_cast<int>(ceil_div(n, kBN));
-  s.m_per_wg = m_per_wg;
-  s.m_groups = static_cast<int>(ceil_div(s.m_tiles, m_per_wg));
   s.sn = pick_sn(s.n_tiles);
   return s;
 }
@@ -510,15 +582,15 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
   const int rows4 = static_cast<int>(L.t_pad / 4);
   hipLaunchKernelGGL(k_gather_rows<E>, dim3(rows4), dim3(256), 0, st, static_cast<const S*>(hidden),
                      ld_hidden, H, idx, count, hc, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
-  GemmShape s = make_shape(w_head, ld_w, V, hc, H, T, H, kFwdMTilesPerWg);
+  GemmShape s = make_shape(w_head, ld_w, V, hc, H, T, H);
   s.n_dev = count;
   const KernelTimer& tm = kernel_timer();
   const bool timed = tm.kernel == SAO_KERNEL_HEAD_FORWARD && tm.start && tm.stop;
-  if (timed) hipEventRecord(tm.start, st);
+  if (timed) (void)hipEventRecord(tm.start, st);
   hipLaunchKernelGGL(k_head_fwd<E>, dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad, V);
-  if (timed) hipEventRecord(tm.stop, st);
+  if (timed) (void)hipEventRecord(tm.stop, st);
   hipLaunchKernelGGL(k_fwd_finalize<E>, dim3(rows4), dim3(256), 0, st, part, L.t_pad,
-                     static_cast<int>(L.m_groups), hc, H, static_cast<const S*>(w_head), ld_w, V, idx,
+                     static_cast<int>(L.m_tiles), hc, H, static_cast<const S*>(w_head), ld_w, V, idx,
                      target, count, logp, lse, status);
   return hipGetLastError();
 }
@@ -565,18 +637,22 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
     const int64_t v0 = vb * L.vc;
     const int64_t vlen = (V - v0) < L.vc ? (V - v0) : L.vc;
     // (A) z^T[v][t] = W[v0 + v] . Hg[t] -> dz in both layouts
-    GemmShape sa = make_shape(w + v0 * ld_w, ld_w, vlen, hg, H, T, H, 1);
+    GemmShape sa = make_shape(w + v0 * ld_w, ld_w, vlen, hg, H, T, H);
     sa.n_dev = count;
     EpiDz<E> ez{dz, L.vc, dzt, L.t_pad, vlen, v0, g_c, lse_c, y_c, {}, {}, {}};
     hipLaunchKernelGGL(k_bwd_dz<E>, dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez);
     // (B) dH[t][h] += sum_v dz[t][v] W^T[h][v0 + v]
-    GemmShape sb = make_shape(dz, L.vc, T, wt + v0, L.v_pad, H, vlen, 1);
+    GemmShape sb = make_shape(dz, L.vc, T, wt + v0, L.v_pad, H, vlen);
     sb.m_dev = count;
+    sb.msplit = 1;
+    sb.sn = pick_sn_msplit(sb.n_tiles);
     EpiAcc eb{dh, H, L.t_pad, H};
     hipLaunchKernelGGL(k_bwd_acc<E>, dim3(gemm_grid(sb)), dim3(kThreads), 0, st, sb, eb);
     // (C) dW[v0 + v][h] += sum_t dz^T[v][t] Hg^T[h][t]
-    GemmShape sc = make_shape(dzt, L.t_pad, vlen, hgt, L.t_pad, H, T, 1);
+    GemmShape sc = make_shape(dzt, L.t_pad, vlen, hgt, L.t_pad, H, T);
     sc.k_dev = count;
+    sc.msplit = 1;
+    sc.sn = pick_sn_msplit(sc.n_tiles);
     EpiAcc ec{dw + v0 * H, H, vlen, H};
     hipLaunchKernelGGL(k_bwd_acc<E>, dim3(gemm_grid(sc)), dim3(kThreads), 0, st, sc, ec);
   }

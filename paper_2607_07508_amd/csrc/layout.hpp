@@ -8,7 +8,6 @@ namespace sao {
 
 constexpr int64_t kTile = 256;
 constexpr int64_t kRowsPerCountBlock = 1024;  // rows per block of the compaction count
-constexpr int kFwdMTilesPerWg = 8;            // vocabulary tiles one forward workgroup walks
 constexpr int64_t kVocabBlock = 16384;        // vocabulary rows per backward dZ block
 constexpr int kLossThreads = 256;
 constexpr int kLossPerThread = 8;
@@ -29,7 +28,7 @@ struct Carve {
 
 // sao_token_logprob
 struct LogprobLayout {
-  int64_t t_pad, n_count_blocks, m_tiles, m_groups;
+  int64_t t_pad, n_count_blocks, m_tiles;
   size_t blk_counts, count, idx, hc, part, total;
 };
 
@@ -38,13 +37,12 @@ inline LogprobLayout logprob_layout(int64_t T, int64_t H, int64_t V, size_t esiz
   L.t_pad = round_up(T, kTile);
   L.n_count_blocks = ceil_div(T, kRowsPerCountBlock);
   L.m_tiles = ceil_div(V, kTile);
-  L.m_groups = ceil_div(L.m_tiles, kFwdMTilesPerWg);
   Carve c;
   L.blk_counts = c.take(4 * static_cast<size_t>(L.n_count_blocks));
   L.count = c.take(4);
   L.idx = c.take(4 * static_cast<size_t>(L.t_pad));
   L.hc = c.take(esize * static_cast<size_t>(L.t_pad) * static_cast<size_t>(H));
-  L.part = c.take(8 * static_cast<size_t>(L.m_groups) * static_cast<size_t>(L.t_pad));
+  L.part = c.take(8 * static_cast<size_t>(L.m_tiles) * static_cast<size_t>(L.t_pad));
   L.total = c.off;
   return L;
 }
