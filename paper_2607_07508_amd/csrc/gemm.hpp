@@ -4,17 +4,22 @@
 //
 // A workgroup of 256 threads (4 waves as 2 x 2) owns a 256 x 256 tile of C;
 // each wave owns 128 x 128 as 4 x 4 MFMA 32x32 blocks held in 256 accumulator
-// registers per lane. K advances in slabs of 128 bytes per row (64 bf16 or 32
-// fp32 elements) through an LDS ring of kStages x (32 KB of A + 32 KB of B).
-// Slabs are copied global -> LDS directly (global_load_lds_dwordx4: no staging
-// registers, no LDS store instructions) kAhead slabs ahead of the MFMAs.
+// registers per lane. K advances in slabs of kRowChunks x 16 bytes per row (64
+// bf16 or 32 fp32 elements) through an LDS ring of kStages x (32 KB of A + 32 KB
+// of B). Slabs are copied global -> LDS directly (global_load_lds_dwordx4: no
+// staging registers, no LDS store instructions), kStages - 1 slabs ahead of the
+// MFMAs; the copies of a slab are spread over the MFMAs of the last K step of
+// the slab before it, right after the barrier that frees their stage.
 //
 // Both operands are stored K-contiguous ([mn][k], row stride ld). LDS holds
-// [mn][k] rows of eight 16-byte chunks with chunk c of row r at position
-// c ^ ((r >> 1) & 7), so that the 16-byte fragment reads of sixteen
-// consecutive lanes touch all 64 banks. The next slab is loaded into registers while the current
-// one feeds the MFMAs, and fragments of K step s+1 are read from LDS while
-// step s multiplies.
+// [mn][k] rows of kRowChunks 16-byte chunks, chunk c of row r at position
+// swz(r, c), so that the 16-byte fragment reads of sixteen consecutive lanes
+// touch all 64 banks. The fragments of K step s+1 are read from LDS while step
+// s multiplies, and the workgroup barrier of a slab sits before its last K
+// step, so that the first fragments of the next slab are read while that step
+// multiplies. (Deeper rings of shorter slabs measured slower on gfx950: with
+// random bf16 operands the MFMA rate is power-limited, and the extra barriers
+// cost more than the added copy slack gains.)
 //
 // Accumulator layout of v_mfma_f32_32x32x{16_bf16,2_f32} (block of 32 x 32):
 // lane l, register r holds row (r & 3) + 8 * (r >> 2) + 4 * (l >> 5), column l & 31.
@@ -45,7 +50,10 @@ constexpr int kRowChunks = 8;                   // 16-byte chunks per LDS row (1
 constexpr int kAChunks = kBM * kRowChunks;      // 32 KB
 constexpr int kBChunks = kBN * kRowChunks;      // 32 KB
 constexpr int kStages = 2;                      // LDS ring depth
-constexpr int kAhead = kStages - 1;             // slabs copied ahead of the MFMAs
+constexpr int kRowsPerCopy = 64 / kRowChunks;   // tile rows filled by one wave-wide 1 KB copy
+constexpr int kSteps = kRowChunks / 2;          // MFMA K steps per slab (two chunks each)
+constexpr int kRowsPerLine = 16 / kRowChunks;   // tile rows per 256-byte line of the 64 banks
+static_assert(kSteps % 2 == 0, "the next slab's first step lands in f0");
 constexpr int kStageChunks = kAChunks + kBChunks;
 
 struct GemmShape {
@@ -112,10 +120,11 @@ struct Mma<F32> {
 __device__ __forceinline__ v4u zero4() { return v4u{0u, 0u, 0u, 0u}; }
 
 // LDS position of 16-byte chunk c of tile row r. The LDS serves 16 lanes of a
-// 16-byte access per cycle across 64 banks (256 bytes, two 128-byte rows), so
-// the 16 rows read by lanes 0-15 (and the 2 rows written by them) must land on
-// 16 distinct (row parity, chunk) pairs: XOR with (r >> 1) & 7 does that.
-__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
+// 16-byte access per cycle across 64 banks (one 256-byte line, kRowsPerLine
+// rows), so the 16 consecutive rows read by lanes 0-15 at one logical chunk
+// must land on 16 distinct (row within line, chunk) pairs: XOR with the line
+// index modulo kRowChunks does that.
+__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r / kRowsPerLine) % kRowChunks); }
 
 // Direct copy of 16 bytes per lane from global memory (uniform base `g` plus the
 // lane's byte offset `off`) into LDS: lane l writes LDS bytes [m0 + 16 l, +16),
@@ -129,7 +138,8 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t off, uint32_t lds_
 
 // This wave's copies except the N most recent have landed in LDS, its LDS
 // reads have returned, then the workgroup barrier: afterwards every wave's
-// copies of the next slab are visible and the stage read before is free.
+// copies of the awaited slab are visible and the stage read before is free.
+// Copies complete in issue order, so the N most recent are the later slabs.
 template <int N>
 __device__ __forceinline__ void wait_copies_barrier() {
   if constexpr (N == 0)
@@ -140,40 +150,63 @@ __device__ __forceinline__ void wait_copies_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// The same with N = PerSlab * pending for a wave-uniform `pending` in
+// [0, kStages - 1] (the count must be an immediate).
+template <int PerSlab, int P = kStages - 1>
+__device__ __forceinline__ void wait_slabs_barrier(int pending) {
+  if constexpr (P == 0) {
+    wait_copies_barrier<0>();
+  } else {
+    if (pending >= P)
+      wait_copies_barrier<PerSlab * P>();
+    else
+      wait_slabs_barrier<PerSlab, P - 1>(pending);
+  }
+}
+
 // Fragments of one K16 step (bf16; K8 for fp32): kMI rows of A, kNI rows of B.
 struct Frags {
   v4u a[kMI];
   v4u b[kNI];
 };
 
-// Rows read by a lane differ by multiples of 32, which leaves (row >> 1) & 7 and
-// hence the swizzle unchanged: one LDS address per operand and K step, the
-// blocks at immediate offsets.
+// Rows read by a lane differ by multiples of 32, which leaves the line index
+// modulo kRowChunks and hence the swizzle unchanged: one LDS address per operand and K step, the
+// blocks at immediate offsets. Chunks past K hold zeros (written by the copy of
+// the last slab), so no fragment needs masking.
 __device__ __forceinline__ void read_frags(Frags& f, const v4u* la, const v4u* lb, int s, int wm, int wn,
-                                           int lane, int c_valid) {
+                                           int lane) {
   const int r32 = lane & 31;
   const int c = 2 * s + (lane >> 5);
-  const int pc = c ^ ((r32 >> 1) & 7);
+  const int pc = swz(r32, c);
   const v4u* pa = la + (wm * (kBM / 2) + r32) * kRowChunks + pc;
   const v4u* pb = lb + (wn * (kBN / kWavesN) + r32) * kRowChunks + pc;
 #pragma unroll
   for (int i = 0; i < kMI; ++i) f.a[i] = pa[i * 32 * kRowChunks];
 #pragma unroll
   for (int j = 0; j < kNI; ++j) f.b[j] = pb[j * 32 * kRowChunks];
-  if (c >= c_valid) {  // K tail of the last slab: chunk beyond K contributes nothing
+}
+
+// The MFMAs of row block i of one K step.
+template <class E>
+__device__ __forceinline__ void mma_row(f32x16_t (&acc)[kMI][kNI], const Frags& f, int i) {
 #pragma unroll
-    for (int i = 0; i < kMI; ++i) f.a[i] = zero4();
-#pragma unroll
-    for (int j = 0; j < kNI; ++j) f.b[j] = zero4();
-  }
+  for (int j = 0; j < kNI; ++j) Mma<E>::run(acc[i][j], f.a[i], f.b[j]);
 }
 
 template <class E>
 __device__ __forceinline__ void mma_step(f32x16_t (&acc)[kMI][kNI], const Frags& f) {
 #pragma unroll
-  for (int i = 0; i < kMI; ++i)
-#pragma unroll
-    for (int j = 0; j < kNI; ++j) Mma<E>::run(acc[i][j], f.a[i], f.b[j]);
+  for (int i = 0; i < kMI; ++i) mma_row<E>(acc, f, i);
+}
+
+// Instruction order is pinned where it matters: the compiler would otherwise
+// defer the LDS reads of the next K step behind the MFMAs of this one and then
+// wait for them, exposing the LDS latency once per step.
+__device__ __forceinline__ void pin_order() {
+#ifndef NO_PIN
+  __builtin_amdgcn_sched_barrier(0);
+#endif
 }
 
 // LDS writes of this thread are complete, then the workgroup barrier. Unlike
@@ -232,8 +265,8 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
 
   constexpr int P = E::kPerChunk;
   const int64_t k_chunks = (k_valid + P - 1) / P;          // valid 16-byte chunks per row
-  const int nk = static_cast<int>((k_chunks + 7) / 8);     // slabs of 8 chunks
-  const int c_last = static_cast<int>(k_chunks - static_cast<int64_t>(nk - 1) * 8);  // 1..8
+  const int nk = static_cast<int>((k_chunks + kRowChunks - 1) / kRowChunks);  // slabs
+  const int c_last = static_cast<int>(k_chunks - static_cast<int64_t>(nk - 1) * kRowChunks);  // 1..kRowChunks
 
   epi.begin(n0, wm, wn, lane);
 
@@ -246,78 +279,122 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   const int esz = static_cast<int>(sizeof(typename E::storage));
   const char* a_base = static_cast<const char*>(s.a);
   const char* b_base = static_cast<const char*>(s.b);
-  // Copy instruction q of this wave covers tile rows (wave * Q + q) * 8 + lane / 8;
-  // lane l lands on physical chunk l & 7 of its row, so it fetches the logical
-  // chunk that the swizzle maps there. Row offsets are 32-bit: operands are
+  // Copy instruction q of this wave covers kRowsPerCopy tile rows from
+  // (wave * Q + q) * kRowsPerCopy; lane l lands on row + l / kRowChunks, physical
+  // chunk l % kRowChunks, so it fetches the logical chunk that the swizzle maps there. Row offsets are 32-bit: operands are
   // limited to 2^31 elements on the host.
-  constexpr int QA = kBM * kRowChunks / 64 / 4;  // copies per wave per A slab
-  constexpr int QB = kBN * kRowChunks / 64 / 4;  // copies per wave per B slab
+  constexpr int QA = kBM / kRowsPerCopy / 4;  // copies per wave per A slab
+  constexpr int QB = kBN / kRowsPerCopy / 4;  // copies per wave per B slab
+  constexpr int kCopiesPerSlab = QA + QB;
   uint32_t offa[QA], offb[QB];
   int lca[QA], lcb[QB];
 #pragma unroll
   for (int q = 0; q < QA; ++q) {
-    const int r = (wave * QA + q) * 8 + (lane >> 3);
-    lca[q] = swz(r, lane & 7);
+    const int r = (wave * QA + q) * kRowsPerCopy + lane / kRowChunks;
+    lca[q] = swz(r, lane % kRowChunks);
     int64_t row = m0 + r;
     row = row < m_valid ? row : m_valid - 1;
     offa[q] = static_cast<uint32_t>(row * s.lda * esz);
   }
 #pragma unroll
   for (int q = 0; q < QB; ++q) {
-    const int r = (wave * QB + q) * 8 + (lane >> 3);
-    lcb[q] = swz(r, lane & 7);
+    const int r = (wave * QB + q) * kRowsPerCopy + lane / kRowChunks;
+    lcb[q] = swz(r, lane % kRowChunks);
     int64_t row = n0 + r;
     row = row < n_valid ? row : n_valid - 1;
     offb[q] = static_cast<uint32_t>(row * s.ldb * esz);
   }
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0]));
-  // Issue the copies of slab kt into `stage` (chunks past K are clamped to the
-  // last valid chunk; their fragments are zeroed in read_frags).
+  // Copy q (of QA for A, then QB for B) of slab kt into `stage`. In the last
+  // slab, lanes whose chunk lies past K write zeros to their LDS slot instead.
+  // Chunk 0 of every row is valid, so each copy instruction keeps at least 16
+  // active lanes and is always issued: the vmcnt arithmetic of the ring holds.
+  v4u* lds_flat = &lds[0][0];
+  auto copy_one = [&](int q, int kt, int stage) {
+    const bool is_a = q < QA;
+    const int qq = is_a ? q : q - QA;
+    const int slot = (is_a ? 0 : kAChunks) + (wave * (is_a ? QA : QB) + qq) * 64;
+    const int64_t c = static_cast<int64_t>(kt) * kRowChunks + (is_a ? lca[qq] : lcb[qq]);
+    dma16(is_a ? a_base : b_base, (is_a ? offa[qq] : offb[qq]) + static_cast<uint32_t>(c * P * esz),
+          __builtin_amdgcn_readfirstlane(lds0 + static_cast<uint32_t>(stage * kStageChunks + slot) * 16));
+  };
   auto copy_slab = [&](int kt, int stage) {
-    const uint32_t sbase = lds0 + static_cast<uint32_t>(stage) * kStageChunks * 16;
+    if (kt == nk - 1 && c_last < kRowChunks) {
 #pragma unroll
-    for (int q = 0; q < QA; ++q) {
-      int64_t c = static_cast<int64_t>(kt) * 8 + lca[q];
-      c = c < k_chunks ? c : k_chunks - 1;
-      dma16(a_base, offa[q] + static_cast<uint32_t>(c * P * esz),
-            __builtin_amdgcn_readfirstlane(sbase + (wave * QA + q) * 1024));
-    }
+      for (int q = 0; q < kCopiesPerSlab; ++q) {
+        const bool is_a = q < QA;
+        const int qq = is_a ? q : q - QA;
+        const int slot = (is_a ? 0 : kAChunks) + (wave * (is_a ? QA : QB) + qq) * 64;
+        const int64_t c = static_cast<int64_t>(kt) * kRowChunks + (is_a ? lca[qq] : lcb[qq]);
+        if (c < k_chunks)
+          copy_one(q, kt, stage);
+        else
+          lds_flat[stage * kStageChunks + slot + lane] = zero4();
+      }
+    } else {
 #pragma unroll
-    for (int q = 0; q < QB; ++q) {
-      int64_t c = static_cast<int64_t>(kt) * 8 + lcb[q];
-      c = c < k_chunks ? c : k_chunks - 1;
-      dma16(b_base, offb[q] + static_cast<uint32_t>(c * P * esz),
-            __builtin_amdgcn_readfirstlane(sbase + kAChunks * 16 + (wave * QB + q) * 1024));
+      for (int q = 0; q < kCopiesPerSlab; ++q) copy_one(q, kt, stage);
     }
   };
 
-  // Slab kt is multiplied from stage kt % kStages while slab kt + kAhead is
-  // copied into stage (kt + kAhead) % kStages. With one slab ahead, nothing is
-  // in flight behind the slab waited for, so the wait is a full drain and the
-  // copy past the last slab is simply skipped.
-  static_assert(kAhead == 1, "wait counts below assume one slab ahead");
-  copy_slab(0, 0);
-  wait_copies_barrier<0>();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int stage = kt & 1;
-    if (kt + 1 < nk) copy_slab(kt + 1, stage ^ 1);
-    const v4u* la = lds[stage];
-    const v4u* lb = lds[stage] + kAChunks;
-    const int c_valid = kt + 1 < nk ? 8 : c_last;
-    // Four K16 steps; the fragments of step s+1 are read while step s multiplies.
-    Frags f0, f1;
-    read_frags(f0, la, lb, 0, wm, wn, lane, c_valid);
-    read_frags(f1, la, lb, 1, wm, wn, lane, c_valid);
-    mma_step<E>(acc, f0);
-    read_frags(f0, la, lb, 2, wm, wn, lane, c_valid);
-    mma_step<E>(acc, f1);
-    read_frags(f1, la, lb, 3, wm, wn, lane, c_valid);
-    mma_step<E>(acc, f0);
-    mma_step<E>(acc, f1);
-    wait_copies_barrier<0>();
+  // Slab kt is multiplied from stage kt % kStages while slabs kt+1 .. kt+3 are
+  // in flight or landed. Once every wave has read slab kt's last fragments (the
+  // barrier inside iteration kt), its stage takes slab kt + kStages. Before that
+  // barrier this wave's copies of slab kt+1 must have landed; the ones issued
+  // after them (slabs kt+2 and kt+3, as far as they exist) may stay in flight.
+  for (int j = 0; j < kStages; ++j)
+    if (j < nk) copy_slab(j, j);
+  {
+    const int pending = nk - 1 < kStages - 1 ? nk - 1 : kStages - 1;
+    wait_slabs_barrier<kCopiesPerSlab>(pending);
   }
-  // After the final drain no copy is in flight and every LDS read has returned:
-  // the epilogue may use LDS as scratch.
+  Frags f0, f1;
+  read_frags(f0, lds[0], lds[0] + kAChunks, 0, wm, wn, lane);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int stage = kt % kStages;
+    // K steps 0 .. kSteps-2: the fragments of the next step are read first, then
+    // this step multiplies (f0 holds the even steps, f1 the odd ones).
+#pragma unroll
+    for (int st = 0; st + 1 < kSteps; ++st) {
+      Frags& cur = st % 2 == 0 ? f0 : f1;
+      Frags& nxt = st % 2 == 0 ? f1 : f0;
+      read_frags(nxt, lds[stage], lds[stage] + kAChunks, st + 1, wm, wn, lane);
+      pin_order();
+      mma_step<E>(acc, cur);
+      pin_order();
+    }
+    Frags& last = kSteps % 2 == 0 ? f1 : f0;
+    const int kn = kt + kStages;  // the slab that refills this stage
+    if (kt + 1 < nk) {
+      const int rest = nk - kt - 2;
+      wait_slabs_barrier<kCopiesPerSlab>(rest < kStages - 2 ? rest : kStages - 2);
+    }
+    // Unconditional, so that the LDS wait counts agree on both paths; after the
+    // last slab it reads a drained stage and the values go unused.
+    const int nstage = (kt + 1) % kStages;
+    read_frags(f0, lds[nstage], lds[nstage] + kAChunks, 0, wm, wn, lane);
+    pin_order();
+    // Full slabs refill the freed stage with copies spread over the last step's
+    // MFMAs; the last slab, when K ends inside it, is copied after them with its
+    // zero fill.
+    const bool refill = kn < nk - 1 || (kn == nk - 1 && c_last == kRowChunks);
+    constexpr int kPerRow = kCopiesPerSlab / kMI;
+    static_assert(kCopiesPerSlab % kMI == 0, "copies spread evenly over the row blocks");
+#pragma unroll
+    for (int i = 0; i < kMI; ++i) {
+      mma_row<E>(acc, last, i);
+      pin_order();
+      if (refill) {
+#pragma unroll
+        for (int q = 0; q < kPerRow; ++q) copy_one(i * kPerRow + q, kn, stage);
+      }
+      pin_order();
+    }
+    if (kn == nk - 1 && c_last < kRowChunks) copy_slab(kn, stage);
+  }
+  // Every copy has landed (the last wait drained them); once every wave's LDS
+  // reads have returned, the epilogue may use LDS as scratch.
+  lds_barrier();
   epi.tile(acc, m0, n0, wm, wn, lane, reinterpret_cast<void*>(&lds[0][0]));
   epi.finish(mt, n0, wm, wn, lane, reinterpret_cast<void*>(&lds[0][0]));
 }
