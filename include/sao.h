@@ -179,6 +179,37 @@ sao_status_t sao_loss_backward(const void* hidden, int64_t ld_hidden, const void
                                hipStream_t stream);
 
 /*
+ * Critic head for the PPO-style update with a learned value model (Sec. 2): a
+ * bias-free H -> 1 projection of the hidden states,
+ *   v[t] = hidden[t] . w_v                        (float32 [T], overwritten)
+ * w_v is H elements of `dtype`, 16-byte aligned. All T rows are computed. No
+ * workspace is needed (ws may be NULL). Use v, detached, as the `values` of
+ * sao_advantage.
+ */
+sao_status_t sao_value_forward(const void* hidden, int64_t ld_hidden, const void* w_v, int64_t T,
+                               int64_t H, sao_dtype_t dtype, float* v, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/*
+ * Squared-error loss of the critic against the lambda = 1 returns `ret` of
+ * sao_advantage (Sec. 2 and Sec. 4.1), token-level mean with the same N:
+ *   loss_v[0]    += (1/N) sum_t mask[t] (v[t] - ret[t])^2        (float64, +=)
+ *   dv_t          = 2 mask[t] (v[t] - ret[t]) / N
+ *   dhidden_v[t]  = dv_t w_v          (dtype of hidden, dense [T][H]; rows with
+ *                                      mask 0 are exact zeros; overwritten)
+ *   dw_v         += sum_t dv_t hidden[t]                          (float32 [H], +=)
+ * N = *n_tokens (device int64) or, when n_tokens is NULL, sum(mask) of this
+ * call; N == 0 adds nothing and writes zero rows. No gradient flows through the
+ * advantages. Reductions are deterministic. Workspace:
+ * sao_workspace_size(SAO_OP_VALUE, T, H, 1, dtype).
+ */
+sao_status_t sao_value_loss(const void* hidden, int64_t ld_hidden, const void* w_v, const float* v,
+                            const float* ret, const uint8_t* mask, int64_t T, int64_t H,
+                            const int64_t* n_tokens, sao_dtype_t dtype, double* loss_v,
+                            void* dhidden_v, float* dw_v, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/*
  * Measurement hook, not part of the pass. For the calling thread, records the
  * caller's HIP events `start_event` and `stop_event` (hipEvent_t, created by
  * the caller with timing enabled) on the launch stream immediately before and

@@ -22,7 +22,7 @@ FLAG_MASKED, FLAG_USED, FLAG_LOW, FLAG_HIGH, FLAG_NONFINITE = 0, 1, 2, 3, 4
 
 EXPORTS = ("sao_status_string", "sao_last_error_message", "sao_version", "sao_workspace_size",
            "sao_token_logprob", "sao_advantage", "sao_clipped_loss", "sao_loss_backward",
-           "sao_debug_time_kernel")
+           "sao_value_forward", "sao_value_loss", "sao_debug_time_kernel")
 KERNEL_NONE, KERNEL_HEAD_FORWARD = 0, 1
 
 
@@ -48,6 +48,9 @@ _SIGS = {
                                         _p, _p, _p, _p, ctypes.c_size_t, _p]),
     "sao_loss_backward": (ctypes.c_int, [_p, _i64, _p, _i64, _p, _p, _p, _i64, _i64, _i64,
                                          ctypes.c_int, _p, _p, _p, ctypes.c_size_t, _p]),
+    "sao_value_forward": (ctypes.c_int, [_p, _i64, _p, _i64, _i64, ctypes.c_int, _p, _p, ctypes.c_size_t, _p]),
+    "sao_value_loss": (ctypes.c_int, [_p, _i64, _p, _p, _p, _p, _i64, _i64, _p, ctypes.c_int, _p, _p, _p, _p,
+                                      ctypes.c_size_t, _p]),
     "sao_debug_time_kernel": (None, [ctypes.c_int, _p, _p]),
 }
 
@@ -182,6 +185,39 @@ def loss_backward(hidden: torch.Tensor, w_head: torch.Tensor, target: torch.Tens
         _ptr(lse), _ptr(g), T, H, V, dt, _ptr(dhidden), _ptr(dw_head), _ptr(ws),
         0 if ws is None else ws.numel(), _stream(dev)))
     return dhidden, dw_head
+
+
+def value_forward(hidden: torch.Tensor, w_value: torch.Tensor, v: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """v [T] f32 = hidden . w_value (bias-free critic head)."""
+    T, H = hidden.shape
+    dev = hidden.device
+    if v is None:
+        v = torch.empty(T, dtype=torch.float32, device=dev)
+    _check(lib().sao_value_forward(_ptr(hidden), _rows(hidden, "hidden"), _ptr(w_value), T, H,
+                                   _dtype_code(hidden), _ptr(v), None, 0, _stream(dev)))
+    return v
+
+
+def value_loss(hidden: torch.Tensor, w_value: torch.Tensor, v: torch.Tensor, ret: torch.Tensor,
+               mask: torch.Tensor, n_tokens: Optional[torch.Tensor] = None,
+               loss: Optional[torch.Tensor] = None, dw_value: Optional[torch.Tensor] = None,
+               dhidden: Optional[torch.Tensor] = None):
+    """(loss_v [1] f64 +=, dhidden_v [T,H] in hidden's dtype, dw_value [H] f32 +=)."""
+    T, H = hidden.shape
+    dt = _dtype_code(hidden)
+    dev = hidden.device
+    if loss is None:
+        loss = torch.zeros(1, dtype=torch.float64, device=dev)
+    if dw_value is None:
+        dw_value = torch.zeros(H, dtype=torch.float32, device=dev)
+    if dhidden is None:
+        dhidden = torch.empty((T, H), dtype=hidden.dtype, device=dev)
+    ws = _workspace(workspace_size(OP_VALUE, T, H, 1, dt), dev)
+    _check(lib().sao_value_loss(
+        _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_value), _ptr(v), _ptr(ret), _ptr(mask), T, H,
+        _ptr(n_tokens), dt, _ptr(loss), _ptr(dhidden), _ptr(dw_value), _ptr(ws),
+        0 if ws is None else ws.numel(), _stream(dev)))
+    return loss, dhidden, dw_value
 
 
 def time_kernel(kernel: int, start: Optional[torch.cuda.Event], stop: Optional[torch.cuda.Event]) -> None:

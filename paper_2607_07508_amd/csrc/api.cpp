@@ -111,7 +111,8 @@ size_t sao_workspace_size(sao_op_t op, int64_t T, int64_t H, int64_t V, sao_dtyp
     case SAO_OP_ADVANTAGE:
       return sao::kAdvantageWorkspace;
     case SAO_OP_VALUE:
-      return 0;
+      if (H < 1) return 0;
+      return sao::value_layout(T, H).total;
   }
   return 0;
 }
@@ -178,6 +179,32 @@ sao_status_t sao_loss_backward(const void* hidden, int64_t ld_hidden, const void
   return device(sao::launch_backward(hidden, ld_hidden, w_head, ld_w, target, lse, g, T, H, V,
                                      dtype == SAO_BF16, dhidden, dw_head, ws, stream),
                 "sao_loss_backward launch");
+}
+
+sao_status_t sao_value_forward(const void* hidden, int64_t ld_hidden, const void* w_v, int64_t T, int64_t H,
+                               sao_dtype_t dtype, float* v, void* ws, size_t ws_bytes, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  if (!hidden || !w_v || !v) return fail(SAO_ERR_NULL, "hidden, w_v and v are required");
+  if (sao_status_t s = check_head(hidden, ld_hidden, w_v, H, T, H, 1, dtype)) return s;
+  if (T == 0) return ok();
+  return device(sao::launch_value_forward(hidden, ld_hidden, w_v, T, H, dtype == SAO_BF16, v, stream),
+                "sao_value_forward launch");
+}
+
+sao_status_t sao_value_loss(const void* hidden, int64_t ld_hidden, const void* w_v, const float* v,
+                            const float* ret, const uint8_t* mask, int64_t T, int64_t H, const int64_t* n_tokens,
+                            sao_dtype_t dtype, double* loss_v, void* dhidden_v, float* dw_v, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  if (!hidden || !w_v || !v || !ret || !mask || !loss_v || !dhidden_v || !dw_v)
+    return fail(SAO_ERR_NULL, "hidden, w_v, v, ret, mask, loss_v, dhidden_v and dw_v are required");
+  if (sao_status_t s = check_head(hidden, ld_hidden, w_v, H, T, H, 1, dtype)) return s;
+  if (!aligned16(dhidden_v)) return fail(SAO_ERR_SHAPE, "dhidden_v must be 16-byte aligned");
+  if (T == 0) return ok();
+  if (sao_status_t s = check_ws(ws, ws_bytes, sao_workspace_size(SAO_OP_VALUE, T, H, 1, dtype))) return s;
+  return device(sao::launch_value_loss(hidden, ld_hidden, w_v, v, ret, mask, T, H, n_tokens, dtype == SAO_BF16,
+                                       loss_v, dhidden_v, dw_v, ws, stream),
+                "sao_value_loss launch");
 }
 
 }  // extern "C"

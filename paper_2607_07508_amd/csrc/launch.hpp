@@ -23,6 +23,13 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const float
                        int64_t T, float eps_low, float eps_high, const int64_t* n_tokens, double* loss,
                        float* g, uint8_t* flags, int64_t* counts, void* ws, hipStream_t st);
 
+hipError_t launch_value_forward(const void* hidden, int64_t ld_hidden, const void* w_v, int64_t T, int64_t H,
+                                bool bf16, float* v, hipStream_t st);
+
+hipError_t launch_value_loss(const void* hidden, int64_t ld_hidden, const void* w_v, const float* v,
+                             const float* ret, const uint8_t* mask, int64_t T, int64_t H, const int64_t* n_tokens,
+                             bool bf16, double* loss_v, void* dhidden_v, float* dw_v, void* ws, hipStream_t st);
+
 // Thread-local measurement hook (see sao_debug_time_kernel).
 struct KernelTimer {
   int kernel = 0;

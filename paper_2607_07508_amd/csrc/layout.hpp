@@ -102,4 +102,29 @@ inline LossLayout loss_layout(int64_t T) {
   return L;
 }
 
+// sao_value_loss (sao_value_forward needs none)
+constexpr int kValueThreads = 256;
+constexpr int64_t kValueRows = 128;           // rows per block of the value-loss pass
+constexpr int64_t kValueCountBlocks = 1024;   // blocks of the mask count when N is not given
+
+struct ValueLayout {
+  int64_t row_blocks, count_blocks;
+  size_t part_cnt, n_count, part_loss, part_dw, total;
+};
+
+inline ValueLayout value_layout(int64_t T, int64_t H) {
+  ValueLayout L{};
+  L.row_blocks = ceil_div(T, kValueRows);
+  L.count_blocks = ceil_div(T, static_cast<int64_t>(kValueThreads) * 8);
+  if (L.count_blocks > kValueCountBlocks) L.count_blocks = kValueCountBlocks;
+  if (L.count_blocks < 1) L.count_blocks = 1;
+  Carve c;
+  L.part_cnt = c.take(8 * static_cast<size_t>(L.count_blocks));
+  L.n_count = c.take(8);
+  L.part_loss = c.take(8 * static_cast<size_t>(L.row_blocks));
+  L.part_dw = c.take(4 * static_cast<size_t>(L.row_blocks) * static_cast<size_t>(H));
+  L.total = c.off;
+  return L;
+}
+
 }  // namespace sao

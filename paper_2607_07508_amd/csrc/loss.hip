@@ -7,41 +7,10 @@
 #include "common.hpp"
 #include "launch.hpp"
 #include "layout.hpp"
+#include "reduce.hpp"
 #include "../../include/sao.h"
 
 namespace sao {
-
-template <typename T>
-__device__ __forceinline__ T block_sum(T v, T* sh) {
-  v = wave_sum(v);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane == 0) sh[wave] = v;
-  __syncthreads();
-  T r = sh[0];
-#pragma unroll
-  for (int w = 1; w < kLossThreads / 64; ++w) r += sh[w];
-  return r;
-}
-
-// Sum of the mask, for calls without a global token count.
-__global__ __launch_bounds__(kLossThreads) void k_mask_count(const uint8_t* mask, int64_t T, int64_t* part) {
-  __shared__ int64_t sh[kLossThreads / 64];
-  int64_t c = 0;
-  for (int64_t t = static_cast<int64_t>(blockIdx.x) * kLossThreads + threadIdx.x; t < T;
-       t += static_cast<int64_t>(gridDim.x) * kLossThreads)
-    c += mask[t] != 0 ? 1 : 0;
-  c = block_sum(c, sh);
-  if (threadIdx.x == 0) part[blockIdx.x] = c;
-}
-
-__global__ __launch_bounds__(kLossThreads) void k_count_total(const int64_t* part, int nblk, int64_t* total) {
-  __shared__ int64_t sh[kLossThreads / 64];
-  int64_t c = 0;
-  for (int i = threadIdx.x; i < nblk; i += kLossThreads) c += part[i];
-  c = block_sum(c, sh);
-  if (threadIdx.x == 0) *total = c;
-}
 
 __global__ __launch_bounds__(kLossThreads) void k_loss(const float* logp, const float* lro, const float* adv,
                                                        const uint8_t* mask, int64_t T, float eps_low,
@@ -85,11 +54,11 @@ __global__ __launch_bounds__(kLossThreads) void k_loss(const float* logp, const 
     }
     g[t] = gt;
   }
-  sL = block_sum(sL, shd);
-  sS = block_sum(sS, shd);
+  sL = block_sum<kLossThreads>(sL, shd);
+  sS = block_sum<kLossThreads>(sS, shd);
   int64_t tot[5];
 #pragma unroll
-  for (int i = 0; i < 5; ++i) tot[i] = block_sum(c[i], shi);
+  for (int i = 0; i < 5; ++i) tot[i] = block_sum<kLossThreads>(c[i], shi);
   if (threadIdx.x == 0) {
     part_f[2 * blockIdx.x] = sL;
     part_f[2 * blockIdx.x + 1] = sS;
@@ -111,11 +80,11 @@ __global__ __launch_bounds__(kLossThreads) void k_loss_final(const double* part_
 #pragma unroll
     for (int k = 0; k < 5; ++k) c[k] += part_i[5 * i + k];
   }
-  sL = block_sum(sL, shd);
-  sS = block_sum(sS, shd);
+  sL = block_sum<kLossThreads>(sL, shd);
+  sS = block_sum<kLossThreads>(sS, shd);
   int64_t tot[5];
 #pragma unroll
-  for (int k = 0; k < 5; ++k) tot[k] = block_sum(c[k], shi);
+  for (int k = 0; k < 5; ++k) tot[k] = block_sum<kLossThreads>(c[k], shi);
   if (threadIdx.x == 0) {
     const int64_t N = *n_ptr;
     if (N > 0) {
@@ -138,8 +107,8 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const float
   const int64_t* n_ptr = n_tokens;
   if (!n_ptr) {
     int64_t* total = reinterpret_cast<int64_t*>(w8 + L.n_count);
-    hipLaunchKernelGGL(k_mask_count, dim3(nblk), dim3(kLossThreads), 0, st, mask, T, part_i);
-    hipLaunchKernelGGL(k_count_total, dim3(1), dim3(kLossThreads), 0, st, part_i, nblk, total);
+    hipLaunchKernelGGL(k_mask_count<kLossThreads>, dim3(nblk), dim3(kLossThreads), 0, st, mask, T, part_i);
+    hipLaunchKernelGGL(k_count_total<kLossThreads>, dim3(1), dim3(kLossThreads), 0, st, part_i, nblk, total);
     n_ptr = total;
   }
   hipLaunchKernelGGL(k_loss, dim3(nblk), dim3(kLossThreads), 0, st, logp, logp_rollout, adv, mask, T,

@@ -109,6 +109,30 @@ def test_backward_validation(L):
     assert bwd(T=0) == OK
 
 
+def test_value_validation(L):
+    def fwd(hidden=FAKE, w=FAKE, v=FAKE, T=16, H=64, ld=64, dt=0):
+        return L.sao_value_forward(hidden, ld, w, T, H, dt, v, None, 0, None)
+    assert fwd(hidden=None) == ERR_NULL
+    assert fwd(v=None) == ERR_NULL
+    assert fwd(H=12, ld=16) == ERR_SHAPE
+    assert fwd(ld=32) == ERR_SHAPE
+    assert fwd(w=FAKE_ODD) == ERR_SHAPE
+    assert fwd(dt=5) == ERR_DTYPE
+    assert fwd(T=-2) == ERR_SHAPE
+    assert fwd(T=0) == OK
+
+    def vl(dh=FAKE, ret=FAKE, T=16, H=64, ws=FAKE, ws_bytes=1 << 30, dt=0):
+        return L.sao_value_loss(FAKE, H, FAKE, FAKE, ret, FAKE, T, H, None, dt, FAKE, dh, FAKE, ws, ws_bytes, None)
+    assert vl(ret=None) == ERR_NULL
+    assert vl(dh=None) == ERR_NULL
+    assert vl(dh=FAKE_ODD) == ERR_SHAPE
+    assert vl(H=0) == ERR_SHAPE
+    assert vl(dt=3) == ERR_DTYPE
+    assert vl(ws_bytes=8) == ERR_WORKSPACE
+    assert vl(ws=None) == ERR_NULL
+    assert vl(T=0) == OK
+
+
 def test_workspace_sizes(L):
     ws = binding.workspace_size
     assert ws(binding.OP_ADVANTAGE, 1000, 1, 1, 0) == 256
@@ -120,3 +144,5 @@ def test_workspace_sizes(L):
     big = ws(binding.OP_BACKWARD, 65536, 2048, 151936, 0)
     assert big < 65536 * 151936 * 2 // 2
     assert ws(binding.OP_LOSS, 1 << 26, 1, 1, 1) < 1 << 20
+    # value loss: per-128-row partials of dw_v, far below the hidden states themselves
+    assert 0 < ws(binding.OP_VALUE, 32768, 6144, 1, 0) < 32768 * 6144 * 2 // 16

@@ -12,7 +12,8 @@ import torch
 
 import oracle
 from synth import CONFIGS, generate, rollout_logprobs
-from tests.gpu_common import TOL_ADV, TOL_G, TOL_LOGP, check_grad, check_loss, gpu_pass, say
+from tests.gpu_common import (TOL_ADV, TOL_G, TOL_LOGP, check_grad, check_loss, check_value, gpu_pass,
+                               say)
 from tests.golden.make_full_logprobs import load as load_golden, path_for
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
@@ -29,14 +30,15 @@ def _full(name, backward, n_rows=24, seed=0):
     say(f"{name}: generating T={cfg.T} H={cfg.H} V={cfg.V}")
     b = generate(cfg)
     ref_lp, ref_lse = load_golden(name, b)
-    say(f"{name}: GPU pass")
-    got = gpu_pass(b, ref_lp, cfg.gamma, cfg.lam, cfg.alpha, backward)
+    say(f"{name}: GPU pass" + (f" in chunks of {cfg.chunk}" if cfg.chunk else ""))
+    got = gpu_pass(b, ref_lp, cfg.gamma, cfg.lam, cfg.alpha, backward, chunk=cfg.chunk)
     m = b.mask == 1
     say(f"{name}: compare logp on {int(m.sum())} rows")
     assert np.abs(got["logp"][m] - ref_lp[m]).max() <= TOL_LOGP
     assert np.abs(got["lse"][m] - ref_lse[m]).max() <= TOL_LOGP
     assert (got["logp"][~m] == 0).all()
-    adv, ret, N = oracle.advantage(b.values, b.rewards, b.mask, b.cu_seqlens, cfg.gamma, cfg.lam, cfg.alpha)
+    values = oracle.value_forward(b.hidden, b.w_value) if cfg.value_head else b.values
+    adv, ret, N = oracle.advantage(values, b.rewards, b.mask, b.cu_seqlens, cfg.gamma, cfg.lam, cfg.alpha)
     assert int(got["n"][0]) == N
     assert (np.abs(got["adv"] - adv) <= TOL_ADV * np.maximum(1, np.abs(adv))).all()
     assert (np.abs(got["ret"] - ret) <= TOL_ADV * np.maximum(1, np.abs(ret))).all()
@@ -47,9 +49,15 @@ def _full(name, backward, n_rows=24, seed=0):
     check_loss(got, dict(loss=loss, flags=flags), ref_lp, lro, adv, b.mask, N)
     assert (np.abs(got["g"] - g) <= TOL_G * np.abs(g) + 1e-12).all()
     say(f"{name}: forward ok, clipped {counts[2] + counts[3]} of {counts[0]}")
+    rng = np.random.default_rng(seed)
+    if cfg.value_head:
+        lv, dhv, dwv = oracle.value_loss(b.hidden, b.w_value, values, ret, b.mask, N)
+        vrow = np.sort(rng.choice(np.nonzero(b.mask)[0], size=n_rows, replace=False))
+        check_value(got, dict(v=values, lv=lv, dhv=dhv, dwv=dwv), b.mask, rows=vrow)
+        del dhv
+        say(f"{name}: critic ok")
     if not backward:
         return
-    rng = np.random.default_rng(seed)
     live = np.nonzero(g)[0]
     rows = np.sort(rng.choice(live, size=n_rows, replace=False))
     vrows = np.unique(np.concatenate([b.target[rows[:n_rows // 2]], rng.choice(cfg.V, n_rows, replace=False),
@@ -74,3 +82,13 @@ def test_c2_full_forward_backward():
 @pytest.mark.skipif(not __import__("os").path.exists(path_for("c1")), reason="stored oracle values missing")
 def test_c1_full_forward():
     _full("c1", backward=False)
+
+
+@pytest.mark.skipif(not __import__("os").path.exists(path_for("c4")), reason="stored oracle values missing")
+def test_c4_full_forward_backward_value_head():
+    _full("c4", backward=True)
+
+
+@pytest.mark.skipif(not __import__("os").path.exists(path_for("c3")), reason="stored oracle values missing")
+def test_c3_full_chunked_forward_backward():
+    _full("c3", backward=True)

@@ -12,7 +12,7 @@ import oracle
 import paper_2607_07508_amd as sao
 from synth import CONFIGS, generate, rollout_logprobs, small_config, with_overrides
 from synth.device import to_device
-from tests.gpu_common import (TOL_LOGP, check_grad, compare_all, gpu_pass, oracle_pass, say)
+from tests.gpu_common import (TOL_LOGP, TOL_LOSS, TOL_V, check_grad, compare_all, gpu_pass, oracle_pass, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -160,3 +160,44 @@ def test_malformed_segments_set_status():
     torch.cuda.synchronize()
     assert int(status) & sao.binding.STATUS_SEGMENTS
     assert np.isnan(adv.cpu().numpy()).any()
+
+
+@pytest.mark.parametrize("case", [
+    dict(name="v1", seed=31, B=4, T=900, H=320, V=700, value_head=True),
+    dict(name="v2", seed=32, B=3, T=500, H=72, V=300, dtype="f32", value_head=True),      # H % 32 != 0
+    dict(name="v3", seed=33, B=8, T=2500, H=512, V=4000, eps_high=0.28, value_head=True),  # c4's shape mix
+])
+def test_value_head(case):
+    """Critic values feed the scan; its squared-error loss and gradients."""
+    _roundtrip(small_config(**case), 1.0, 1.0, 1.5)
+
+
+def test_value_loss_local_count_and_masked_rows():
+    b = generate(small_config("vmask", 34, B=3, T=600, H=96, V=200, value_head=True))
+    b.mask[:200] = 0
+    ref = oracle_pass(b, 1.0, 1.0, 1.5, backward=False)
+    db = to_device(b, ref["logp"])
+    v = sao.value_forward(db.hidden, db.w_value)
+    adv, ret, n = sao.advantage(v, db.rewards, db.mask, db.cu_seqlens, 1.0, 1.0, 1.5)
+    lv_g, dh_g, dw_g = sao.value_loss(db.hidden, db.w_value, v, ret, db.mask, n)
+    lv_l, dh_l, dw_l = sao.value_loss(db.hidden, db.w_value, v, ret, db.mask, None)   # N = sum(mask)
+    # a second call accumulates into the loss and dw_v
+    sao.value_loss(db.hidden, db.w_value, v, ret, db.mask, n, loss=lv_g, dw_value=dw_g)
+    torch.cuda.synchronize()
+    assert torch.equal(dh_g, dh_l) and (dh_g[:200] == 0).all()
+    assert abs(float(lv_g) - 2 * float(lv_l)) <= 1e-12 * abs(float(lv_l))
+    assert abs(float(lv_l) - ref["lv"]) <= TOL_LOSS * abs(ref["lv"])
+    check_grad(dw_g.cpu().numpy()[None, :], 2 * ref["dwv"][None, :], None, "dw_v x2")
+    assert (np.abs(v.cpu().numpy() - ref["v"]) <= TOL_V * np.maximum(1, np.abs(ref["v"]))).all()
+
+
+def test_value_loss_all_masked():
+    b = generate(small_config("vzero", 35, B=2, T=300, H=64, V=100, value_head=True))
+    b.mask[:] = 0
+    db = to_device(b)
+    v = sao.value_forward(db.hidden, db.w_value)
+    ret = torch.randn(b.T, device="cuda")
+    dw0 = torch.full((b.cfg.H,), 0.25, dtype=torch.float32, device="cuda")
+    lv, dh, dw = sao.value_loss(db.hidden, db.w_value, v, ret, db.mask, None, dw_value=dw0)
+    torch.cuda.synchronize()
+    assert float(lv) == 0.0 and (dh == 0).all() and (dw == 0.25).all()
