@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "tokens/s SAO logprob+clipped-loss fwd+bwd (H2048,V152k); % bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA, TFLOP/s
+PEAK_HBM_GBS = 8000.0              # MI355X HBM3E, GB/s
 WORKLOAD_TEXT = {
     "c2": "16 single rollouts, T=65536, H=2048, V=151936, bf16, fwd+bwd, ~30% observation tokens, "
           "drift sigma 0.2, eps 0.2/0.2, gamma 1, alpha 1.5",
@@ -72,6 +73,69 @@ def copy_calibration(nbytes: int = 1 << 30):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes": nbytes, "launches": 3}), flush=True)
+
+
+def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
+    """Achieved HBM bandwidth of the scan (sao_advantage) and the loss epilogue
+    (sao_clipped_loss) at T = 2^e tokens, B = T/4096 trajectories, c2's span mix.
+    Algorithmic bytes: 17 per token for the scan (values, rewards, mask in; adv,
+    ret out), 18 for the loss (logp, logp_rollout, adv, mask in; g, flags out).
+    One JSON line per size."""
+    import torch
+    import paper_2607_07508_amd as sao
+    from paper_2607_07508_amd import binding as B
+    from synth import generate, small_config
+    from synth.device import to_device
+    if not torch.cuda.is_available():
+        print("the sweep needs a HIP device", file=sys.stderr)
+        sys.exit(1)
+    for e in exps:
+        T = 1 << e
+        cfg = small_config(f"sweep{e}", 2000 + e, B=T // 4096, T=T, H=8, V=16,
+                           length=("lognormal", 4096, 0.5, 16384), act_span=(800, 2400), obs_span=(64, 2048))
+        log(f"sweep T=2^{e}: generating")
+        b = generate(cfg, with_head=False)
+        db = to_device(b)
+        g = torch.Generator(device="cpu").manual_seed(e)
+        logp = (-torch.rand(T, generator=g) * 4.0).to("cuda")
+        lro = logp + torch.from_numpy(b.xi).float().to("cuda")
+        L = sao.lib()
+        f32 = dict(dtype=torch.float32, device="cuda")
+        adv, ret, g_out = torch.empty(T, **f32), torch.empty(T, **f32), torch.empty(T, **f32)
+        flags = torch.empty(T, dtype=torch.uint8, device="cuda")
+        n = torch.zeros(1, dtype=torch.int64, device="cuda")
+        loss = torch.zeros(2, dtype=torch.float64, device="cuda")
+        counts = torch.zeros(5, dtype=torch.int64, device="cuda")
+        ws_bytes = max(B.workspace_size(B.OP_ADVANTAGE, T, 1, 1, B.SAO_F32),
+                       B.workspace_size(B.OP_LOSS, T, 1, 1, B.SAO_F32))
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+        st = torch.cuda.current_stream().cuda_stream
+        p = lambda t: t.data_ptr()  # noqa: E731
+
+        def scan():
+            B._check(L.sao_advantage(p(db.values), p(db.rewards), p(db.mask), p(db.cu_seqlens), cfg.B, T, 1.0, 1.0,
+                                     1.5, p(adv), p(ret), p(n), None, p(ws), ws_bytes, st))
+
+        def epilogue():
+            B._check(L.sao_clipped_loss(p(logp), p(lro), p(adv), p(db.mask), T, 0.2, 0.2, p(n), p(loss), p(g_out),
+                                        p(flags), p(counts), p(ws), ws_bytes, st))
+        out = {}
+        for name, fn, nbytes in (("advantage", scan, 17 * T), ("clipped_loss", epilogue, 18 * T)):
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                fn()
+            z.record()
+            torch.cuda.synchronize()
+            ms = a.elapsed_time(z) / reps
+            out[name] = {"ms": ms, "GB/s": nbytes / ms / 1e6, "frac_hbm": nbytes / ms / 1e6 / PEAK_HBM_GBS,
+                         "bytes": nbytes}
+        print(json.dumps({"mode": "epilogue_sweep", "T": T, "B": cfg.B, **out}), flush=True)
+        del db, b, logp, lro, adv, ret, g_out, flags, ws
+        torch.cuda.empty_cache()
 
 
 def log(msg):
@@ -119,13 +183,18 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_TEXT))
-    ap.add_argument("--cpu-rows", type=int, default=256, help="loss-mask tokens in the oracle sample")
+    ap.add_argument("--cpu-rows", type=int, default=2048, help="loss-mask tokens in the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--epilogue-sweep", action="store_true",
+                    help="HBM bandwidth of the scan and loss epilogue at T = 2^20 .. 2^26 (one line per size)")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.epilogue_sweep:
+        epilogue_sweep()
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

@@ -12,9 +12,11 @@
 // rewards before the first action leave through the left end and are dropped).
 // Every such map, and every composition of them, has the form
 //   Vn' = pV Vn + cV,  R' = pR R + cR,  A' = aV Vn + aR R + aA A + cA,  G' = gR R + gG G + cG,
-// so a thread summarises its contiguous chunk by 11 numbers, the block scans the
+// so a thread summarises its contiguous tokens by 11 numbers, the block scans the
 // summaries (wave shuffles, then across waves through LDS), and each thread
-// replays its chunk from the exact state that enters it. Arithmetic is float64.
+// replays its tokens from the exact state that enters it. Arithmetic is float64.
+// Tiles of 2048 tokens aligned to the global index give every thread 8 tokens
+// that it reads and writes with 16-byte vector accesses.
 #include "common.hpp"
 #include "launch.hpp"
 #include "../../include/sao.h"
@@ -89,13 +91,35 @@ __global__ __launch_bounds__(256) void k_check_segments(const int32_t* cu, int32
 }
 
 constexpr int kScanThreads = 256;
+constexpr int kScanPer = 8;                               // tokens per thread per tile
+constexpr int kScanTile = kScanThreads * kScanPer;        // tokens per tile
 
+// State after applying map M to (Vn, R, A, G).
+struct St {
+  double Vn, R, A, G;
+};
+__device__ __forceinline__ St apply(const Aff& M, const St& s) {
+  St o;
+  o.Vn = fma(M.pV, s.Vn, M.cV);
+  o.R = fma(M.pR, s.R, M.cR);
+  o.A = fma(M.aV, s.Vn, fma(M.aR, s.R, fma(M.aA, s.A, M.cA)));
+  o.G = fma(M.gR, s.R, fma(M.gG, s.G, M.cG));
+  return o;
+}
+
+// One workgroup per trajectory. The trajectory is walked right to left in tiles
+// of kScanTile tokens aligned to the global token index (so that each thread's
+// kScanPer tokens are one aligned vector load per array); the state leaving a
+// tile on the left enters the next tile from the right. Inside a tile each
+// thread composes the maps of its tokens, the block scans the compositions,
+// and each thread replays its tokens from the exact entering state.
 __global__ __launch_bounds__(kScanThreads) void k_advantage(
     const float* values, const float* rewards, const uint8_t* mask, const int32_t* cu, int32_t B,
     int64_t T, double gamma, double lam, double alpha, float* adv, float* ret, int64_t* n_tokens,
-    const int32_t* bad) {
+    const int32_t* bad, bool vec_ok) {
   __shared__ Aff s_agg[kScanThreads / 64];
   __shared__ int64_t s_cnt[kScanThreads / 64];
+  __shared__ St s_carry;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
   if (*bad) {
@@ -114,79 +138,123 @@ __global__ __launch_bounds__(kScanThreads) void k_advantage(
   }
   const int64_t s = cu[b], e = cu[b + 1];
   const int64_t L = e - s;
-  if (L == 0) return;
+  if (L <= 0) return;
   double lam_b = lam;
   if (alpha > 0.0) {
     lam_b = 1.0 - 1.0 / (alpha * static_cast<double>(L));
     if (lam_b < 0.0) lam_b = 0.0;
   }
   const double kappa = gamma * lam_b;
-  const int64_t chunk = (L + kScanThreads - 1) / kScanThreads;
-  const int64_t c0 = s + tid * chunk;
-  const int64_t c1 = c0 + chunk < e ? c0 + chunk : e;
-
-  // Pass 1: this thread's chunk as one map, and its action count.
-  Aff F = aff_identity();
-  int64_t cnt = 0;
-  for (int64_t t = c1 - 1; t >= c0; --t) {
-    const bool act = mask[t] != 0;
-    cnt += act ? 1 : 0;
-    F = compose(token_map(act, values[t], rewards[t], gamma, kappa), F);
-  }
-
-  // Reverse inclusive scan inside the wave: P_l = F_l o F_{l+1} o ... o F_63.
-  Aff P = F;
+  const int64_t first = s / kScanTile * kScanTile;           // aligned tile containing s
+  int64_t total = 0;
+  St carry{0.0, 0.0, 0.0, 0.0};                               // nothing after the last token
+  for (int64_t t0 = (e - 1) / kScanTile * kScanTile; t0 >= first; t0 -= kScanTile) {
+    const int64_t c0 = t0 + static_cast<int64_t>(tid) * kScanPer;   // this thread's aligned block
+    // Tokens of the block inside [s, e), and whether the whole block is (then vector
+    // access, when the array bases allow it).
+    const bool full = vec_ok && c0 >= s && c0 + kScanPer <= e;
+    float v[kScanPer], r[kScanPer];
+    bool act[kScanPer];
+    if (full) {
+      const f32x4_t* pv = reinterpret_cast<const f32x4_t*>(values + c0);
+      const f32x4_t* pr = reinterpret_cast<const f32x4_t*>(rewards + c0);
+      const f32x4_t v0 = pv[0], v1 = pv[1], r0 = pr[0], r1 = pr[1];
+      const uint2 m8 = *reinterpret_cast<const uint2*>(mask + c0);
 #pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const Aff o = shfl_down_aff(P, d);
-    if (lane + d < 64) P = compose(P, o);
-  }
-  const int64_t wcnt = wave_sum(cnt);
-  if (lane == 0) {
-    s_agg[wave] = P;
-    s_cnt[wave] = wcnt;
-  }
-  __syncthreads();
-  // State entering this wave from the right: later waves applied to the zero state.
-  double sV = 0.0, sR = 0.0, sA = 0.0, sG = 0.0;
-  for (int w = kScanThreads / 64 - 1; w > wave; --w) {
-    const Aff& M = s_agg[w];
-    const double nV = fma(M.pV, sV, M.cV);
-    const double nR = fma(M.pR, sR, M.cR);
-    const double nA = fma(M.aV, sV, fma(M.aR, sR, fma(M.aA, sA, M.cA)));
-    const double nG = fma(M.gR, sR, fma(M.gG, sG, M.cG));
-    sV = nV; sR = nR; sA = nA; sG = nG;
-  }
-  // State entering this thread: lanes to its right inside the wave, then the rest.
-  const Aff Q = shfl_down_aff(P, 1);
-  double Vn = sV, R = sR, A = sA, G = sG;
-  if (lane < 63) {
-    Vn = fma(Q.pV, sV, Q.cV);
-    R = fma(Q.pR, sR, Q.cR);
-    A = fma(Q.aV, sV, fma(Q.aR, sR, fma(Q.aA, sA, Q.cA)));
-    G = fma(Q.gR, sR, fma(Q.gG, sG, Q.cG));
-  }
-
-  // Pass 2: replay the chunk from that state and write the outputs.
-  for (int64_t t = c1 - 1; t >= c0; --t) {
-    const double r = rewards[t];
-    if (mask[t] != 0) {
-      const double v = values[t];
-      const double rt = r + R;
-      const double An = fma(kappa, A, fma(gamma, Vn, rt - v));
-      const double Gn = fma(gamma, G, rt);
-      adv[t] = static_cast<float>(An);
-      ret[t] = static_cast<float>(Gn);
-      Vn = v;
-      R = 0.0;
-      A = An;
-      G = Gn;
+      for (int j = 0; j < 4; ++j) {
+        v[j] = v0[j]; v[4 + j] = v1[j]; r[j] = r0[j]; r[4 + j] = r1[j];
+        act[j] = ((m8.x >> (8 * j)) & 0xffu) != 0;
+        act[4 + j] = ((m8.y >> (8 * j)) & 0xffu) != 0;
+      }
     } else {
-      R += r;
-      adv[t] = 0.0f;
-      ret[t] = 0.0f;
+#pragma unroll
+      for (int j = 0; j < kScanPer; ++j) {
+        const int64_t t = c0 + j;
+        const bool in = t >= s && t < e;
+        v[j] = in ? values[t] : 0.0f;
+        r[j] = in ? rewards[t] : 0.0f;
+        act[j] = in && mask[t] != 0;
+      }
     }
+    // Pass 1: this thread's tokens as one map (tokens outside [s, e) are identities).
+    Aff F = aff_identity();
+    int64_t cnt = 0;
+#pragma unroll
+    for (int j = kScanPer - 1; j >= 0; --j) {
+      const bool in = full || (c0 + j >= s && c0 + j < e);
+      if (!in) continue;
+      cnt += act[j] ? 1 : 0;
+      F = compose(token_map(act[j], v[j], r[j], gamma, kappa), F);
+    }
+    total += cnt;
+    // Reverse inclusive scan inside the wave: P_l = F_l o F_{l+1} o ... o F_63.
+    Aff P = F;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const Aff o = shfl_down_aff(P, d);
+      if (lane + d < 64) P = compose(P, o);
+    }
+    __syncthreads();  // the previous tile's readers of s_agg / s_carry are done
+    if (lane == 0) s_agg[wave] = P;
+    if (tid == 0) s_carry = carry;
+    __syncthreads();
+    // State entering this wave from the right: the carry through later waves.
+    St sw = s_carry;
+    for (int w = kScanThreads / 64 - 1; w > wave; --w) sw = apply(s_agg[w], sw);
+    // State entering this thread: lanes to its right inside the wave, then the rest.
+    const Aff Q = shfl_down_aff(P, 1);
+    St st = lane < 63 ? apply(Q, sw) : sw;
+    // Pass 2: replay the tokens from that state and write the outputs.
+    float oa[kScanPer], og[kScanPer];
+#pragma unroll
+    for (int j = kScanPer - 1; j >= 0; --j) {
+      oa[j] = 0.0f;
+      og[j] = 0.0f;
+      const bool in = full || (c0 + j >= s && c0 + j < e);
+      if (!in) continue;
+      const double rr = r[j];
+      if (act[j]) {
+        const double vv = v[j];
+        const double rt = rr + st.R;
+        const double An = fma(kappa, st.A, fma(gamma, st.Vn, rt - vv));
+        const double Gn = fma(gamma, st.G, rt);
+        oa[j] = static_cast<float>(An);
+        og[j] = static_cast<float>(Gn);
+        st.Vn = vv;
+        st.R = 0.0;
+        st.A = An;
+        st.G = Gn;
+      } else {
+        st.R += rr;
+      }
+    }
+    if (full) {
+      f32x4_t* qa = reinterpret_cast<f32x4_t*>(adv + c0);
+      f32x4_t* qg = reinterpret_cast<f32x4_t*>(ret + c0);
+      qa[0] = f32x4_t{oa[0], oa[1], oa[2], oa[3]};
+      qa[1] = f32x4_t{oa[4], oa[5], oa[6], oa[7]};
+      qg[0] = f32x4_t{og[0], og[1], og[2], og[3]};
+      qg[1] = f32x4_t{og[4], og[5], og[6], og[7]};
+    } else {
+#pragma unroll
+      for (int j = 0; j < kScanPer; ++j) {
+        const int64_t t = c0 + j;
+        if (t >= s && t < e) {
+          adv[t] = oa[j];
+          ret[t] = og[j];
+        }
+      }
+    }
+    // The state leaving this tile on the left (thread 0's final state) is the next carry.
+    __syncthreads();
+    if (tid == 0) s_carry = st;
+    __syncthreads();
+    carry = s_carry;
   }
+  const int64_t wcnt = wave_sum(total);
+  __syncthreads();
+  if (lane == 0) s_cnt[wave] = wcnt;
+  __syncthreads();
   if (tid == 0 && n_tokens) {
     int64_t tot = 0;
     for (int w = 0; w < kScanThreads / 64; ++w) tot += s_cnt[w];
@@ -200,8 +268,12 @@ hipError_t launch_advantage(const float* values, const float* rewards, const uin
                             void* ws, hipStream_t st) {
   int32_t* bad = static_cast<int32_t*>(ws);
   hipLaunchKernelGGL(k_check_segments, dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, n_tokens, status);
+  // Vector access needs 16-byte aligned float arrays and an 8-byte aligned mask.
+  const uintptr_t f = reinterpret_cast<uintptr_t>(values) | reinterpret_cast<uintptr_t>(rewards) |
+                      reinterpret_cast<uintptr_t>(adv) | reinterpret_cast<uintptr_t>(ret);
+  const bool vec_ok = (f & 15u) == 0 && (reinterpret_cast<uintptr_t>(mask) & 7u) == 0;
   hipLaunchKernelGGL(k_advantage, dim3(B), dim3(kScanThreads), 0, st, values, rewards, mask, cu_seqlens,
-                     B, T, gamma, lam, alpha, adv, ret, n_tokens, bad);
+                     B, T, gamma, lam, alpha, adv, ret, n_tokens, bad, vec_ok);
   return hipGetLastError();
 }
 
