@@ -299,8 +299,8 @@ __device__ __forceinline__ void store4(typename E::storage* p, const float (&d)[
 
 template <>
 __device__ __forceinline__ void store4<BF16>(uint16_t* p, const float (&d)[4]) {
-  const uint32_t lo = static_cast<uint32_t>(f32_to_bf16(d[0])) | (static_cast<uint32_t>(f32_to_bf16(d[1])) << 16);
-  const uint32_t hi = static_cast<uint32_t>(f32_to_bf16(d[2])) | (static_cast<uint32_t>(f32_to_bf16(d[3])) << 16);
+  const uint32_t lo = pack_bf16x2(d[0], d[1]);
+  const uint32_t hi = pack_bf16x2(d[2], d[3]);
   *reinterpret_cast<uint2*>(p) = make_uint2(lo, hi);
 }
 
@@ -390,10 +390,8 @@ struct EpiDz {
             const int vl = acc_row(wm, mi, 4 * j, lane);   // multiple of 4
             float d[4];
             dz4(acc, mi, ni, j, m0 + vl, d);
-            const uint32_t lo = static_cast<uint32_t>(f32_to_bf16(d[0])) |
-                                (static_cast<uint32_t>(f32_to_bf16(d[1])) << 16);
-            const uint32_t hi = static_cast<uint32_t>(f32_to_bf16(d[2])) |
-                                (static_cast<uint32_t>(f32_to_bf16(d[3])) << 16);
+            const uint32_t lo = pack_bf16x2(d[0], d[1]);
+            const uint32_t hi = pack_bf16x2(d[2], d[3]);
             uint2* p = reinterpret_cast<uint2*>(tile16 + t * 32 + tswz(t, vl >> 3)) + ((vl >> 2) & 1);
             *p = make_uint2(lo, hi);
           }

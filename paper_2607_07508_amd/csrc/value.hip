@@ -28,7 +28,7 @@ __device__ __forceinline__ v4u narrow(const float (&f)[8], BF16) {
   v4u x;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
-    x[i] = static_cast<uint32_t>(f32_to_bf16(f[2 * i])) | (static_cast<uint32_t>(f32_to_bf16(f[2 * i + 1])) << 16);
+    x[i] = pack_bf16x2(f[2 * i], f[2 * i + 1]);
   return x;
 }
 __device__ __forceinline__ v4u narrow(const float (&f)[4], F32) {

@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import paper_2607_07508_amd as sao
-from synth import CONFIGS, generate, rollout_logprobs, small_config, with_overrides
+from synth import CONFIGS, bf16_bits, bf16_round, generate, rollout_logprobs, small_config, with_overrides
 from synth.device import to_device
 from tests.gpu_common import (TOL_LOGP, TOL_LOSS, TOL_V, check_grad, compare_all, gpu_pass, oracle_pass, say)
 
@@ -201,3 +201,23 @@ def test_value_loss_all_masked():
     lv, dh, dw = sao.value_loss(db.hidden, db.w_value, v, ret, db.mask, None, dw_value=dw0)
     torch.cuda.synchronize()
     assert float(lv) == 0.0 and (dh == 0).all() and (dw == 0.25).all()
+
+
+def test_value_dhidden_is_rne_of_fp32_product():
+    """dH_v = bf16(dv * w_v): the kernel's fp32 product rounded to nearest even, bit for bit."""
+    b = generate(small_config("vrne", 36, B=3, T=700, H=256, V=100, value_head=True))
+    db = to_device(b)
+    rng = np.random.default_rng(36)
+    ret_h = rng.normal(0.5, 0.5, b.T).astype(np.float32)
+    v = sao.value_forward(db.hidden, db.w_value)
+    _, dh, _ = sao.value_loss(db.hidden, db.w_value, v, torch.from_numpy(ret_h).cuda(), db.mask, None)
+    torch.cuda.synchronize()
+    m = b.mask != 0
+    N = int(m.sum())
+    d64 = v.cpu().numpy().astype(np.float64) - ret_h.astype(np.float64)
+    dv = np.where(m, (2.0 * d64 * (1.0 / N)).astype(np.float32), np.float32(0.0))
+    prod = dv[:, None] * b.w_value[None, :].astype(np.float32)
+    want = bf16_bits(bf16_round(prod))
+    want[~m] = 0
+    got = dh.view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got, want), int((got != want).sum())
