@@ -75,6 +75,27 @@ def copy_calibration(nbytes: int = 1 << 30):
     print(json.dumps({"copy_bytes": nbytes, "launches": 3}), flush=True)
 
 
+def vendor_gemm(db, t_act: int, torch, reps: int = 3):
+    """torch.matmul (hipBLASLt) in bf16 at the forward's shape (T_act x H) . (H x V), bf16 out: a
+    library GEMM on the same operands, for context only (it is run, never inspected)."""
+    h = db.hidden[:t_act].contiguous()
+    w_t = db.w_head.t().contiguous()
+    out = torch.matmul(h, w_t)
+    torch.cuda.synchronize()
+    a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        torch.matmul(h, w_t, out=out)
+    z.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(z) / reps
+    flops = 2.0 * t_act * w_t.shape[1] * h.shape[1]
+    del out, w_t, h
+    torch.cuda.empty_cache()
+    return {"op": "torch.matmul bf16 (T_act x H) @ (H x V)", "ms": ms, "TFLOP/s": flops / ms / 1e9,
+            "frac": flops / ms / 1e9 / PEAK_BF16_TFLOPS}
+
+
 def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
     """Achieved HBM bandwidth of the scan (sao_advantage) and the loss epilogue
     (sao_clipped_loss) at T = 2^e tokens, B = T/4096 trajectories, c2's span mix.
@@ -183,10 +204,12 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_TEXT))
-    ap.add_argument("--cpu-rows", type=int, default=2048, help="loss-mask tokens in the oracle sample")
+    ap.add_argument("--cpu-rows", type=int, default=4096, help="loss-mask tokens in the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--vendor-gemm", action="store_true",
+                    help="also time torch.matmul (bf16) at the forward's shape, as context (allocates the T_act x V output)")
     ap.add_argument("--epilogue-sweep", action="store_true",
                     help="HBM bandwidth of the scan and loss epilogue at T = 2^20 .. 2^26 (one line per size)")
     args = ap.parse_args()
@@ -264,22 +287,24 @@ def main():
 
     fwd_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(args.steps)]
+    step_ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     for a, b in fwd_ev:        # materialise the event handles
         a.record()
         b.record()
+    for a in step_ev:
+        a.record()
     torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
     log(f"timing {args.steps} steps")
     torch.cuda.synchronize()
-    start.record()
+    step_ev[0].record()
     for i in range(args.steps):
         B.time_kernel(B.KERNEL_HEAD_FORWARD, *fwd_ev[i])
         step()
-    stop.record()
+        step_ev[i + 1].record()
     torch.cuda.synchronize()
     B.time_kernel(B.KERNEL_NONE, None, None)
-    ms = start.elapsed_time(stop) / args.steps
+    per_step = [step_ev[i].elapsed_time(step_ev[i + 1]) for i in range(args.steps)]
+    ms = step_ev[0].elapsed_time(step_ev[-1]) / args.steps
     fwd_ms = float(np.mean([a.elapsed_time(b) for a, b in fwd_ev]))
 
     fwd_flops = 2.0 * t_act * V * H
@@ -304,7 +329,15 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": measured_traffic(), "launch_ms": fwd_ms, "flops_per_launch": fwd_flops},
         "algorithmic_mfma_frac": algo_flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        "step_ms": {"median": float(np.median(per_step)), "min": float(np.min(per_step)),
+                    "max": float(np.max(per_step))},
+        "device": {"name": torch.cuda.get_device_properties(dev).name,
+                   "arch": getattr(torch.cuda.get_device_properties(dev), "gcnArchName", ""),
+                   "compute_units": torch.cuda.get_device_properties(dev).multi_processor_count},
     }
+    if args.vendor_gemm:
+        log("vendor GEMM (context)")
+        out["vendor_gemm_context"] = vendor_gemm(db, t_act, torch)
     if not args.no_cpu_baseline:
         log(f"cpu baseline over {args.cpu_rows} rows")
         out["cpu_baseline"] = cpu_baseline(batch, ref_logp, args.cpu_rows)
