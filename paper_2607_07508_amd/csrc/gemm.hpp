@@ -11,10 +11,16 @@
 // MFMAs; the copies of a slab are spread over the MFMAs of the last K step of
 // the slab before it, right after the barrier that frees their stage.
 //
-// Both operands are stored K-contiguous ([mn][k], row stride ld). LDS holds
-// [mn][k] rows of kRowChunks 16-byte chunks, chunk c of row r at position
+// Each operand is stored either K-major ([mn][k], row stride ld) or MN-major
+// ([k][mn], row stride ld), chosen at compile time. A K-major slab sits in LDS
+// as [mn][k] rows of kRowChunks 16-byte chunks, chunk c of row r at position
 // swz(r, c), so that the 16-byte fragment reads of sixteen consecutive lanes
-// touch all 64 banks. The fragments of K step s+1 are read from LDS while step
+// touch all 64 banks. An MN-major slab sits as [k][mn] rows of 256 elements,
+// chunk c of row k at c ^ (4 (k & 3)); bf16 fragments come from it through
+// gfx950's transposing LDS read (ds_read_b64_tr_b16: within each 16 lanes,
+// lane j names 4 elements of row j >> 2 and receives column j of the 4 x 16
+// block that the group names), two reads per 8-element fragment, and the
+// XOR keeps the 32 lanes of each read on distinct banks. The fragments of K step s+1 are read from LDS while step
 // s multiplies, and the workgroup barrier of a slab sits before its last K
 // step, so that the first fragments of the next slab are read while that step
 // multiplies. (Deeper rings of shorter slabs measured slower on gfx950: with
@@ -35,6 +41,8 @@
 // 32/SN tiles); in M-split mode they take different M-tiles of the same N-tiles
 // (SN x 256/SN), so an M-tile's rows are fetched by one XCD only.
 #pragma once
+
+#include <type_traits>
 
 #include "common.hpp"
 
@@ -170,21 +178,82 @@ struct Frags {
   v4u b[kNI];
 };
 
-// Rows read by a lane differ by multiples of 32, which leaves the line index
-// modulo kRowChunks and hence the swizzle unchanged: one LDS address per operand and K step, the
-// blocks at immediate offsets. Chunks past K hold zeros (written by the copy of
-// the last slab), so no fragment needs masking.
-__device__ __forceinline__ void read_frags(Frags& f, const v4u* la, const v4u* lb, int s, int wm, int wn,
-                                           int lane) {
+// K-major fragments of one operand for K step s: blocks of 32 rows at
+// wave_row0 + 32 i. Rows read by a lane differ by multiples of 32, which leaves
+// the line index modulo kRowChunks and hence the swizzle unchanged: one LDS
+// address per step, the blocks at immediate offsets. Chunks past K hold zeros
+// (written by the copy of the last slab), so no fragment needs masking.
+template <int NB>
+__device__ __forceinline__ void read_frag_k(v4u (&f)[NB], const v4u* l, int s, int wave_row0, int lane) {
   const int r32 = lane & 31;
   const int c = 2 * s + (lane >> 5);
-  const int pc = swz(r32, c);
-  const v4u* pa = la + (wm * (kBM / 2) + r32) * kRowChunks + pc;
-  const v4u* pb = lb + (wn * (kBN / kWavesN) + r32) * kRowChunks + pc;
+  const v4u* p = l + (wave_row0 + r32) * kRowChunks + swz(r32, c);
 #pragma unroll
-  for (int i = 0; i < kMI; ++i) f.a[i] = pa[i * 32 * kRowChunks];
+  for (int i = 0; i < NB; ++i) f[i] = p[i * 32 * kRowChunks];
+}
+
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+
+// MN-major slab geometry for element type E: rows of 256 elements.
+template <class E>
+struct MnSlab {
+  static constexpr int kRowBytes = 256 * static_cast<int>(sizeof(typename E::storage));
+  static constexpr int kChunksPerRow = kRowBytes / 16;
+  static constexpr int kRows = kRowChunks * E::kPerChunk;        // K per slab
+  static constexpr int kRowsPerCopy = 1024 / kRowBytes;           // rows filled by one 1 KB copy
+  static_assert(kRows * kRowBytes == kAChunks * 16, "an MN-major slab fills one operand stage");
+};
+__device__ __forceinline__ int mn_swz(int k, int c) { return c ^ (4 * (k & 3)); }
+
+// MN-major fragments of one operand for K step s (same k <-> lane mapping as the
+// K-major path: lane half h holds the k chunk 2 s + h, element e at k offset e).
+template <class E, int NB>
+__device__ __forceinline__ void read_frag_mn(v4u (&f)[NB], const v4u* l, int s, int wave_row0, int lane) {
+  using G = MnSlab<E>;
+  const char* base = reinterpret_cast<const char*>(l);
+  const int h = lane >> 5;
+  if constexpr (sizeof(typename E::storage) == 2) {
+    // Lane j of a 16-lane group names row k0 + (j >> 2), columns m0 + 4 (j & 3) .. +3,
+    // and receives column m0 + j of rows k0 .. k0+3; two reads give rows k0 .. k0+7.
+    const int j = lane & 15;
+    const int k = 8 * (2 * s + h) + (j >> 2);
 #pragma unroll
-  for (int j = 0; j < kNI; ++j) f.b[j] = pb[j * 32 * kRowChunks];
+    for (int i = 0; i < NB; ++i) {
+      const int m = wave_row0 + 32 * i + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+      const int off = k * G::kRowBytes + mn_swz(k, m >> 3) * 16 + (m & 7) * 2;
+      const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(base + off));
+      const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(base + off + 4 * G::kRowBytes));
+      const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+      f[i] = v4u{a.x, a.y, b.x, b.y};
+    }
+  } else {
+    // fp32: element e of the chunk is row 4 (2 s + h) + e of column wave_row0 + 32 i + (lane & 31).
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int m = wave_row0 + 32 * i + (lane & 31);
+      uint32_t x[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int k = 4 * (2 * s + h) + e;
+        x[e] = *reinterpret_cast<const uint32_t*>(base + k * G::kRowBytes + mn_swz(k, m >> 2) * 16 + (m & 3) * 4);
+      }
+      f[i] = v4u{x[0], x[1], x[2], x[3]};
+    }
+  }
+}
+
+template <class E, bool AMn, bool BMn>
+__device__ __forceinline__ void read_frags(Frags& f, const v4u* la, const v4u* lb, int s, int wm, int wn,
+                                           int lane) {
+  if constexpr (AMn)
+    read_frag_mn<E>(f.a, la, s, wm * (kBM / 2), lane);
+  else
+    read_frag_k(f.a, la, s, wm * (kBM / 2), lane);
+  if constexpr (BMn)
+    read_frag_mn<E>(f.b, lb, s, wn * (kBN / kWavesN), lane);
+  else
+    read_frag_k(f.b, lb, s, wn * (kBN / kWavesN), lane);
 }
 
 // The MFMAs of row block i of one K step.
@@ -231,7 +300,7 @@ __device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
 //   tile(acc, m0, n0, wm, wn, lane, lds)    after it (LDS is free)
 //   finish(mt, n0, wm, wn, lane, lds)  last (LDS is free)
 // Both operands are K-contiguous.
-template <class E, class Epi>
+template <class E, bool AMn, bool BMn, class Epi>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*lds)[kStageChunks]) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -266,7 +335,6 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   constexpr int P = E::kPerChunk;
   const int64_t k_chunks = (k_valid + P - 1) / P;          // valid 16-byte chunks per row
   const int nk = static_cast<int>((k_chunks + kRowChunks - 1) / kRowChunks);  // slabs
-  const int c_last = static_cast<int>(k_chunks - static_cast<int64_t>(nk - 1) * kRowChunks);  // 1..kRowChunks
 
   epi.begin(n0, wm, wn, lane);
 
@@ -279,54 +347,80 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   const int esz = static_cast<int>(sizeof(typename E::storage));
   const char* a_base = static_cast<const char*>(s.a);
   const char* b_base = static_cast<const char*>(s.b);
-  // Copy instruction q of this wave covers kRowsPerCopy tile rows from
-  // (wave * Q + q) * kRowsPerCopy; lane l lands on row + l / kRowChunks, physical
-  // chunk l % kRowChunks, so it fetches the logical chunk that the swizzle maps there. Row offsets are 32-bit: operands are
-  // limited to 2^31 elements on the host.
-  constexpr int QA = kBM / kRowsPerCopy / 4;  // copies per wave per A slab
-  constexpr int QB = kBN / kRowsPerCopy / 4;  // copies per wave per B slab
+  using G = MnSlab<E>;
+  // Every 1 KB copy instruction of a wave fills 64 consecutive LDS chunks (lane l
+  // writes chunk l). K-major: copy q covers kRowsPerCopy tile rows from
+  // (wave * Q + q) * kRowsPerCopy, lane l row + l / kRowChunks at physical chunk
+  // l % kRowChunks, fetching the logical chunk swizzled there; lc[q] is that chunk
+  // and off[q] the row's byte offset. MN-major: copy q covers G::kRowsPerCopy slab
+  // rows (k) from (wave * Q + q) * G::kRowsPerCopy, lane l row + l / G::kChunksPerRow
+  // at physical chunk l % G::kChunksPerRow, fetching the logical column chunk
+  // mn_swz maps there; lc[q] is the slab row and off[q] the byte offset of that
+  // row and column in slab 0. Offsets are 32-bit: operands are limited to 2^31
+  // elements on the host. Rows (K-major) or columns (MN-major) past the valid
+  // range read the last valid one; their results are never stored.
+  constexpr int QA = kAChunks / 64 / 4;  // copies per wave per A slab
+  constexpr int QB = kBChunks / 64 / 4;  // copies per wave per B slab
   constexpr int kCopiesPerSlab = QA + QB;
   uint32_t offa[QA], offb[QB];
   int lca[QA], lcb[QB];
+  auto setup = [&](auto mn_major, int Q, int q, int64_t row0, int64_t valid, int64_t ld, uint32_t& off, int& lc) {
+    if constexpr (decltype(mn_major)::value) {
+      const int k = (wave * Q + q) * G::kRowsPerCopy + lane / G::kChunksPerRow;
+      const int c = mn_swz(k, lane % G::kChunksPerRow);
+      int64_t col = row0 + static_cast<int64_t>(c) * P;
+      if (col >= valid) col = (valid - 1) / P * P;
+      lc = k;
+      off = static_cast<uint32_t>((static_cast<int64_t>(k) * ld + col) * esz);
+    } else {
+      const int r = (wave * Q + q) * kRowsPerCopy + lane / kRowChunks;
+      lc = swz(r, lane % kRowChunks);
+      int64_t row = row0 + r;
+      row = row < valid ? row : valid - 1;
+      off = static_cast<uint32_t>(row * ld * esz);
+    }
+  };
 #pragma unroll
-  for (int q = 0; q < QA; ++q) {
-    const int r = (wave * QA + q) * kRowsPerCopy + lane / kRowChunks;
-    lca[q] = swz(r, lane % kRowChunks);
-    int64_t row = m0 + r;
-    row = row < m_valid ? row : m_valid - 1;
-    offa[q] = static_cast<uint32_t>(row * s.lda * esz);
-  }
+  for (int q = 0; q < QA; ++q) setup(std::bool_constant<AMn>{}, QA, q, m0, m_valid, s.lda, offa[q], lca[q]);
 #pragma unroll
-  for (int q = 0; q < QB; ++q) {
-    const int r = (wave * QB + q) * kRowsPerCopy + lane / kRowChunks;
-    lcb[q] = swz(r, lane % kRowChunks);
-    int64_t row = n0 + r;
-    row = row < n_valid ? row : n_valid - 1;
-    offb[q] = static_cast<uint32_t>(row * s.ldb * esz);
-  }
+  for (int q = 0; q < QB; ++q) setup(std::bool_constant<BMn>{}, QB, q, n0, n_valid, s.ldb, offb[q], lcb[q]);
+  // Byte offset of slab kt for copy q, and whether that copy's data lies inside K.
+  const uint32_t slab_a = static_cast<uint32_t>(static_cast<int64_t>(G::kRows) * s.lda * esz);
+  const uint32_t slab_b = static_cast<uint32_t>(static_cast<int64_t>(G::kRows) * s.ldb * esz);
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0]));
-  // Copy q (of QA for A, then QB for B) of slab kt into `stage`. In the last
-  // slab, lanes whose chunk lies past K write zeros to their LDS slot instead.
-  // Chunk 0 of every row is valid, so each copy instruction keeps at least 16
-  // active lanes and is always issued: the vmcnt arithmetic of the ring holds.
   v4u* lds_flat = &lds[0][0];
   auto copy_one = [&](int q, int kt, int stage) {
     const bool is_a = q < QA;
     const int qq = is_a ? q : q - QA;
     const int slot = (is_a ? 0 : kAChunks) + (wave * (is_a ? QA : QB) + qq) * 64;
-    const int64_t c = static_cast<int64_t>(kt) * kRowChunks + (is_a ? lca[qq] : lcb[qq]);
-    dma16(is_a ? a_base : b_base, (is_a ? offa[qq] : offb[qq]) + static_cast<uint32_t>(c * P * esz),
+    const bool mn = is_a ? AMn : BMn;
+    const uint32_t k_off = mn ? static_cast<uint32_t>(kt) * (is_a ? slab_a : slab_b)
+                              : static_cast<uint32_t>((static_cast<int64_t>(kt) * kRowChunks +
+                                                       (is_a ? lca[qq] : lcb[qq])) * P * esz);
+    dma16(is_a ? a_base : b_base, (is_a ? offa[qq] : offb[qq]) + k_off,
           __builtin_amdgcn_readfirstlane(lds0 + static_cast<uint32_t>(stage * kStageChunks + slot) * 16));
   };
+  auto inside_k = [&](int q, int kt) -> bool {
+    const bool is_a = q < QA;
+    const int qq = is_a ? q : q - QA;
+    const int lc = is_a ? lca[qq] : lcb[qq];
+    if (is_a ? AMn : BMn) return static_cast<int64_t>(kt) * G::kRows + lc < k_valid;
+    return static_cast<int64_t>(kt) * kRowChunks + lc < k_chunks;
+  };
+  // The last slab is partial when K ends inside it. Then lanes whose data lies
+  // past K write zeros to their LDS slot instead of copying. A K-major copy
+  // always keeps chunk 0 of its rows, but an MN-major one can lose all its rows:
+  // its instruction is then not issued, so waits that count copies must not
+  // span that slab.
+  const bool tail = k_valid < static_cast<int64_t>(nk) * G::kRows;
   auto copy_slab = [&](int kt, int stage) {
-    if (kt == nk - 1 && c_last < kRowChunks) {
+    if (kt == nk - 1 && tail) {
 #pragma unroll
       for (int q = 0; q < kCopiesPerSlab; ++q) {
         const bool is_a = q < QA;
         const int qq = is_a ? q : q - QA;
         const int slot = (is_a ? 0 : kAChunks) + (wave * (is_a ? QA : QB) + qq) * 64;
-        const int64_t c = static_cast<int64_t>(kt) * kRowChunks + (is_a ? lca[qq] : lcb[qq]);
-        if (c < k_chunks)
+        if (inside_k(q, kt))
           copy_one(q, kt, stage);
         else
           lds_flat[stage * kStageChunks + slot + lane] = zero4();
@@ -345,11 +439,12 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   for (int j = 0; j < kStages; ++j)
     if (j < nk) copy_slab(j, j);
   {
-    const int pending = nk - 1 < kStages - 1 ? nk - 1 : kStages - 1;
+    int pending = nk - 1 < kStages - 1 ? nk - 1 : kStages - 1;
+    if (tail && nk <= kStages) pending = 0;  // the partial slab is among these copies
     wait_slabs_barrier<kCopiesPerSlab>(pending);
   }
   Frags f0, f1;
-  read_frags(f0, lds[0], lds[0] + kAChunks, 0, wm, wn, lane);
+  read_frags<E, AMn, BMn>(f0, lds[0], lds[0] + kAChunks, 0, wm, wn, lane);
   for (int kt = 0; kt < nk; ++kt) {
     const int stage = kt % kStages;
     // K steps 0 .. kSteps-2: the fragments of the next step are read first, then
@@ -358,7 +453,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
     for (int st = 0; st + 1 < kSteps; ++st) {
       Frags& cur = st % 2 == 0 ? f0 : f1;
       Frags& nxt = st % 2 == 0 ? f1 : f0;
-      read_frags(nxt, lds[stage], lds[stage] + kAChunks, st + 1, wm, wn, lane);
+      read_frags<E, AMn, BMn>(nxt, lds[stage], lds[stage] + kAChunks, st + 1, wm, wn, lane);
       pin_order();
       mma_step<E>(acc, cur);
       pin_order();
@@ -372,12 +467,12 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
     // Unconditional, so that the LDS wait counts agree on both paths; after the
     // last slab it reads a drained stage and the values go unused.
     const int nstage = (kt + 1) % kStages;
-    read_frags(f0, lds[nstage], lds[nstage] + kAChunks, 0, wm, wn, lane);
+    read_frags<E, AMn, BMn>(f0, lds[nstage], lds[nstage] + kAChunks, 0, wm, wn, lane);
     pin_order();
     // Full slabs refill the freed stage with copies spread over the last step's
     // MFMAs; the last slab, when K ends inside it, is copied after them with its
     // zero fill.
-    const bool refill = kn < nk - 1 || (kn == nk - 1 && c_last == kRowChunks);
+    const bool refill = kn < nk - 1 || (kn == nk - 1 && !tail);
     constexpr int kPerRow = kCopiesPerSlab / kMI;
     static_assert(kCopiesPerSlab % kMI == 0, "copies spread evenly over the row blocks");
 #pragma unroll
@@ -390,7 +485,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
       }
       pin_order();
     }
-    if (kn == nk - 1 && c_last < kRowChunks) copy_slab(kn, stage);
+    if (kn == nk - 1 && tail) copy_slab(kn, stage);
   }
   // Every copy has landed (the last wait drained them); once every wave's LDS
   // reads have returned, the epilogue may use LDS as scratch.

@@ -2,15 +2,14 @@
 // backward into hidden states and head weights, both on bf16 (or fp32) MFMA.
 //
 // Forward (Sec. 3.1, Eq. 1-2): rows with mask 1 are compacted, then
-//   z = W_head . h_t over 256 x 128 tiles (vocabulary x tokens); each tile is
-//   reduced in registers to a running (max, sum exp) per token, so the logits
-//   never leave the chip; partials over vocabulary groups are merged per token
-//   and the target logit z_{t,y_t} is a separate dot product.
-// Backward: rows with g != 0 are compacted (Hg, and its transpose Hg^T), W is
-//   transposed once per call (W^T); for each vocabulary block of Vc rows
-//   (A) recompute z and write dz = g (onehot - exp(z - lse)) to [T x Vc] and
-//       [Vc x T] scratch, (B) dH += dz . W_block, (C) dW_block += dz^T . Hg,
-//   all three on MFMA with K-contiguous operands.
+//   z = W_head . h_t over 256 x 256 tiles (vocabulary x tokens); each tile is
+//   reduced in registers to a (max, sum exp) pair per token, so the logits never
+//   leave the chip; the pairs of all vocabulary tiles are merged per token and
+//   the target logit z_{t,y_t} is a separate dot product.
+// Backward: rows with g != 0 are compacted (Hg); for each vocabulary block of Vc
+//   rows (A) recompute z and write dz = g (onehot - exp(z - lse)) to a [T x Vc]
+//   scratch, (B) dH += dz . W_block (W read MN-major), (C) dW_block += dz^T . Hg
+//   (dz and Hg read MN-major), all three on MFMA.
 #include "common.hpp"
 #include "gemm.hpp"
 #include "launch.hpp"
@@ -219,7 +218,7 @@ void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t V) {
   epi.part = part;
   epi.ldp = ldp;
   epi.M = V;
-  gemm_body<E>(s, epi, lds);
+  gemm_body<E, false, false>(s, epi, lds);
 }
 
 template <class E>
@@ -309,20 +308,6 @@ __device__ __forceinline__ void store4<F32>(float* p, const float (&d)[4]) {
   *reinterpret_cast<float4*>(p) = make_float4(d[0], d[1], d[2], d[3]);
 }
 
-// Transpose of an 8 x 8 block of 16-bit values held as 8 rows of 16 bytes.
-__device__ __forceinline__ void transpose8x8_b16(const v4u (&in)[8], v4u (&out)[8]) {
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    v4u o;
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-      const uint32_t lo = in[2 * d][i >> 1];
-      const uint32_t hi = in[2 * d + 1][i >> 1];
-      o[d] = (i & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
-    }
-    out[i] = o;
-  }
-}
 
 template <class E>
 __device__ __forceinline__ typename E::storage to_storage(float x);
@@ -332,14 +317,13 @@ template <>
 __device__ __forceinline__ float to_storage<F32>(float x) { return x; }
 
 // dz_{t,v} = g_t (1[v = y_t] - exp(z_{t,v} - lse_t)) for one vocabulary block, stored
-// token-major dz[c][v - v0] (row stride ldz) for the dH product and vocabulary-major
-// dzt[v - v0][c] (row stride ldzt) for the dW product.
+// token-major dz[c][v - v0] (row stride ldz). The dH product reads it K-major, the
+// dW product MN-major, so no transposed copy is written. Columns past the block's
+// valid vocabulary rows hold zeros.
 template <class E>
 struct EpiDz {
   typename E::storage* dz;
   int64_t ldz;
-  typename E::storage* dzt;
-  int64_t ldzt;
   int64_t m_valid;   // vocabulary rows of this block
   int64_t v_base;    // vocabulary index of block row 0
   const float* g_c;
@@ -377,8 +361,8 @@ struct EpiDz {
   __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t n0, int wm, int wn,
                                        int lane, void* smem) {
     if constexpr (sizeof(typename E::storage) == 2) {
-      // Stage the 256 x 256 bf16 tile in LDS as [t][v] (128 KB), then write both
-      // global layouts with 16-byte stores.
+      // Stage the 256 x 256 bf16 tile in LDS as [t][v] (128 KB), then write it
+      // with 16-byte stores.
       v4u* tile16 = static_cast<v4u*>(smem);       // [256 rows][32 chunks]
 #pragma unroll
       for (int ni = 0; ni < kNI; ++ni) {
@@ -407,20 +391,6 @@ struct EpiDz {
         const v4u x = tile16[t * 32 + tswz(t, c)];
         *reinterpret_cast<v4u*>(dz + (n0 + t) * ldz + m0 + c * 8) = x;
       }
-      // [v][t]: thread takes 8 x 8 blocks (8 tokens x 8 vocabulary entries), transposes them
-      // in registers and writes 8 rows of 8 tokens.
-#pragma unroll 1
-      for (int k = 0; k < 4; ++k) {
-        const int id = k * kThreads + tid;
-        const int c = id >> 5, t0 = (id & 31) * 8;
-        v4u in[8], out[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) in[e] = tile16[(t0 + e) * 32 + tswz(t0 + e, c)];
-        transpose8x8_b16(in, out);
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-          *reinterpret_cast<v4u*>(dzt + (m0 + c * 8 + i) * ldzt + n0 + t0) = out[i];
-      }
     } else {
 #pragma unroll
       for (int ni = 0; ni < kNI; ++ni) {
@@ -434,8 +404,6 @@ struct EpiDz {
             float d[4];
             dz4(acc, mi, ni, j, v, d);
             store4<E>(row + v, d);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) dzt[(v + e) * ldzt + c] = to_storage<E>(d[e]);
           }
         }
       }
@@ -480,42 +448,17 @@ template <class E>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_bwd_dz(GemmShape s, EpiDz<E> epi) {
   __shared__ v4u lds[kStages][kStageChunks];
-  gemm_body<E>(s, epi, lds);
+  gemm_body<E, false, false>(s, epi, lds);
 }
 
-template <class E>
+// dH += dz . W (dz K-major, W MN-major) and dW += dz^T . Hg (both MN-major).
+template <class E, bool AMn, bool BMn>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_bwd_acc(GemmShape s, EpiAcc epi) {
   __shared__ v4u lds[kStages][kStageChunks];
-  gemm_body<E>(s, epi, lds);
+  gemm_body<E, AMn, BMn>(s, epi, lds);
 }
 
-// dst[c][r] = src[r][c] for r < rows (rows = *rows_dev when given), zero for
-// rows <= r < round_up(rows, kRowPad); one 64 x 64 tile per block through LDS.
-template <typename S>
-__global__ __launch_bounds__(256) void k_transpose(const S* src, int64_t ld_s, int64_t rows_host,
-                                                   const int32_t* rows_dev, int64_t cols, S* dst,
-                                                   int64_t ld_d) {
-  __shared__ S tile[64][65];
-  const int64_t rows = rows_dev ? static_cast<int64_t>(*rows_dev) : rows_host;
-  const int64_t fill = round_up_dev(rows, kRowPad);
-  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * 64, c0 = static_cast<int64_t>(blockIdx.x) * 64;
-  if (r0 >= fill) return;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int r = i * 4 + ty;
-    const int64_t gr = r0 + r, gc = c0 + tx;
-    tile[r][tx] = (gr < rows && gc < cols) ? src[gr * ld_s + gc] : S(0);
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int oc = i * 4 + ty;
-    const int64_t gc = c0 + oc, gr = r0 + tx;
-    if (gc < cols && gr < fill) dst[gc * ld_d + gr] = tile[tx][oc];
-  }
-}
 
 // Zero rows [0, round_up(*count, 256)) of a [rows][H] fp32 buffer.
 __global__ __launch_bounds__(256) void k_zero_rows(float* p, int64_t H, const int32_t* count) {
@@ -611,9 +554,6 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
   S* hg = reinterpret_cast<S*>(w8 + L.hg);
   float* dh = reinterpret_cast<float*>(w8 + L.dh);
   S* dz = reinterpret_cast<S*>(w8 + L.dz);
-  S* dzt = reinterpret_cast<S*>(w8 + L.dzt);
-  S* hgt = reinterpret_cast<S*>(w8 + L.hgt);
-  S* wt = reinterpret_cast<S*>(w8 + L.wt);
   const S* w = static_cast<const S*>(w_head);
 
   const int nb = static_cast<int>(L.n_count_blocks);
@@ -623,36 +563,30 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
   const int rows4 = static_cast<int>(L.t_pad / 4);
   hipLaunchKernelGGL(k_gather_rows<E>, dim3(rows4), dim3(256), 0, st, static_cast<const S*>(hidden),
                      ld_hidden, H, idx, count, hg, target, y_c, g, g_c, lse, lse_c);
-  const int hb = static_cast<int>(ceil_div(H, 64));
-  // Hg^T [H][t_pad] and W^T [H][v_pad]: K-contiguous operands of the dW and dH products.
-  hipLaunchKernelGGL(k_transpose<S>, dim3(hb, static_cast<int>(L.t_pad / 64)), dim3(256), 0, st,
-                     static_cast<const S*>(hg), H, L.t_pad, count, H, hgt, L.t_pad);
-  hipLaunchKernelGGL(k_transpose<S>, dim3(hb, static_cast<int>(L.v_pad / 64)), dim3(256), 0, st, w, ld_w, V,
-                     nullptr, H, wt, L.v_pad);
   hipLaunchKernelGGL(k_zero_rows, dim3(rows4), dim3(256), 0, st, dh, H, count);
 
   for (int64_t vb = 0; vb < L.n_vblocks; ++vb) {
     const int64_t v0 = vb * L.vc;
     const int64_t vlen = (V - v0) < L.vc ? (V - v0) : L.vc;
-    // (A) z^T[v][t] = W[v0 + v] . Hg[t] -> dz in both layouts
+    // (A) z^T[v][t] = W[v0 + v] . Hg[t] -> dz[t][v]
     GemmShape sa = make_shape(w + v0 * ld_w, ld_w, vlen, hg, H, T, H);
     sa.n_dev = count;
-    EpiDz<E> ez{dz, L.vc, dzt, L.t_pad, vlen, v0, g_c, lse_c, y_c, {}, {}, {}};
+    EpiDz<E> ez{dz, L.vc, vlen, v0, g_c, lse_c, y_c, {}, {}, {}};
     hipLaunchKernelGGL(k_bwd_dz<E>, dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez);
-    // (B) dH[t][h] += sum_v dz[t][v] W^T[h][v0 + v]
-    GemmShape sb = make_shape(dz, L.vc, T, wt + v0, L.v_pad, H, vlen);
+    // (B) dH[t][h] += sum_v dz[t][v] W[v0 + v][h]: A = dz K-major, B = W MN-major
+    GemmShape sb = make_shape(dz, L.vc, T, w + v0 * ld_w, ld_w, H, vlen);
     sb.m_dev = count;
     sb.msplit = 1;
     sb.sn = pick_sn_msplit(sb.n_tiles);
     EpiAcc eb{dh, H, L.t_pad, H};
-    hipLaunchKernelGGL(k_bwd_acc<E>, dim3(gemm_grid(sb)), dim3(kThreads), 0, st, sb, eb);
-    // (C) dW[v0 + v][h] += sum_t dz^T[v][t] Hg^T[h][t]
-    GemmShape sc = make_shape(dzt, L.t_pad, vlen, hgt, L.t_pad, H, T);
+    hipLaunchKernelGGL((k_bwd_acc<E, false, true>), dim3(gemm_grid(sb)), dim3(kThreads), 0, st, sb, eb);
+    // (C) dW[v0 + v][h] += sum_t dz[t][v] Hg[t][h]: both MN-major
+    GemmShape sc = make_shape(dz, L.vc, vlen, hg, H, H, T);
     sc.k_dev = count;
     sc.msplit = 1;
     sc.sn = pick_sn_msplit(sc.n_tiles);
     EpiAcc ec{dw + v0 * H, H, vlen, H};
-    hipLaunchKernelGGL(k_bwd_acc<E>, dim3(gemm_grid(sc)), dim3(kThreads), 0, st, sc, ec);
+    hipLaunchKernelGGL((k_bwd_acc<E, true, true>), dim3(gemm_grid(sc)), dim3(kThreads), 0, st, sc, ec);
   }
   const int t4 = static_cast<int>(ceil_div(T, 4));
   hipLaunchKernelGGL(k_dh_scatter<E>, dim3(t4), dim3(256), 0, st, dh, H, pos, T, static_cast<S*>(dhidden));

@@ -49,8 +49,8 @@ inline LogprobLayout logprob_layout(int64_t T, int64_t H, int64_t V, size_t esiz
 
 // sao_loss_backward
 struct BackwardLayout {
-  int64_t t_pad, n_count_blocks, vc, n_vblocks, v_pad;
-  size_t blk_counts, count, idx, pos, g_c, lse_c, y_c, hg, hgt, wt, dh, dz, dzt, total;
+  int64_t t_pad, n_count_blocks, vc, n_vblocks;
+  size_t blk_counts, count, idx, pos, g_c, lse_c, y_c, hg, dh, dz, total;
 };
 
 inline BackwardLayout backward_layout(int64_t T, int64_t H, int64_t V, size_t esize) {
@@ -59,7 +59,6 @@ inline BackwardLayout backward_layout(int64_t T, int64_t H, int64_t V, size_t es
   L.n_count_blocks = ceil_div(T, kRowsPerCountBlock);
   L.vc = round_up(V, kTile) < kVocabBlock ? round_up(V, kTile) : kVocabBlock;
   L.n_vblocks = ceil_div(V, L.vc);
-  L.v_pad = round_up(V, kTile);
   Carve c;
   const size_t tp = static_cast<size_t>(L.t_pad);
   L.blk_counts = c.take(4 * static_cast<size_t>(L.n_count_blocks));
@@ -70,11 +69,8 @@ inline BackwardLayout backward_layout(int64_t T, int64_t H, int64_t V, size_t es
   L.lse_c = c.take(4 * tp);
   L.y_c = c.take(4 * tp);
   L.hg = c.take(esize * tp * static_cast<size_t>(H));
-  L.hgt = c.take(esize * tp * static_cast<size_t>(H));
-  L.wt = c.take(esize * static_cast<size_t>(L.v_pad) * static_cast<size_t>(H));
   L.dh = c.take(4 * tp * static_cast<size_t>(H));
   L.dz = c.take(esize * tp * static_cast<size_t>(L.vc));
-  L.dzt = c.take(esize * tp * static_cast<size_t>(L.vc));
   L.total = c.off;
   return L;
 }
