@@ -110,6 +110,23 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
     if not torch.cuda.is_available():
         print("the sweep needs a HIP device", file=sys.stderr)
         sys.exit(1)
+    # Reference: a plain device copy (1 GiB read + 1 GiB written) on the same box.
+    src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    z.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(z) / reps
+    print(json.dumps({"mode": "copy_reference", "bytes": 2 << 30, "ms": ms, "GB/s": (2 << 30) / ms / 1e6,
+                      "frac_hbm": (2 << 30) / ms / 1e6 / PEAK_HBM_GBS}), flush=True)
+    del src, dst
+    torch.cuda.empty_cache()
     for e in exps:
         T = 1 << e
         cfg = small_config(f"sweep{e}", 2000 + e, B=T // 4096, T=T, H=8, V=16,

@@ -1,9 +1,9 @@
 // Direct double-sided importance sampling and the token-level mean (Sec. 3.1, Eq. 1-3).
 //
-// One pass over the tokens: rho = exp(logp - logp_rollout) in float64, the strict
-// band flag, g = d loss / d logp, and per-block partial sums (loss terms in
-// float64, counts in int64) reduced in a fixed order by a one-block final kernel,
-// so results do not depend on scheduling.
+// One pass over the tokens: the strict band flag of rho = exp(logp - logp_rollout),
+// decided exactly as in float64, g = d loss / d logp, and per-block partial sums
+// (loss terms in float64, counts in int64) reduced in a fixed order by a one-block
+// final kernel, so results do not depend on scheduling.
 #include "common.hpp"
 #include "launch.hpp"
 #include "layout.hpp"
@@ -18,26 +18,44 @@ struct LossAcc {
   int64_t c[5] = {0, 0, 0, 0, 0};
 };
 
-// One loss-mask token: rho in float64 (Eq. 2), the strict band (Eq. 3), and
-// the token's share of the mean (Eq. 1). Returns the flag; writes g.
-__device__ __forceinline__ uint8_t loss_token(bool active, float lpf, float lrof, float advf, double lo, double hi,
+// The band edges of Eq. (3) in ratio and in log-ratio space.
+struct Band {
+  double lo, hi, ln_lo, ln_hi;
+};
+
+// Whether d lies within a margin of a band edge in log space. fp64 exp is
+// faithful to about one ulp, so outside 1e-12 (relative) comparing
+// d = logp - logp_rollout with ln(1 -+ eps) decides exactly as comparing
+// exp(d) with 1 -+ eps; inside, the ratio itself is compared.
+__device__ __forceinline__ bool near_edge(double d, double edge) {
+  return fabs(d - edge) <= 1e-12 * fmax(1.0, fabs(edge));
+}
+
+// One loss-mask token: the strict band of Eq. (3) on rho = exp(logp - logp_rollout)
+// (Eq. 2), decided as in float64, and the token's share of the mean (Eq. 1), whose
+// weight rho is evaluated in float32. Returns the flag; writes g.
+__device__ __forceinline__ uint8_t loss_token(bool active, float lpf, float lrof, float advf, const Band& bd,
                                               int64_t N, double invN, LossAcc& acc, float& g) {
   g = 0.0f;
   if (!active) return SAO_FLAG_MASKED;
   ++acc.c[0];
   const double lp = lpf;
-  const double rho = exp(lp - static_cast<double>(lrof));
+  const double d = lp - static_cast<double>(lrof);
   uint8_t f;
-  if (__builtin_isnan(rho))
+  if (__builtin_isnan(d)) {
     f = SAO_FLAG_NONFINITE;
-  else if (rho <= lo)
-    f = SAO_FLAG_LOW;
-  else if (rho >= hi)
-    f = SAO_FLAG_HIGH;
-  else
-    f = SAO_FLAG_USED;  // 1 - eps_l < rho < 1 + eps_h
+  } else {
+    bool low;
+    if (bd.lo > 0.0)
+      low = near_edge(d, bd.ln_lo) ? exp(d) <= bd.lo : d < bd.ln_lo;
+    else  // rho > 0 unless exp underflows
+      low = d < -700.0 ? exp(d) <= bd.lo : false;
+    const bool high = near_edge(d, bd.ln_hi) ? exp(d) >= bd.hi : d > bd.ln_hi;
+    f = low ? SAO_FLAG_LOW : (high ? SAO_FLAG_HIGH : SAO_FLAG_USED);  // 1 - eps_l < rho < 1 + eps_h
+  }
   ++acc.c[f];
   if (f == SAO_FLAG_USED && N > 0) {
+    const double rho = fast_exp2(static_cast<float>(d) * kLog2e);
     const double w = rho * static_cast<double>(advf);
     acc.sL = fma(w, lp, acc.sL);
     acc.sS += w;
@@ -46,52 +64,55 @@ __device__ __forceinline__ uint8_t loss_token(bool active, float lpf, float lrof
   return f;
 }
 
-// Each thread takes groups of kLossPerThread consecutive tokens (grid-stride
-// over groups); whole groups use 16-byte vector accesses when the bases allow.
+// Each wave takes chunks of 512 consecutive tokens (grid-stride over chunks);
+// lane l handles tokens 4l .. 4l+3 and 256 + 4l .. 256 + 4l+3 of a chunk, so every
+// load and store instruction of a whole chunk covers one contiguous span (when
+// the bases allow vector access).
 __global__ __launch_bounds__(kLossThreads) void k_loss(const float* logp, const float* lro, const float* adv,
                                                        const uint8_t* mask, int64_t T, float eps_low,
                                                        float eps_high, const int64_t* n_ptr, double* part_f,
                                                        int64_t* part_i, float* g, uint8_t* flags, bool vec_ok) {
-  static_assert(kLossPerThread == 8, "vector path handles 8 tokens per group");
+  static_assert(kLossPerThread == 8, "a wave chunk is 64 lanes x 8 tokens");
+  constexpr int kChunk = 64 * kLossPerThread;
   __shared__ double shd[kLossThreads / 64];
   __shared__ int64_t shi[kLossThreads / 64];
   const int64_t N = *n_ptr;
-  const double lo = 1.0 - static_cast<double>(eps_low);
-  const double hi = 1.0 + static_cast<double>(eps_high);
+  Band bd;
+  bd.lo = 1.0 - static_cast<double>(eps_low);
+  bd.hi = 1.0 + static_cast<double>(eps_high);
+  bd.ln_lo = bd.lo > 0.0 ? log(bd.lo) : 0.0;
+  bd.ln_hi = log(bd.hi);
   const double invN = N > 0 ? 1.0 / static_cast<double>(N) : 0.0;
   LossAcc acc;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kLossThreads * kLossPerThread;
-  for (int64_t t0 = (static_cast<int64_t>(blockIdx.x) * kLossThreads + threadIdx.x) * kLossPerThread; t0 < T;
-       t0 += stride) {
-    if (vec_ok && t0 + kLossPerThread <= T) {
-      const f32x4_t* pl = reinterpret_cast<const f32x4_t*>(logp + t0);
-      const f32x4_t* pr = reinterpret_cast<const f32x4_t*>(lro + t0);
-      const f32x4_t* pa = reinterpret_cast<const f32x4_t*>(adv + t0);
-      const f32x4_t l0 = pl[0], l1 = pl[1], r0 = pr[0], r1 = pr[1], a0 = pa[0], a1 = pa[1];
-      const uint2 m8 = *reinterpret_cast<const uint2*>(mask + t0);
-      float gg[8];
-      uint32_t fl[2] = {0u, 0u};
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t waves = static_cast<int64_t>(gridDim.x) * (kLossThreads / 64);
+  for (int64_t w0 = (static_cast<int64_t>(blockIdx.x) * (kLossThreads / 64) + wave) * kChunk; w0 < T;
+       w0 += waves * kChunk) {
+    if (vec_ok && w0 + kChunk <= T) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t mw = j < 4 ? m8.x : m8.y;
-        const bool act = ((mw >> (8 * (j & 3))) & 0xffu) != 0;
-        const float lpv = j < 4 ? l0[j & 3] : l1[j & 3];
-        const float lrv = j < 4 ? r0[j & 3] : r1[j & 3];
-        const float adv_ = j < 4 ? a0[j & 3] : a1[j & 3];
-        const uint8_t f = loss_token(act, lpv, lrv, adv_, lo, hi, N, invN, acc, gg[j]);
-        fl[j >> 2] |= static_cast<uint32_t>(f) << (8 * (j & 3));
+      for (int half = 0; half < 2; ++half) {
+        const int64_t t = w0 + half * (kChunk / 2) + 4 * lane;
+        const f32x4_t l4 = *reinterpret_cast<const f32x4_t*>(logp + t);
+        const f32x4_t r4 = *reinterpret_cast<const f32x4_t*>(lro + t);
+        const f32x4_t a4 = *reinterpret_cast<const f32x4_t*>(adv + t);
+        const uint32_t m4 = *reinterpret_cast<const uint32_t*>(mask + t);
+        float gg[4];
+        uint32_t fl = 0u;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const bool act = ((m4 >> (8 * j)) & 0xffu) != 0;
+          fl |= static_cast<uint32_t>(loss_token(act, l4[j], r4[j], a4[j], bd, N, invN, acc, gg[j])) << (8 * j);
+        }
+        *reinterpret_cast<f32x4_t*>(g + t) = f32x4_t{gg[0], gg[1], gg[2], gg[3]};
+        *reinterpret_cast<uint32_t*>(flags + t) = fl;
       }
-      f32x4_t* pg = reinterpret_cast<f32x4_t*>(g + t0);
-      pg[0] = f32x4_t{gg[0], gg[1], gg[2], gg[3]};
-      pg[1] = f32x4_t{gg[4], gg[5], gg[6], gg[7]};
-      *reinterpret_cast<uint2*>(flags + t0) = uint2{fl[0], fl[1]};
     } else {
       for (int j = 0; j < kLossPerThread; ++j) {
-        const int64_t t = t0 + j;
-        if (t >= T) break;
+        const int64_t t = w0 + (j < 4 ? 4 * lane + j : kChunk / 2 + 4 * lane + (j - 4));
+        if (t >= T) continue;
         const bool act = mask[t] != 0;
         float gt;
-        flags[t] = loss_token(act, act ? logp[t] : 0.0f, act ? lro[t] : 0.0f, act ? adv[t] : 0.0f, lo, hi, N,
+        flags[t] = loss_token(act, act ? logp[t] : 0.0f, act ? lro[t] : 0.0f, act ? adv[t] : 0.0f, bd, N,
                               invN, acc, gt);
         g[t] = gt;
       }
@@ -156,7 +177,7 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const float
   }
   const uintptr_t f = reinterpret_cast<uintptr_t>(logp) | reinterpret_cast<uintptr_t>(logp_rollout) |
                       reinterpret_cast<uintptr_t>(adv) | reinterpret_cast<uintptr_t>(g);
-  const bool vec_ok = (f & 15u) == 0 && ((reinterpret_cast<uintptr_t>(mask) | reinterpret_cast<uintptr_t>(flags)) & 7u) == 0;
+  const bool vec_ok = (f & 15u) == 0 && ((reinterpret_cast<uintptr_t>(mask) | reinterpret_cast<uintptr_t>(flags)) & 3u) == 0;
   hipLaunchKernelGGL(k_loss, dim3(nblk), dim3(kLossThreads), 0, st, logp, logp_rollout, adv, mask, T,
                      eps_low, eps_high, n_ptr, part_f, part_i, g, flags, vec_ok);
   hipLaunchKernelGGL(k_loss_final, dim3(1), dim3(kLossThreads), 0, st, part_f, part_i, nblk, n_ptr, loss,

@@ -13,10 +13,10 @@
 // Every such map, and every composition of them, has the form
 //   Vn' = pV Vn + cV,  R' = pR R + cR,  A' = aV Vn + aR R + aA A + cA,  G' = gR R + gG G + cG,
 // so a thread summarises its contiguous tokens by 11 numbers, the block scans the
-// summaries (wave shuffles, then across waves through LDS), and each thread
-// replays its tokens from the exact state that enters it. Arithmetic is float64.
-// Tiles of 2048 tokens aligned to the global index give every thread 8 tokens
-// that it reads and writes with 16-byte vector accesses.
+// summaries (DPP lane moves inside each wave, then across waves through LDS), and
+// each thread replays its tokens from the exact state that enters it. Arithmetic
+// is float64. Tiles of 2048 tokens aligned to the global index give every thread
+// 8 tokens that it reads and writes with 16-byte vector accesses.
 #include "common.hpp"
 #include "launch.hpp"
 #include "../../include/sao.h"
@@ -48,29 +48,63 @@ __device__ __forceinline__ Aff compose(const Aff& F, const Aff& G) {
   return r;
 }
 
-__device__ __forceinline__ Aff token_map(bool action, double v, double r, double gamma, double kappa) {
-  if (!action) {
-    Aff m = aff_identity();
-    m.cR = r;
-    return m;
-  }
-  return Aff{0.0, v, 0.0, 0.0, gamma, 1.0, kappa, r - v, 1.0, gamma, r};
+// M o F for the map M of one token, F covering the tokens to its right
+// (the general compose() with M's constants substituted).
+__device__ __forceinline__ void push_action(Aff& F, double v, double r, double gamma, double kappa) {
+  const Aff G = F;
+  F.pV = 0.0;
+  F.cV = v;
+  F.pR = 0.0;
+  F.cR = 0.0;
+  F.aV = fma(gamma, G.pV, kappa * G.aV);
+  F.aR = fma(kappa, G.aR, G.pR);
+  F.aA = kappa * G.aA;
+  F.cA = fma(kappa, G.cA, fma(gamma, G.cV, G.cR + (r - v)));
+  F.gR = fma(gamma, G.gR, G.pR);
+  F.gG = gamma * G.gG;
+  F.cG = fma(gamma, G.cG, G.cR + r);
+}
+__device__ __forceinline__ void push_observation(Aff& F, double r) { F.cR += r; }
+
+// A double moved across lanes by DPP (CTRL, ROW_MASK); lanes without a source keep `old`.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_f64(double old, double x) {
+  const uint2 o = __builtin_bit_cast(uint2, old), v = __builtin_bit_cast(uint2, x);
+  const int lo = __builtin_amdgcn_update_dpp(static_cast<int>(o.x), static_cast<int>(v.x), CTRL, ROW_MASK, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(static_cast<int>(o.y), static_cast<int>(v.y), CTRL, ROW_MASK, 0xf, false);
+  return __builtin_bit_cast(double, make_uint2(static_cast<uint32_t>(lo), static_cast<uint32_t>(hi)));
+}
+// The map of another lane (identity where there is none).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ Aff dpp_aff(const Aff& x) {
+  Aff o;
+  o.pV = dpp_f64<CTRL, ROW_MASK>(1.0, x.pV);
+  o.cV = dpp_f64<CTRL, ROW_MASK>(0.0, x.cV);
+  o.pR = dpp_f64<CTRL, ROW_MASK>(1.0, x.pR);
+  o.cR = dpp_f64<CTRL, ROW_MASK>(0.0, x.cR);
+  o.aV = dpp_f64<CTRL, ROW_MASK>(0.0, x.aV);
+  o.aR = dpp_f64<CTRL, ROW_MASK>(0.0, x.aR);
+  o.aA = dpp_f64<CTRL, ROW_MASK>(1.0, x.aA);
+  o.cA = dpp_f64<CTRL, ROW_MASK>(0.0, x.cA);
+  o.gR = dpp_f64<CTRL, ROW_MASK>(0.0, x.gR);
+  o.gG = dpp_f64<CTRL, ROW_MASK>(1.0, x.gG);
+  o.cG = dpp_f64<CTRL, ROW_MASK>(0.0, x.cG);
+  return o;
 }
 
-__device__ __forceinline__ Aff shfl_down_aff(const Aff& a, int d) {
-  Aff o;
-  o.pV = __shfl_down(a.pV, d, 64);
-  o.cV = __shfl_down(a.cV, d, 64);
-  o.pR = __shfl_down(a.pR, d, 64);
-  o.cR = __shfl_down(a.cR, d, 64);
-  o.aV = __shfl_down(a.aV, d, 64);
-  o.aR = __shfl_down(a.aR, d, 64);
-  o.aA = __shfl_down(a.aA, d, 64);
-  o.cA = __shfl_down(a.cA, d, 64);
-  o.gR = __shfl_down(a.gR, d, 64);
-  o.gG = __shfl_down(a.gG, d, 64);
-  o.cG = __shfl_down(a.cG, d, 64);
-  return o;
+// Inclusive scan over the wave in lane order, S_l = F_l o F_{l-1} o ... o F_0:
+// shifts by 1, 2, 4, 8 inside each row of 16 lanes (row_shr), then the last lane
+// of row 0 into row 1 and of row 2 into row 3 (row_bcast:15), then lane 31 into
+// rows 2 and 3 (row_bcast:31). DPP moves are VALU operations, so no step waits
+// on the LDS crossbar.
+__device__ __forceinline__ Aff wave_scan(Aff S) {
+  S = compose(S, dpp_aff<0x111, 0xf>(S));
+  S = compose(S, dpp_aff<0x112, 0xf>(S));
+  S = compose(S, dpp_aff<0x114, 0xf>(S));
+  S = compose(S, dpp_aff<0x118, 0xf>(S));
+  S = compose(S, dpp_aff<0x142, 0xa>(S));
+  S = compose(S, dpp_aff<0x143, 0xc>(S));
+  return S;
 }
 
 // One block: cu_seqlens must rise from 0 to T without decreasing. Sets *bad (0/1),
@@ -148,23 +182,45 @@ __global__ __launch_bounds__(kScanThreads) void k_advantage(
   const int64_t first = s / kScanTile * kScanTile;           // aligned tile containing s
   int64_t total = 0;
   St carry{0.0, 0.0, 0.0, 0.0};                               // nothing after the last token
-  for (int64_t t0 = (e - 1) / kScanTile * kScanTile; t0 >= first; t0 -= kScanTile) {
-    const int64_t c0 = t0 + static_cast<int64_t>(tid) * kScanPer;   // this thread's aligned block
-    // Tokens of the block inside [s, e), and whether the whole block is (then vector
-    // access, when the array bases allow it).
-    const bool full = vec_ok && c0 >= s && c0 + kScanPer <= e;
+  // Thread i takes block 255 - i of each tile, so lane order runs right to left
+  // and the reverse scan over tokens is a forward scan over lanes. Whole blocks
+  // inside [s, e) use vector access (when the array bases allow it), and the next
+  // tile's block is loaded before the current one is processed.
+  struct Blk {
+    f32x4_t v0, v1, r0, r1;
+    uint2 m;
+  };
+  auto block_start = [&](int64_t t0) { return t0 + static_cast<int64_t>(kScanThreads - 1 - tid) * kScanPer; };
+  auto whole = [&](int64_t t0, int64_t c0) { return vec_ok && t0 >= first && c0 >= s && c0 + kScanPer <= e; };
+  auto load = [&](int64_t c0) {
+    Blk x;
+    const f32x4_t* pv = reinterpret_cast<const f32x4_t*>(values + c0);
+    const f32x4_t* pr = reinterpret_cast<const f32x4_t*>(rewards + c0);
+    x.v0 = pv[0];
+    x.v1 = pv[1];
+    x.r0 = pr[0];
+    x.r1 = pr[1];
+    x.m = *reinterpret_cast<const uint2*>(mask + c0);
+    return x;
+  };
+  int64_t t0 = (e - 1) / kScanTile * kScanTile;
+  int64_t c0 = block_start(t0);
+  bool full = whole(t0, c0);
+  Blk cur{};
+  if (full) cur = load(c0);
+  for (; t0 >= first; t0 -= kScanTile) {
+    const int64_t c0n = block_start(t0 - kScanTile);
+    const bool fulln = whole(t0 - kScanTile, c0n);
+    Blk nxt{};
+    if (fulln) nxt = load(c0n);
     float v[kScanPer], r[kScanPer];
     bool act[kScanPer];
     if (full) {
-      const f32x4_t* pv = reinterpret_cast<const f32x4_t*>(values + c0);
-      const f32x4_t* pr = reinterpret_cast<const f32x4_t*>(rewards + c0);
-      const f32x4_t v0 = pv[0], v1 = pv[1], r0 = pr[0], r1 = pr[1];
-      const uint2 m8 = *reinterpret_cast<const uint2*>(mask + c0);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        v[j] = v0[j]; v[4 + j] = v1[j]; r[j] = r0[j]; r[4 + j] = r1[j];
-        act[j] = ((m8.x >> (8 * j)) & 0xffu) != 0;
-        act[4 + j] = ((m8.y >> (8 * j)) & 0xffu) != 0;
+        v[j] = cur.v0[j]; v[4 + j] = cur.v1[j]; r[j] = cur.r0[j]; r[4 + j] = cur.r1[j];
+        act[j] = ((cur.m.x >> (8 * j)) & 0xffu) != 0;
+        act[4 + j] = ((cur.m.y >> (8 * j)) & 0xffu) != 0;
       }
     } else {
 #pragma unroll
@@ -183,27 +239,24 @@ __global__ __launch_bounds__(kScanThreads) void k_advantage(
     for (int j = kScanPer - 1; j >= 0; --j) {
       const bool in = full || (c0 + j >= s && c0 + j < e);
       if (!in) continue;
-      cnt += act[j] ? 1 : 0;
-      F = compose(token_map(act[j], v[j], r[j], gamma, kappa), F);
+      if (act[j]) {
+        ++cnt;
+        push_action(F, v[j], r[j], gamma, kappa);
+      } else {
+        push_observation(F, r[j]);
+      }
     }
     total += cnt;
-    // Reverse inclusive scan inside the wave: P_l = F_l o F_{l+1} o ... o F_63.
-    Aff P = F;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const Aff o = shfl_down_aff(P, d);
-      if (lane + d < 64) P = compose(P, o);
-    }
+    const Aff S = wave_scan(F);                     // this lane and the lanes to its right
+    const Aff E = dpp_aff<0x138, 0xf>(S);          // wave_shr:1, the lanes to its right only
     __syncthreads();  // the previous tile's readers of s_agg / s_carry are done
-    if (lane == 0) s_agg[wave] = P;
+    if (lane == 63) s_agg[wave] = S;
     if (tid == 0) s_carry = carry;
     __syncthreads();
-    // State entering this wave from the right: the carry through later waves.
+    // State entering this wave: the carry through the waves to its right (lower waves).
     St sw = s_carry;
-    for (int w = kScanThreads / 64 - 1; w > wave; --w) sw = apply(s_agg[w], sw);
-    // State entering this thread: lanes to its right inside the wave, then the rest.
-    const Aff Q = shfl_down_aff(P, 1);
-    St st = lane < 63 ? apply(Q, sw) : sw;
+    for (int w = 0; w < wave; ++w) sw = apply(s_agg[w], sw);
+    St st = apply(E, sw);
     // Pass 2: replay the tokens from that state and write the outputs.
     float oa[kScanPer], og[kScanPer];
 #pragma unroll
@@ -245,11 +298,14 @@ __global__ __launch_bounds__(kScanThreads) void k_advantage(
         }
       }
     }
-    // The state leaving this tile on the left (thread 0's final state) is the next carry.
+    // The state leaving this tile on the left (the last thread's final state) is the next carry.
     __syncthreads();
-    if (tid == 0) s_carry = st;
+    if (tid == kScanThreads - 1) s_carry = st;
     __syncthreads();
     carry = s_carry;
+    cur = nxt;
+    full = fulln;
+    c0 = c0n;
   }
   const int64_t wcnt = wave_sum(total);
   __syncthreads();

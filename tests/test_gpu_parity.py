@@ -221,3 +221,45 @@ def test_value_dhidden_is_rne_of_fp32_product():
     want[~m] = 0
     got = dh.view(torch.int16).cpu().numpy().view(np.uint16)
     assert np.array_equal(got, want), int((got != want).sum())
+
+
+@pytest.mark.parametrize("eps_low,eps_high", [(0.2, 0.28), (0.3, 5.0), (0.8, 3.0)])
+def test_band_decisions_near_edges(eps_low, eps_high):
+    """Ratios within 1e-6 of either band edge (in log space) flag exactly as in float64."""
+    rng = np.random.default_rng(41)
+    n = 8192
+    lro = rng.uniform(-6.0, -0.05, n).astype(np.float32)
+    edges = np.array([np.log1p(-eps_low), np.log1p(eps_high)])
+    d = edges[rng.integers(0, 2, n)] + rng.uniform(-1e-6, 1e-6, n)
+    lp = (lro.astype(np.float64) + d).astype(np.float32)
+    adv = rng.normal(0.0, 1.0, n).astype(np.float32)
+    mask = np.ones(n, dtype=np.uint8)
+    mask[::17] = 0
+    t = lambda x: torch.from_numpy(x).cuda()  # noqa: E731
+    loss, g, flags, counts = sao.clipped_loss(t(lp), t(lro), t(adv), t(mask), eps_low, eps_high, None)
+    torch.cuda.synchronize()
+    ref_loss, ref_g, ref_flags, ref_counts = oracle.dis_loss(lp.astype(np.float64), lro.astype(np.float64), adv,
+                                                             mask, eps_low, eps_high)
+    assert np.array_equal(flags.cpu().numpy(), ref_flags)
+    assert np.array_equal(counts.cpu().numpy(), ref_counts)
+    assert ref_counts[2] > 100 and ref_counts[3] > 100 and ref_counts[1] > 100
+    assert np.allclose(loss.cpu().numpy(), ref_loss, rtol=1e-5, atol=1e-12)
+    assert np.allclose(g.cpu().numpy(), ref_g, rtol=1e-5, atol=1e-12)
+
+
+def test_band_without_lower_edge_and_extremes():
+    """eps_low >= 1 clips low only where exp underflows; +-inf and NaN ratios."""
+    lp = np.array([-800.0, -0.5, 0.0, -3.0, np.inf, -np.inf, np.nan, -1.0], dtype=np.float32)
+    lro = np.array([0.0, 0.0, 0.0, -3.0, 0.0, 0.0, 0.0, np.nan], dtype=np.float32)
+    adv = np.linspace(-1.0, 1.0, lp.size).astype(np.float32)
+    mask = np.ones(lp.size, dtype=np.uint8)
+    t = lambda x: torch.from_numpy(x).cuda()  # noqa: E731
+    for eps_low in (1.0, 1.5, 0.2):
+        loss, g, flags, counts = sao.clipped_loss(t(lp), t(lro), t(adv), t(mask), eps_low, 0.28, None)
+        torch.cuda.synchronize()
+        rl, rg, rf, rc = oracle.dis_loss(lp.astype(np.float64), lro.astype(np.float64), adv, mask, eps_low, 0.28)
+        assert np.array_equal(flags.cpu().numpy(), rf), (eps_low, flags.cpu().numpy(), rf)
+        assert np.array_equal(counts.cpu().numpy(), rc)
+        # with eps_low = 1.5 the log pi = -inf token stays in band with rho = 0, and its
+        # term rho A log pi is 0 * inf: NaN on both sides
+        assert np.allclose(loss.cpu().numpy(), rl, rtol=1e-5, atol=1e-12, equal_nan=True)
