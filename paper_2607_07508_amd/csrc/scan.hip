@@ -147,7 +147,7 @@ __device__ __forceinline__ St apply(const Aff& M, const St& s) {
 // tile on the left enters the next tile from the right. Inside a tile each
 // thread composes the maps of its tokens, the block scans the compositions,
 // and each thread replays its tokens from the exact entering state.
-__global__ __launch_bounds__(kScanThreads) void k_advantage(
+__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_advantage(
     const float* values, const float* rewards, const uint8_t* mask, const int32_t* cu, int32_t B,
     int64_t T, double gamma, double lam, double alpha, float* adv, float* ret, int64_t* n_tokens,
     const int32_t* bad, bool vec_ok) {
@@ -184,43 +184,22 @@ __global__ __launch_bounds__(kScanThreads) void k_advantage(
   St carry{0.0, 0.0, 0.0, 0.0};                               // nothing after the last token
   // Thread i takes block 255 - i of each tile, so lane order runs right to left
   // and the reverse scan over tokens is a forward scan over lanes. Whole blocks
-  // inside [s, e) use vector access (when the array bases allow it), and the next
-  // tile's block is loaded before the current one is processed.
-  struct Blk {
-    f32x4_t v0, v1, r0, r1;
-    uint2 m;
-  };
-  auto block_start = [&](int64_t t0) { return t0 + static_cast<int64_t>(kScanThreads - 1 - tid) * kScanPer; };
-  auto whole = [&](int64_t t0, int64_t c0) { return vec_ok && t0 >= first && c0 >= s && c0 + kScanPer <= e; };
-  auto load = [&](int64_t c0) {
-    Blk x;
-    const f32x4_t* pv = reinterpret_cast<const f32x4_t*>(values + c0);
-    const f32x4_t* pr = reinterpret_cast<const f32x4_t*>(rewards + c0);
-    x.v0 = pv[0];
-    x.v1 = pv[1];
-    x.r0 = pr[0];
-    x.r1 = pr[1];
-    x.m = *reinterpret_cast<const uint2*>(mask + c0);
-    return x;
-  };
-  int64_t t0 = (e - 1) / kScanTile * kScanTile;
-  int64_t c0 = block_start(t0);
-  bool full = whole(t0, c0);
-  Blk cur{};
-  if (full) cur = load(c0);
-  for (; t0 >= first; t0 -= kScanTile) {
-    const int64_t c0n = block_start(t0 - kScanTile);
-    const bool fulln = whole(t0 - kScanTile, c0n);
-    Blk nxt{};
-    if (fulln) nxt = load(c0n);
+  // inside [s, e) use vector access (when the array bases allow it).
+  for (int64_t t0 = (e - 1) / kScanTile * kScanTile; t0 >= first; t0 -= kScanTile) {
+    const int64_t c0 = t0 + static_cast<int64_t>(kScanThreads - 1 - tid) * kScanPer;
+    const bool full = vec_ok && c0 >= s && c0 + kScanPer <= e;
     float v[kScanPer], r[kScanPer];
     bool act[kScanPer];
     if (full) {
+      const f32x4_t* pv = reinterpret_cast<const f32x4_t*>(values + c0);
+      const f32x4_t* pr = reinterpret_cast<const f32x4_t*>(rewards + c0);
+      const f32x4_t v0 = pv[0], v1 = pv[1], r0 = pr[0], r1 = pr[1];
+      const uint2 m8 = *reinterpret_cast<const uint2*>(mask + c0);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        v[j] = cur.v0[j]; v[4 + j] = cur.v1[j]; r[j] = cur.r0[j]; r[4 + j] = cur.r1[j];
-        act[j] = ((cur.m.x >> (8 * j)) & 0xffu) != 0;
-        act[4 + j] = ((cur.m.y >> (8 * j)) & 0xffu) != 0;
+        v[j] = v0[j]; v[4 + j] = v1[j]; r[j] = r0[j]; r[4 + j] = r1[j];
+        act[j] = ((m8.x >> (8 * j)) & 0xffu) != 0;
+        act[4 + j] = ((m8.y >> (8 * j)) & 0xffu) != 0;
       }
     } else {
 #pragma unroll
@@ -303,9 +282,6 @@ __global__ __launch_bounds__(kScanThreads) void k_advantage(
     if (tid == kScanThreads - 1) s_carry = st;
     __syncthreads();
     carry = s_carry;
-    cur = nxt;
-    full = fulln;
-    c0 = c0n;
   }
   const int64_t wcnt = wave_sum(total);
   __syncthreads();
