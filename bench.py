@@ -7,8 +7,10 @@ One step is the whole hot path over one synthetic batch: skip-observation GAE
 (sao_loss_backward), with the zeroing of the accumulated outputs. Inputs are
 resident in HBM before the timed region.
 
-Default workload: 16 single rollouts, T = 65,536 tokens, H = 2048, V = 151,936,
-bf16 hidden/W_head, forward + backward, drift noise sigma 0.2.
+Default workload (c2): 16 single rollouts, T = 65,536 tokens, H = 2048,
+V = 151,936, bf16 hidden/W_head, forward + backward, drift noise sigma 0.2.
+--workload c1 / c3 / c4 run the forward-only, the long-horizon chunked and the
+large-head-with-critic workloads the same way (reported, not the headline).
 
 Prints one JSON line (rank 0, one GPU): tokens/s, the roofline figure of the
 head-forward MFMA kernel (timed live with HIP events around its launches) and
@@ -31,8 +33,14 @@ METRIC = "tokens/s SAO logprob+clipped-loss fwd+bwd (H2048,V152k); % bf16 MFMA p
 PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA, TFLOP/s
 PEAK_HBM_GBS = 8000.0              # MI355X HBM3E, GB/s
 WORKLOAD_TEXT = {
+    "c1": "16 single rollouts, T=65536, H=2048, V=151936, bf16, forward only (log-probs, scan, loss), "
+          "~30% observation tokens, drift sigma 0.1, eps 0.2/0.2, gamma 1, alpha 1.5",
     "c2": "16 single rollouts, T=65536, H=2048, V=151936, bf16, fwd+bwd, ~30% observation tokens, "
           "drift sigma 0.2, eps 0.2/0.2, gamma 1, alpha 1.5",
+    "c3": "8 long-horizon rollouts (Pareto lengths, cap 65536), T=262144, H=2048, V=151936, bf16, fwd+bwd in "
+          "32 chunks of 8192 tokens with the whole-batch scan and N, ~50% observation tokens, eps 0.2/0.2",
+    "c4": "64 single rollouts, T=32768, H=6144, V=151552, bf16, fwd+bwd plus the critic head (values from "
+          "h.w_v, squared-error loss), ~25% observation tokens, eps 0.2/0.28",
 }
 
 
@@ -271,28 +279,57 @@ def main():
     n_tok = torch.zeros(1, dtype=torch.int64, device=dev)
     loss = torch.zeros(2, dtype=torch.float64, device=dev)
     counts = torch.zeros(5, dtype=torch.int64, device=dev)
-    dhid = torch.empty((T, H), dtype=db.hidden.dtype, device=dev)
-    dw = torch.zeros((V, H), **f32)
+    dhid = torch.empty((T, H), dtype=db.hidden.dtype, device=dev) if cfg.backward else None
+    dw = torch.zeros((V, H), **f32) if cfg.backward else None
     dt = B.SAO_BF16 if cfg.dtype == "bf16" else B.SAO_F32
-    ws_bytes = max(B.workspace_size(B.OP_LOGPROB, T, H, V, dt), B.workspace_size(B.OP_BACKWARD, T, H, V, dt),
-                   B.workspace_size(B.OP_LOSS, T, 1, 1, dt), B.workspace_size(B.OP_ADVANTAGE, T, 1, 1, dt))
+    esz = db.hidden.element_size()
+    chunk = cfg.chunk or T
+    chunks = [(s0, min(T, s0 + chunk)) for s0 in range(0, T, chunk)]
+    ws_bytes = max(B.workspace_size(B.OP_LOGPROB, chunk, H, V, dt), B.workspace_size(B.OP_BACKWARD, chunk, H, V, dt),
+                   B.workspace_size(B.OP_LOSS, T, 1, 1, dt), B.workspace_size(B.OP_ADVANTAGE, T, 1, 1, dt),
+                   B.workspace_size(B.OP_VALUE, T, H, 1, dt))
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    if cfg.value_head:
+        v_out = torch.empty(T, **f32)
+        loss_v = torch.zeros(1, dtype=torch.float64, device=dev)
+        dhid_v = torch.empty((T, H), dtype=db.hidden.dtype, device=dev)
+        dw_v = torch.zeros(H, **f32)
     p = lambda t: t.data_ptr()  # noqa: E731
+    fwd_pairs = []   # event pairs bracketing the head-forward launches of the timed steps
 
-    def step():
+    def step(timed_pairs=None):
         loss.zero_()
         counts.zero_()
-        dw.zero_()
-        B._check(L.sao_advantage(p(db.values), p(db.rewards), p(db.mask), p(db.cu_seqlens), cfg.B, T,
+        if cfg.backward:
+            dw.zero_()
+        values = db.values
+        if cfg.value_head:
+            loss_v.zero_()
+            dw_v.zero_()
+            B._check(L.sao_value_forward(p(db.hidden), H, p(db.w_value), T, H, dt, p(v_out), None, 0, st))
+            values = v_out
+        B._check(L.sao_advantage(p(values), p(db.rewards), p(db.mask), p(db.cu_seqlens), cfg.B, T,
                                  cfg.gamma, cfg.lam, cfg.alpha, p(adv), p(ret), p(n_tok), None, p(ws), ws_bytes,
                                  st))
-        B._check(L.sao_token_logprob(p(db.hidden), H, p(db.w_head), H, p(db.target), p(db.mask), T, H, V, dt,
-                                     p(logp), p(lse), None, p(ws), ws_bytes, st))
-        B._check(L.sao_clipped_loss(p(logp), p(db.logp_rollout), p(adv), p(db.mask), T, cfg.eps_low,
-                                    cfg.eps_high, p(n_tok), p(loss), p(g), p(flags), p(counts), p(ws),
-                                    ws_bytes, st))
-        B._check(L.sao_loss_backward(p(db.hidden), H, p(db.w_head), H, p(db.target), p(lse), p(g), T, H, V,
-                                     dt, p(dhid), p(dw), p(ws), ws_bytes, st))
+        if cfg.value_head:
+            B._check(L.sao_value_loss(p(db.hidden), H, p(db.w_value), p(v_out), p(ret), p(db.mask), T, H,
+                                      p(n_tok), dt, p(loss_v), p(dhid_v), p(dw_v), p(ws), ws_bytes, st))
+        for i, (s0, e0) in enumerate(chunks):
+            n = e0 - s0
+            if timed_pairs is not None:
+                B.time_kernel(B.KERNEL_HEAD_FORWARD, *timed_pairs[i])
+            B._check(L.sao_token_logprob(p(db.hidden) + s0 * H * esz, H, p(db.w_head), H, p(db.target) + 4 * s0,
+                                         p(db.mask) + s0, n, H, V, dt, p(logp) + 4 * s0, p(lse) + 4 * s0, None,
+                                         p(ws), ws_bytes, st))
+            B._check(L.sao_clipped_loss(p(logp) + 4 * s0, p(db.logp_rollout) + 4 * s0, p(adv) + 4 * s0,
+                                        p(db.mask) + s0, n, cfg.eps_low, cfg.eps_high, p(n_tok), p(loss),
+                                        p(g) + 4 * s0, p(flags) + s0, p(counts), p(ws), ws_bytes, st))
+            if cfg.backward:
+                B._check(L.sao_loss_backward(p(db.hidden) + s0 * H * esz, H, p(db.w_head), H,
+                                             p(db.target) + 4 * s0, p(lse) + 4 * s0, p(g) + 4 * s0, n, H, V, dt,
+                                             p(dhid) + s0 * H * esz, p(dw), p(ws), ws_bytes, st))
+        if timed_pairs is not None:
+            B.time_kernel(B.KERNEL_NONE, None, None)
 
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
@@ -302,12 +339,13 @@ def main():
     t_act = int(counts_h[0])
     t_grad = int(counts_h[1])
 
-    fwd_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)]
+    fwd_ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in chunks] for _ in range(args.steps)]
     step_ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    for a, b in fwd_ev:        # materialise the event handles
-        a.record()
-        b.record()
+    for pairs in fwd_ev:       # materialise the event handles
+        for a, b in pairs:
+            a.record()
+            b.record()
     for a in step_ev:
         a.record()
     torch.cuda.synchronize()
@@ -315,18 +353,19 @@ def main():
     torch.cuda.synchronize()
     step_ev[0].record()
     for i in range(args.steps):
-        B.time_kernel(B.KERNEL_HEAD_FORWARD, *fwd_ev[i])
-        step()
+        step(fwd_ev[i])
         step_ev[i + 1].record()
     torch.cuda.synchronize()
     B.time_kernel(B.KERNEL_NONE, None, None)
     per_step = [step_ev[i].elapsed_time(step_ev[i + 1]) for i in range(args.steps)]
     ms = step_ev[0].elapsed_time(step_ev[-1]) / args.steps
-    fwd_ms = float(np.mean([a.elapsed_time(b) for a, b in fwd_ev]))
+    # the forward kernel's time per step (all chunks), and per launch
+    fwd_step_ms = float(np.mean([sum(a.elapsed_time(b) for a, b in pairs) for pairs in fwd_ev]))
+    fwd_ms = fwd_step_ms / len(chunks)
 
-    fwd_flops = 2.0 * t_act * V * H
+    fwd_flops = 2.0 * t_act * V * H / len(chunks)   # per launch, averaged over the chunks
     achieved = fwd_flops / (fwd_ms * 1e-3) / 1e12
-    algo_flops = (2.0 * t_act + 4.0 * t_grad) * V * H
+    algo_flops = (2.0 * t_act + (4.0 * t_grad if cfg.backward else 0.0)) * V * H
     out = {
         "metric": METRIC,
         "value": T / (ms * 1e-3),
@@ -344,7 +383,8 @@ def main():
                    "B": cfg.B, "T_act": t_act, "T_grad": t_grad, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "mfma", "kernel": "k_head_fwd (sao_token_logprob)", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": measured_traffic(), "launch_ms": fwd_ms, "flops_per_launch": fwd_flops},
+                     "traffic": measured_traffic() if args.workload == "c2" else None, "launch_ms": fwd_ms,
+                     "flops_per_launch": fwd_flops},
         "algorithmic_mfma_frac": algo_flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
         "step_ms": {"median": float(np.median(per_step)), "min": float(np.min(per_step)),
                     "max": float(np.max(per_step))},

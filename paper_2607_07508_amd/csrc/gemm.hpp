@@ -39,7 +39,10 @@
 // blocks sharing an XCD's L2 share operand panels. In N-split mode the XCDs of
 // a wave take different N-tiles of the same M-tiles (the wave covers 8 SN x
 // 32/SN tiles); in M-split mode they take different M-tiles of the same N-tiles
-// (SN x 256/SN), so an M-tile's rows are fetched by one XCD only.
+// (SN x 256/SN), so an M-tile's rows are fetched by one XCD only. The split
+// dimension is dealt out to the XCDs in turn (XCD x takes tiles x, x + 8, ...),
+// so that when only part of it holds valid rows (a device-side count below the
+// host bound) every XCD still gets its share of the work.
 #pragma once
 
 #include <type_traits>
@@ -98,6 +101,9 @@ inline int pick_sn(int n_tiles) {
   if (n_tiles % 16 == 0) return 2;
   return 1;
 }
+
+// Launches with at most this many N tiles (host bound) use the M-split raster.
+constexpr int kMsplitMaxNTiles = 64;
 
 // M-split: all of a narrow N range per XCD (up to 8 tiles).
 inline int pick_sn_msplit(int n_tiles) {
@@ -318,9 +324,9 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   int n_tile, mt;
   if (s.msplit) {
     n_tile = (w % nw) * sn + slot % sn;
-    mt = (w / nw) * (256 / sn) + xcd * (32 / sn) + slot / sn;
+    mt = (w / nw) * (256 / sn) + (slot / sn) * 8 + xcd;
   } else {
-    n_tile = (w % nw) * 8 * sn + xcd * sn + slot % sn;
+    n_tile = (w % nw) * 8 * sn + (slot % sn) * 8 + xcd;
     mt = (w / nw) * (32 / sn) + slot / sn;
   }
 

@@ -498,7 +498,11 @@ static GemmShape make_shape(const void* a, int64_t lda, int64_t m, const void* b
   s.k = k;
   s.m_tiles = static_cast<int>(ceil_div(m, kBM));
   s.n_tiles = static_cast<int>(ceil_div(n, kBN));
-  s.sn = pick_sn(s.n_tiles);
+  // Few N tiles (a token chunk against the whole vocabulary): split M across the
+  // XCDs, so each XCD streams its own share of A while the small B is shared.
+  // Otherwise split N, so that the 8 XCDs read each A panel together.
+  s.msplit = s.n_tiles <= kMsplitMaxNTiles ? 1 : 0;
+  s.sn = s.msplit ? pick_sn_msplit(s.n_tiles) : pick_sn(s.n_tiles);
   return s;
 }
 
