@@ -82,6 +82,8 @@ struct GemmShape {
   int n_tiles;             // ceil(n / kBN) with the host bound
   int sn;                  // N tiles per XCD per raster wave (1, 2, 4 or 8)
   int msplit;              // 0: XCDs split the wave's N tiles; 1: XCDs split its M tiles
+  int64_t k_split;         // > 0: K is cut into pieces of this length (a multiple of 64),
+                           // piece blockIdx.y per workgroup; the epilogue keeps them apart
 };
 
 // Tiles of one raster wave (256 blocks) along N and along M.
@@ -332,7 +334,12 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
 
   const int64_t n_valid = s.n_dev ? static_cast<int64_t>(*s.n_dev) : s.n;
   const int64_t m_valid = s.m_dev ? static_cast<int64_t>(*s.m_dev) : s.m;
-  const int64_t k_valid = s.k_dev ? static_cast<int64_t>(*s.k_dev) : s.k;
+  int64_t k_valid = s.k_dev ? static_cast<int64_t>(*s.k_dev) : s.k;
+  int64_t k0 = 0;  // first K index of this workgroup's piece
+  if (s.k_split > 0) {
+    k0 = static_cast<int64_t>(blockIdx.y) * s.k_split;
+    k_valid = k_valid - k0 < s.k_split ? k_valid - k0 : s.k_split;
+  }
   if (n_tile >= s.n_tiles || mt >= s.m_tiles) return;
   const int64_t n0 = static_cast<int64_t>(n_tile) * kBN;
   const int64_t m0 = static_cast<int64_t>(mt) * kBM;
@@ -351,8 +358,8 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
     for (int j = 0; j < kNI; ++j) acc[i][j] = f32x16_t{};
 
   const int esz = static_cast<int>(sizeof(typename E::storage));
-  const char* a_base = static_cast<const char*>(s.a);
-  const char* b_base = static_cast<const char*>(s.b);
+  const char* a_base = static_cast<const char*>(s.a) + (AMn ? k0 * s.lda : k0) * esz;
+  const char* b_base = static_cast<const char*>(s.b) + (BMn ? k0 * s.ldb : k0) * esz;
   using G = MnSlab<E>;
   // Every 1 KB copy instruction of a wave fills 64 consecutive LDS chunks (lane l
   // writes chunk l). K-major: copy q covers kRowsPerCopy tile rows from

@@ -422,6 +422,7 @@ struct EpiAcc {
   int64_t ldo;
   int64_t m_valid;
   int64_t n_valid;
+  int64_t split_stride;  // elements between the outputs of successive K pieces
 
   __device__ __forceinline__ void begin(int64_t, int, int, int) {}
 
@@ -456,32 +457,40 @@ template <class E, bool AMn, bool BMn>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_bwd_acc(GemmShape s, EpiAcc epi) {
   __shared__ v4u lds[kStages][kStageChunks];
+  epi.out += static_cast<int64_t>(blockIdx.y) * epi.split_stride;  // this K piece's own output
   gemm_body<E, AMn, BMn>(s, epi, lds);
 }
 
 
 // Zero rows [0, round_up(*count, 256)) of a [rows][H] fp32 buffer.
-__global__ __launch_bounds__(256) void k_zero_rows(float* p, int64_t H, const int32_t* count) {
+// Zero rows [0, round_up(count, kRowPad)) of `pieces` accumulators `stride` floats apart.
+__global__ __launch_bounds__(256) void k_zero_rows(float* p, int64_t H, const int32_t* count, int pieces,
+                                                   int64_t stride) {
   const int64_t c = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (c >= round_up_dev(*count, kRowPad)) return;
-  float4* r = reinterpret_cast<float4*>(p + c * H);
-  for (int64_t k = threadIdx.x & 63; k < H / 4; k += 64) r[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int q = 0; q < pieces; ++q) {
+    float4* r = reinterpret_cast<float4*>(p + q * stride + c * H);
+    for (int64_t k = threadIdx.x & 63; k < H / 4; k += 64) r[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
 }
 
-// dhidden[t] = dH[pos[t]] rounded to the element type, or zeros when pos[t] < 0.
+// dhidden[t] = sum over the K pieces (in order) of dH[pos[t]], rounded to the
+// element type, or zeros when pos[t] < 0.
 template <class E>
 __global__ __launch_bounds__(256) void k_dh_scatter(const float* dh, int64_t H, const int32_t* pos,
-                                                    int64_t T, typename E::storage* dhid) {
+                                                    int64_t T, int pieces, int64_t stride,
+                                                    typename E::storage* dhid) {
   const int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
   const int32_t c = pos[t];
   typename E::storage* out = dhid + t * H;
-  const float4* src = reinterpret_cast<const float4*>(dh + static_cast<int64_t>(c < 0 ? 0 : c) * H);
   for (int64_t k = threadIdx.x & 63; k < H / 4; k += 64) {
     float d[4] = {0.f, 0.f, 0.f, 0.f};
     if (c >= 0) {
-      const float4 v = src[k];
-      d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+      for (int q = 0; q < pieces; ++q) {
+        const float4 v = reinterpret_cast<const float4*>(dh + q * stride + static_cast<int64_t>(c) * H)[k];
+        d[0] += v.x; d[1] += v.y; d[2] += v.z; d[3] += v.w;
+      }
     }
     store4<E>(out + 4 * k, d);
   }
@@ -567,7 +576,8 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
   const int rows4 = static_cast<int>(L.t_pad / 4);
   hipLaunchKernelGGL(k_gather_rows<E>, dim3(rows4), dim3(256), 0, st, static_cast<const S*>(hidden),
                      ld_hidden, H, idx, count, hg, target, y_c, g, g_c, lse, lse_c);
-  hipLaunchKernelGGL(k_zero_rows, dim3(rows4), dim3(256), 0, st, dh, H, count);
+  const int64_t dh_stride = L.t_pad * H;
+  hipLaunchKernelGGL(k_zero_rows, dim3(rows4), dim3(256), 0, st, dh, H, count, L.dh_pieces, dh_stride);
 
   for (int64_t vb = 0; vb < L.n_vblocks; ++vb) {
     const int64_t v0 = vb * L.vc;
@@ -578,22 +588,28 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
     EpiDz<E> ez{dz, L.vc, vlen, v0, g_c, lse_c, y_c, {}, {}, {}};
     hipLaunchKernelGGL(k_bwd_dz<E>, dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez);
     // (B) dH[t][h] += sum_v dz[t][v] W[v0 + v][h]: A = dz K-major, B = W MN-major
+    // With few token rows the dH tiles cannot fill the GPU: K (the vocabulary)
+    // is cut into dh_pieces pieces, each adding into its own accumulator.
     GemmShape sb = make_shape(dz, L.vc, T, w + v0 * ld_w, ld_w, H, vlen);
     sb.m_dev = count;
     sb.msplit = 1;
     sb.sn = pick_sn_msplit(sb.n_tiles);
-    EpiAcc eb{dh, H, L.t_pad, H};
-    hipLaunchKernelGGL((k_bwd_acc<E, false, true>), dim3(gemm_grid(sb)), dim3(kThreads), 0, st, sb, eb);
+    sb.k_split = L.dh_pieces > 1 ? round_up(ceil_div(vlen, L.dh_pieces), 64) : 0;
+    const int pieces_b = L.dh_pieces > 1 ? static_cast<int>(ceil_div(vlen, sb.k_split)) : 1;
+    EpiAcc eb{dh, H, L.t_pad, H, dh_stride};
+    hipLaunchKernelGGL((k_bwd_acc<E, false, true>), dim3(gemm_grid(sb), pieces_b), dim3(kThreads), 0, st, sb,
+                       eb);
     // (C) dW[v0 + v][h] += sum_t dz[t][v] Hg[t][h]: both MN-major
     GemmShape sc = make_shape(dz, L.vc, vlen, hg, H, H, T);
     sc.k_dev = count;
     sc.msplit = 1;
     sc.sn = pick_sn_msplit(sc.n_tiles);
-    EpiAcc ec{dw + v0 * H, H, vlen, H};
+    EpiAcc ec{dw + v0 * H, H, vlen, H, 0};
     hipLaunchKernelGGL((k_bwd_acc<E, true, true>), dim3(gemm_grid(sc)), dim3(kThreads), 0, st, sc, ec);
   }
   const int t4 = static_cast<int>(ceil_div(T, 4));
-  hipLaunchKernelGGL(k_dh_scatter<E>, dim3(t4), dim3(256), 0, st, dh, H, pos, T, static_cast<S*>(dhidden));
+  hipLaunchKernelGGL(k_dh_scatter<E>, dim3(t4), dim3(256), 0, st, dh, H, pos, T, L.dh_pieces, dh_stride,
+                     static_cast<S*>(dhidden));
   return hipGetLastError();
 }
 

@@ -50,8 +50,20 @@ inline LogprobLayout logprob_layout(int64_t T, int64_t H, int64_t V, size_t esiz
 // sao_loss_backward
 struct BackwardLayout {
   int64_t t_pad, n_count_blocks, vc, n_vblocks;
+  int dh_pieces;   // K pieces of the dH product (each with its own fp32 accumulator)
   size_t blk_counts, count, idx, pos, g_c, lse_c, y_c, hg, dh, dz, total;
 };
+
+// K pieces of the dH product: enough that its output tiles (host bound) number
+// at least 512 (two per CU), at most 4.
+constexpr int kMaxDhPieces = 4;
+inline int dh_pieces(int64_t T, int64_t H) {
+  const int64_t tiles = ceil_div(T, kTile) * ceil_div(H, kTile);
+  int64_t p = ceil_div(512, tiles);
+  if (p < 1) p = 1;
+  if (p > kMaxDhPieces) p = kMaxDhPieces;
+  return static_cast<int>(p);
+}
 
 inline BackwardLayout backward_layout(int64_t T, int64_t H, int64_t V, size_t esize) {
   BackwardLayout L{};
@@ -59,6 +71,7 @@ inline BackwardLayout backward_layout(int64_t T, int64_t H, int64_t V, size_t es
   L.n_count_blocks = ceil_div(T, kRowsPerCountBlock);
   L.vc = round_up(V, kTile) < kVocabBlock ? round_up(V, kTile) : kVocabBlock;
   L.n_vblocks = ceil_div(V, L.vc);
+  L.dh_pieces = dh_pieces(T, H);
   Carve c;
   const size_t tp = static_cast<size_t>(L.t_pad);
   L.blk_counts = c.take(4 * static_cast<size_t>(L.n_count_blocks));
@@ -69,7 +82,7 @@ inline BackwardLayout backward_layout(int64_t T, int64_t H, int64_t V, size_t es
   L.lse_c = c.take(4 * tp);
   L.y_c = c.take(4 * tp);
   L.hg = c.take(esize * tp * static_cast<size_t>(H));
-  L.dh = c.take(4 * tp * static_cast<size_t>(H));
+  L.dh = c.take(4 * tp * static_cast<size_t>(H) * static_cast<size_t>(L.dh_pieces));
   L.dz = c.take(esize * tp * static_cast<size_t>(L.vc));
   L.total = c.off;
   return L;
