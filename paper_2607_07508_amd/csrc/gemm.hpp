@@ -20,10 +20,11 @@
 // gfx950's transposing LDS read (ds_read_b64_tr_b16: within each 16 lanes,
 // lane j names 4 elements of row j >> 2 and receives column j of the 4 x 16
 // block that the group names), two reads per 8-element fragment, and the
-// XOR keeps the 32 lanes of each read on distinct banks. The fragments of K step s+1 are read from LDS while step
-// s multiplies, and the workgroup barrier of a slab sits before its last K
-// step, so that the first fragments of the next slab are read while that step
-// multiplies. (Deeper rings of shorter slabs measured slower on gfx950: with
+// XOR keeps the 32 lanes of each read on distinct banks.
+//
+// The fragments of K step s+1 are read from LDS while step s multiplies, and
+// the workgroup barrier of a slab sits before its last K step, so that the
+// first fragments of the next slab are read while that step multiplies. (Deeper rings of shorter slabs measured slower on gfx950: with
 // random bf16 operands the MFMA rate is power-limited, and the extra barriers
 // cost more than the added copy slack gains.)
 //
@@ -307,7 +308,7 @@ __device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
 //   begin(n0, wm, wn, lane)                 before the K loop
 //   tile(acc, m0, n0, wm, wn, lane, lds)    after it (LDS is free)
 //   finish(mt, n0, wm, wn, lane, lds)  last (LDS is free)
-// Both operands are K-contiguous.
+// AMn / BMn select the MN-major layout for A / B.
 template <class E, bool AMn, bool BMn, class Epi>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*lds)[kStageChunks]) {
   const int tid = threadIdx.x;
