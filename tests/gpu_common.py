@@ -4,7 +4,10 @@ Tolerances (the GPU side computes in fp32 from bf16/fp32 inputs; the oracle in f
   log-probs and lse: max abs <= 2e-3 (expected ~1e-5)
   flags, counts, N: bit-exact (the drift noise keeps every ratio >= 4e-3 in
       log space from a band edge, far beyond the ~1e-5 log-prob error)
-  loss values: |d| <= 1e-3 * max(|ref|, (1/N) sum |terms|)
+  loss values: |d| <= 1e-3 * max(|ref|, (1/N) sum |terms|), or (when larger) 4x the
+      change that the measured per-token log-prob differences propagate into the
+      loss; this floor only matters where log pi is exactly 0 (a one-row vocabulary),
+      where both sides carry nothing but rounding
   g: |d| <= 1e-3 * |ref| + 1e-12 (g = -rho A / N inherits the log-prob error ~1e-5)
   advantages/returns: |d| <= 1e-6 * max(1, |ref|) (fp64 inside, rounded to fp32)
   dH, dW: Frobenius relative <= 1e-2, per-row relative <= 1e-2 on rows whose norm
@@ -129,10 +132,16 @@ def check_loss(got, ref, lp, lro, adv, mask, N):
     """Loss values against the oracle, guarded against cancellation."""
     rho = np.exp(lp - lro)
     used = (ref["flags"] == 1)
-    scale0 = np.abs(rho * adv * lp)[used].sum() / max(N, 1)
-    scale1 = np.abs(rho * adv)[used].sum() / max(N, 1)
-    for k, sc in ((0, scale0), (1, scale1)):
-        tol = TOL_LOSS * max(abs(ref["loss"][k]), sc, 1e-300)
+    n = max(N, 1)
+    scale0 = np.abs(rho * adv * lp)[used].sum() / n
+    scale1 = np.abs(rho * adv)[used].sum() / n
+    # d(rho logp)/dlogp = rho (1 + logp) and d(rho)/dlogp = rho: the loss change that
+    # the measured log-prob differences alone account for
+    dlp = np.abs(np.asarray(got["logp"], dtype=np.float64) - lp)
+    prop0 = (np.abs(rho * adv * (1.0 + lp)) * dlp)[used].sum() / n
+    prop1 = (np.abs(rho * adv) * dlp)[used].sum() / n
+    for k, sc, prop in ((0, scale0, prop0), (1, scale1, prop1)):
+        tol = max(TOL_LOSS * max(abs(ref["loss"][k]), sc, 1e-300), 4.0 * prop)
         assert abs(got["loss"][k] - ref["loss"][k]) <= tol, (k, got["loss"][k], ref["loss"][k], tol)
 
 

@@ -263,3 +263,88 @@ def test_band_without_lower_edge_and_extremes():
         # with eps_low = 1.5 the log pi = -inf token stays in band with rho = 0, and its
         # term rho A log pi is 0 * inf: NaN on both sides
         assert np.allclose(loss.cpu().numpy(), rl, rtol=1e-5, atol=1e-12, equal_nan=True)
+
+
+def test_seven_row_vocabulary():
+    """A head of seven rows: a single, mostly empty vocabulary tile."""
+    _roundtrip(small_config("v7", 67, B=3, T=500, H=64, V=7), 1.0, 1.0, 1.5)
+
+
+def test_one_row_vocabulary():
+    """With V = 1, log pi = 0 and dz = g (1 - p) = 0 exactly: both sides hold only
+    rounding there, so those are checked against their natural scale."""
+    from tests.gpu_common import check_loss
+    b = generate(small_config("v1", 61, B=3, T=500, H=64, V=1))
+    ref = oracle_pass(b, 1.0, 1.0, 1.5)
+    got = gpu_pass(b, ref["logp"], 1.0, 1.0, 1.5)
+    m = b.mask == 1
+    assert np.abs(got["logp"][m]).max() <= 1e-6 and (got["logp"][~m] == 0).all()
+    assert np.array_equal(got["flags"], ref["flags"]) and np.array_equal(got["counts"], ref["counts"])
+    check_loss(got, ref, ref["logp"], ref["lro"], ref["adv"], b.mask, ref["n"])
+    gmax = np.abs(ref["g"]).max()
+    assert np.abs(got["dh"]).max() <= 1e-5 * gmax * np.abs(b.w_head).max()
+    assert np.abs(got["dw"]).max() <= 1e-5 * gmax * np.abs(b.hidden).sum(axis=0).max()
+
+
+def _scan_case(name, seed, B, T, cu=None, mask_fn=None):
+    b = generate(small_config(name, seed, B=B, T=T, H=8, V=16))
+    if cu is not None:
+        b.cu_seqlens[:] = np.asarray(cu, dtype=np.int32)
+    if mask_fn is not None:
+        mask_fn(b)
+    adv_r, ret_r, n_r = oracle.advantage(b.values, b.rewards, b.mask, b.cu_seqlens, 0.99, 0.9, 1.5)
+    return b, adv_r, ret_r, n_r
+
+
+def _check_scan(got, adv_r, ret_r, n_r):
+    adv, ret, n = (x.cpu().numpy() for x in got)
+    assert int(n[0]) == n_r
+    assert (np.abs(adv - adv_r) <= 1e-6 * np.maximum(1, np.abs(adv_r))).all()
+    assert (np.abs(ret - ret_r) <= 1e-6 * np.maximum(1, np.abs(ret_r))).all()
+
+
+def test_scan_empty_and_observation_only_trajectories():
+    T = 5000
+    cu = [0, 0, 1200, 1200, 1201, 3300, 3300, T]          # empty segments, a one-token one
+    def obs_only(b):
+        b.mask[1201:3300] = 0                              # a trajectory with no action at all
+        b.rewards[1201:3300] = 0.25
+    b, a, r, n = _scan_case("scan-edge", 71, B=7, T=T, cu=cu, mask_fn=obs_only)
+    db = to_device(b)
+    got = sao.advantage(db.values, db.rewards, db.mask, db.cu_seqlens, 0.99, 0.9, 1.5)
+    torch.cuda.synchronize()
+    _check_scan(got, a, r, n)
+
+
+def test_scan_one_long_trajectory():
+    """One trajectory over many 2048-token tiles, ending mid-tile."""
+    T = 70001
+    b, a, r, n = _scan_case("scan-long", 72, B=1, T=T, cu=[0, T])
+    db = to_device(b)
+    got = sao.advantage(db.values, db.rewards, db.mask, db.cu_seqlens, 0.99, 0.9, 1.5)
+    torch.cuda.synchronize()
+    _check_scan(got, a, r, n)
+
+
+def test_unaligned_per_token_arrays():
+    """Slices at odd offsets take the scalar paths of the scan and the loss."""
+    b = generate(small_config("unaligned", 73, B=5, T=3001, H=64, V=200))
+    ref = oracle_pass(b, 0.99, 0.9, 1.5, backward=False)
+    db = to_device(b, ref["logp"])
+    # copy every per-token array into a buffer one element longer and take [1:]
+    def shifted(x):
+        buf = torch.empty(x.numel() + 1, dtype=x.dtype, device=x.device)
+        buf[1:] = x
+        return buf[1:]
+    vals, rews, mask = shifted(db.values), shifted(db.rewards), shifted(db.mask)
+    assert vals.data_ptr() % 16 != 0 and mask.data_ptr() % 8 != 0
+    adv, ret, n = sao.advantage(vals, rews, mask, db.cu_seqlens, 0.99, 0.9, 1.5)
+    _check_scan((adv, ret, n), ref["adv"], ref["ret"], ref["n"])
+    lp = shifted(torch.from_numpy(ref["logp"].astype(np.float32)).cuda())
+    lro = shifted(db.logp_rollout)
+    loss, g, flags, counts = sao.clipped_loss(lp, lro, shifted(torch.from_numpy(ref["adv"].astype(np.float32)).cuda()),
+                                              mask, b.cfg.eps_low, b.cfg.eps_high, n)
+    torch.cuda.synchronize()
+    assert np.array_equal(flags.cpu().numpy(), ref["flags"])
+    assert np.array_equal(counts.cpu().numpy(), ref["counts"])
+    assert np.allclose(loss.cpu().numpy(), ref["loss"], rtol=1e-5, atol=1e-12)
