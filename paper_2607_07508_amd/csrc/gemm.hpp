@@ -67,6 +67,9 @@ constexpr int kSteps = kRowChunks / 2;          // MFMA K steps per slab (two ch
 constexpr int kRowsPerLine = 16 / kRowChunks;   // tile rows per 256-byte line of the 64 banks
 static_assert(kSteps % 2 == 0, "the next slab's first step lands in f0");
 constexpr int kStageChunks = kAChunks + kBChunks;
+// Of the copies per wave of one slab, kCopyNow are issued in the last K step
+// of the slab two before it and the rest in step 0 of the slab just before it.
+constexpr int kCopyNow = 8;
 
 struct GemmShape {
   const void* a;
@@ -143,6 +146,18 @@ __device__ __forceinline__ v4u zero4() { return v4u{0u, 0u, 0u, 0u}; }
 // index modulo kRowChunks does that.
 __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r / kRowsPerLine) % kRowChunks); }
 
+// A wave-uniform value as a scalar (the builtin yields a signed int: going
+// through uint32_t keeps a widened address from being sign-extended).
+__device__ __forceinline__ uint32_t uniform_u32(uint32_t x) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(x)));
+}
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint64_t lo = uniform_u32(static_cast<uint32_t>(v));
+  const uint64_t hi = uniform_u32(static_cast<uint32_t>(v >> 32));
+  return reinterpret_cast<const void*>((hi << 32) | lo);
+}
+
 // Direct copy of 16 bytes per lane from global memory (uniform base `g` plus the
 // lane's byte offset `off`) into LDS: lane l writes LDS bytes [m0 + 16 l, +16),
 // m0 being the wave-uniform LDS byte address `lds_addr`. Issued as inline
@@ -181,24 +196,30 @@ __device__ __forceinline__ void wait_slabs_barrier(int pending) {
   }
 }
 
+// Instruction order is pinned where it matters: the compiler would otherwise
+// defer the LDS reads of the next K step behind the MFMAs of this one and then
+// wait for them, exposing the LDS latency once per step.
+__device__ __forceinline__ void pin_order() {
+#ifndef NO_PIN
+  __builtin_amdgcn_sched_barrier(0);
+#endif
+}
+
 // Fragments of one K16 step (bf16; K8 for fp32): kMI rows of A, kNI rows of B.
 struct Frags {
   v4u a[kMI];
   v4u b[kNI];
 };
 
-// K-major fragments of one operand for K step s: blocks of 32 rows at
-// wave_row0 + 32 i. Rows read by a lane differ by multiples of 32, which leaves
-// the line index modulo kRowChunks and hence the swizzle unchanged: one LDS
-// address per step, the blocks at immediate offsets. Chunks past K hold zeros
-// (written by the copy of the last slab), so no fragment needs masking.
-template <int NB>
-__device__ __forceinline__ void read_frag_k(v4u (&f)[NB], const v4u* l, int s, int wave_row0, int lane) {
+// K-major fragment i (rows wave_row0 + 32 i ..) of one operand for K step s.
+// Rows read by a lane differ by multiples of 32, which leaves the line index
+// modulo kRowChunks and hence the swizzle unchanged: one LDS address per step,
+// the blocks at immediate offsets. Chunks past K hold zeros (written by the
+// copy of the last slab), so no fragment needs masking.
+__device__ __forceinline__ v4u read_frag_k(const v4u* l, int s, int wave_row0, int i, int lane) {
   const int r32 = lane & 31;
   const int c = 2 * s + (lane >> 5);
-  const v4u* p = l + (wave_row0 + r32) * kRowChunks + swz(r32, c);
-#pragma unroll
-  for (int i = 0; i < NB; ++i) f[i] = p[i * 32 * kRowChunks];
+  return l[(wave_row0 + r32) * kRowChunks + swz(r32, c) + i * 32 * kRowChunks];
 }
 
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
@@ -215,10 +236,10 @@ struct MnSlab {
 };
 __device__ __forceinline__ int mn_swz(int k, int c) { return c ^ (4 * (k & 3)); }
 
-// MN-major fragments of one operand for K step s (same k <-> lane mapping as the
-// K-major path: lane half h holds the k chunk 2 s + h, element e at k offset e).
-template <class E, int NB>
-__device__ __forceinline__ void read_frag_mn(v4u (&f)[NB], const v4u* l, int s, int wave_row0, int lane) {
+// MN-major fragment i of one operand for K step s (same k <-> lane mapping as
+// the K-major path: lane half h holds the k chunk 2 s + h, element e at k offset e).
+template <class E>
+__device__ __forceinline__ v4u read_frag_mn(const v4u* l, int s, int wave_row0, int i, int lane) {
   using G = MnSlab<E>;
   const char* base = reinterpret_cast<const char*>(l);
   const int h = lane >> 5;
@@ -227,42 +248,53 @@ __device__ __forceinline__ void read_frag_mn(v4u (&f)[NB], const v4u* l, int s, 
     // and receives column m0 + j of rows k0 .. k0+3; two reads give rows k0 .. k0+7.
     const int j = lane & 15;
     const int k = 8 * (2 * s + h) + (j >> 2);
-#pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int m = wave_row0 + 32 * i + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
-      const int off = k * G::kRowBytes + mn_swz(k, m >> 3) * 16 + (m & 7) * 2;
-      const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(base + off));
-      const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(base + off + 4 * G::kRowBytes));
-      const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
-      f[i] = v4u{a.x, a.y, b.x, b.y};
-    }
+    const int m = wave_row0 + 32 * i + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+    const int off = k * G::kRowBytes + mn_swz(k, m >> 3) * 16 + (m & 7) * 2;
+    const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(base + off));
+    const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(base + off + 4 * G::kRowBytes));
+    const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+    return v4u{a.x, a.y, b.x, b.y};
   } else {
     // fp32: element e of the chunk is row 4 (2 s + h) + e of column wave_row0 + 32 i + (lane & 31).
+    const int m = wave_row0 + 32 * i + (lane & 31);
+    uint32_t x[4];
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int m = wave_row0 + 32 * i + (lane & 31);
-      uint32_t x[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int k = 4 * (2 * s + h) + e;
-        x[e] = *reinterpret_cast<const uint32_t*>(base + k * G::kRowBytes + mn_swz(k, m >> 2) * 16 + (m & 3) * 4);
-      }
-      f[i] = v4u{x[0], x[1], x[2], x[3]};
+    for (int e = 0; e < 4; ++e) {
+      const int k = 4 * (2 * s + h) + e;
+      x[e] = *reinterpret_cast<const uint32_t*>(base + k * G::kRowBytes + mn_swz(k, m >> 2) * 16 + (m & 3) * 4);
     }
+    return v4u{x[0], x[1], x[2], x[3]};
+  }
+}
+
+// Fragment idx (0 .. kMI + kNI - 1) of K step s in the order in which the
+// MFMAs of a step first use them: A0, B0, B1, .., B(kNI-1), A1, .., A(kMI-1).
+template <class E, bool AMn, bool BMn>
+__device__ __forceinline__ void read_one(Frags& f, int idx, const v4u* la, const v4u* lb, int s, int wm, int wn,
+                                         int lane) {
+  const bool is_a = idx == 0 || idx > kNI;
+  const int i = idx == 0 ? 0 : idx - kNI;
+  if (is_a) {
+    if constexpr (AMn)
+      f.a[i] = read_frag_mn<E>(la, s, wm * (kBM / 2), i, lane);
+    else
+      f.a[i] = read_frag_k(la, s, wm * (kBM / 2), i, lane);
+  } else {
+    if constexpr (BMn)
+      f.b[idx - 1] = read_frag_mn<E>(lb, s, wn * (kBN / kWavesN), idx - 1, lane);
+    else
+      f.b[idx - 1] = read_frag_k(lb, s, wn * (kBN / kWavesN), idx - 1, lane);
   }
 }
 
 template <class E, bool AMn, bool BMn>
 __device__ __forceinline__ void read_frags(Frags& f, const v4u* la, const v4u* lb, int s, int wm, int wn,
                                            int lane) {
-  if constexpr (AMn)
-    read_frag_mn<E>(f.a, la, s, wm * (kBM / 2), lane);
-  else
-    read_frag_k(f.a, la, s, wm * (kBM / 2), lane);
-  if constexpr (BMn)
-    read_frag_mn<E>(f.b, lb, s, wn * (kBN / kWavesN), lane);
-  else
-    read_frag_k(f.b, lb, s, wn * (kBN / kWavesN), lane);
+#pragma unroll
+  for (int idx = 0; idx < kMI + kNI; ++idx) {
+    read_one<E, AMn, BMn>(f, idx, la, lb, s, wm, wn, lane);
+    pin_order();  // in the same order as the loop reads them, so waits agree
+  }
 }
 
 // The MFMAs of row block i of one K step.
@@ -278,13 +310,27 @@ __device__ __forceinline__ void mma_step(f32x16_t (&acc)[kMI][kNI], const Frags&
   for (int i = 0; i < kMI; ++i) mma_row<E>(acc, f, i);
 }
 
-// Instruction order is pinned where it matters: the compiler would otherwise
-// defer the LDS reads of the next K step behind the MFMAs of this one and then
-// wait for them, exposing the LDS latency once per step.
-__device__ __forceinline__ void pin_order() {
-#ifndef NO_PIN
-  __builtin_amdgcn_sched_barrier(0);
-#endif
+// One K step of one wave: the kMI x kNI MFMAs of `cur`, with the fragments of
+// the next step (read into `nxt` from la / lb) and the hook's copies placed
+// between them. A wave issues in order and each SIMD runs one wave, so the
+// MFMA pipe idles while the wave issues a burst of other instructions; the
+// reads therefore go one after every kReadEvery MFMAs, in the order in which
+// the next step uses them, and the hook may add a copy after any MFMA.
+constexpr int kReadEvery = 1;
+static_assert((kMI + kNI) * kReadEvery <= kMI * kNI, "all reads fit in one step");
+template <class E, bool AMn, bool BMn, class Hook>
+__device__ __forceinline__ void mma_step_mix(f32x16_t (&acc)[kMI][kNI], const Frags& cur, Frags& nxt,
+                                             const v4u* la, const v4u* lb, int s_next, int wm, int wn,
+                                             int lane, Hook&& hook) {
+#pragma unroll
+  for (int t = 0; t < kMI * kNI; ++t) {
+    Mma<E>::run(acc[t / kNI][t % kNI], cur.a[t / kNI], cur.b[t % kNI]);
+    pin_order();
+    if (t % kReadEvery == kReadEvery - 1 && t / kReadEvery < kMI + kNI)
+      read_one<E, AMn, BMn>(nxt, t / kReadEvery, la, lb, s_next, wm, wn, lane);
+    hook(t);
+    pin_order();
+  }
 }
 
 // LDS writes of this thread are complete, then the workgroup barrier. Unlike
@@ -313,7 +359,7 @@ template <class E, bool AMn, bool BMn, class Epi>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*lds)[kStageChunks]) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = static_cast<int>(uniform_u32(static_cast<uint32_t>(tid >> 6)));  // keeps copy addresses scalar
   const int wm = wave / kWavesN;
   const int wn = wave % kWavesN;
 
@@ -366,7 +412,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   // writes chunk l). K-major: copy q covers kRowsPerCopy tile rows from
   // (wave * Q + q) * kRowsPerCopy, lane l row + l / kRowChunks at physical chunk
   // l % kRowChunks, fetching the logical chunk swizzled there; lc[q] is that chunk
-  // and off[q] the row's byte offset. MN-major: copy q covers G::kRowsPerCopy slab
+  // and off[q] the byte offset of that row and chunk in slab 0. MN-major: copy q covers G::kRowsPerCopy slab
   // rows (k) from (wave * Q + q) * G::kRowsPerCopy, lane l row + l / G::kChunksPerRow
   // at physical chunk l % G::kChunksPerRow, fetching the logical column chunk
   // mn_swz maps there; lc[q] is the slab row and off[q] the byte offset of that
@@ -391,7 +437,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
       lc = swz(r, lane % kRowChunks);
       int64_t row = row0 + r;
       row = row < valid ? row : valid - 1;
-      off = static_cast<uint32_t>(row * ld * esz);
+      off = static_cast<uint32_t>(row * ld * esz + static_cast<int64_t>(lc) * P * esz);
     }
   };
 #pragma unroll
@@ -401,18 +447,18 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   // Byte offset of slab kt for copy q, and whether that copy's data lies inside K.
   const uint32_t slab_a = static_cast<uint32_t>(static_cast<int64_t>(G::kRows) * s.lda * esz);
   const uint32_t slab_b = static_cast<uint32_t>(static_cast<int64_t>(G::kRows) * s.ldb * esz);
-  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0]));
+  const uint32_t lds0 = uniform_u32(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0])));
   v4u* lds_flat = &lds[0][0];
   auto copy_one = [&](int q, int kt, int stage) {
     const bool is_a = q < QA;
     const int qq = is_a ? q : q - QA;
     const int slot = (is_a ? 0 : kAChunks) + (wave * (is_a ? QA : QB) + qq) * 64;
     const bool mn = is_a ? AMn : BMn;
-    const uint32_t k_off = mn ? static_cast<uint32_t>(kt) * (is_a ? slab_a : slab_b)
-                              : static_cast<uint32_t>((static_cast<int64_t>(kt) * kRowChunks +
-                                                       (is_a ? lca[qq] : lcb[qq])) * P * esz);
-    dma16(is_a ? a_base : b_base, (is_a ? offa[qq] : offb[qq]) + k_off,
-          __builtin_amdgcn_readfirstlane(lds0 + static_cast<uint32_t>(stage * kStageChunks + slot) * 16));
+    // The slab's offset is uniform and goes into the scalar base address.
+    const int64_t k_off = mn ? static_cast<int64_t>(kt) * (is_a ? slab_a : slab_b)
+                             : static_cast<int64_t>(kt) * kRowChunks * P * esz;
+    dma16(uniform_ptr((is_a ? a_base : b_base) + k_off), is_a ? offa[qq] : offb[qq],
+          uniform_u32(lds0 + static_cast<uint32_t>(stage * kStageChunks + slot) * 16));
   };
   auto inside_k = [&](int q, int kt) -> bool {
     const bool is_a = q < QA;
@@ -459,18 +505,26 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   }
   Frags f0, f1;
   read_frags<E, AMn, BMn>(f0, lds[0], lds[0] + kAChunks, 0, wm, wn, lane);
+  constexpr int kCopyNext = kCopiesPerSlab - kCopyNow;
+  static_assert(kCopyNow > 0 && kCopyNext > 0 && (kMI * kNI) % kCopyNow == 0 && (kMI * kNI) % kCopyNext == 0,
+                "copies spread evenly over a step's MFMAs");
+  bool carry = false;  // the previous iteration left copies of slab kt + 1 to step 0
   for (int kt = 0; kt < nk; ++kt) {
     const int stage = kt % kStages;
-    // K steps 0 .. kSteps-2: the fragments of the next step are read first, then
-    // this step multiplies (f0 holds the even steps, f1 the odd ones).
+    const int cstage = (kt + 1) % kStages;
+    // K steps 0 .. kSteps-2 multiply f0 / f1 (even / odd steps) while reading
+    // the next step's fragments from this stage. Step 0 also issues the copies
+    // of slab kt + 1 that the previous iteration left over.
+    constexpr int kEveryNext = kMI * kNI / kCopyNext;
 #pragma unroll
     for (int st = 0; st + 1 < kSteps; ++st) {
       Frags& cur = st % 2 == 0 ? f0 : f1;
       Frags& nxt = st % 2 == 0 ? f1 : f0;
-      read_frags<E, AMn, BMn>(nxt, lds[stage], lds[stage] + kAChunks, st + 1, wm, wn, lane);
-      pin_order();
-      mma_step<E>(acc, cur);
-      pin_order();
+      mma_step_mix<E, AMn, BMn>(acc, cur, nxt, lds[stage], lds[stage] + kAChunks, st + 1, wm, wn, lane,
+                                [&](int t) {
+                                  if (st == 0 && t % kEveryNext == kEveryNext - 1 && carry)
+                                    copy_one(kCopyNow + t / kEveryNext, kt + 1, cstage);
+                                });
     }
     Frags& last = kSteps % 2 == 0 ? f1 : f0;
     const int kn = kt + kStages;  // the slab that refills this stage
@@ -478,28 +532,19 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
       const int rest = nk - kt - 2;
       wait_slabs_barrier<kCopiesPerSlab>(rest < kStages - 2 ? rest : kStages - 2);
     }
-    // Unconditional, so that the LDS wait counts agree on both paths; after the
-    // last slab it reads a drained stage and the values go unused.
-    const int nstage = (kt + 1) % kStages;
-    read_frags<E, AMn, BMn>(f0, lds[nstage], lds[nstage] + kAChunks, 0, wm, wn, lane);
-    pin_order();
-    // Full slabs refill the freed stage with copies spread over the last step's
-    // MFMAs; the last slab, when K ends inside it, is copied after them with its
-    // zero fill.
+    // The last step reads the next slab's first fragments (unconditionally, so
+    // that the LDS wait counts agree on both paths; after the last slab it reads
+    // a drained stage and the values go unused). Full slabs refill the freed
+    // stage: kCopyNow copies spread over this step's MFMAs, the rest over step 0
+    // of the next slab; the last slab, when K ends inside it, is copied after
+    // them with its zero fill.
     const bool refill = kn < nk - 1 || (kn == nk - 1 && !tail);
-    constexpr int kPerRow = kCopiesPerSlab / kMI;
-    static_assert(kCopiesPerSlab % kMI == 0, "copies spread evenly over the row blocks");
-#pragma unroll
-    for (int i = 0; i < kMI; ++i) {
-      mma_row<E>(acc, last, i);
-      pin_order();
-      if (refill) {
-#pragma unroll
-        for (int q = 0; q < kPerRow; ++q) copy_one(i * kPerRow + q, kn, stage);
-      }
-      pin_order();
-    }
+    constexpr int kEveryNow = kMI * kNI / kCopyNow;
+    mma_step_mix<E, AMn, BMn>(acc, last, f0, lds[cstage], lds[cstage] + kAChunks, 0, wm, wn, lane, [&](int t) {
+      if (t % kEveryNow == kEveryNow - 1 && refill) copy_one(t / kEveryNow, kn, stage);
+    });
     if (kn == nk - 1 && tail) copy_slab(kn, stage);
+    carry = refill;
   }
   // Every copy has landed (the last wait drained them); once every wave's LDS
   // reads have returned, the epilogue may use LDS as scratch.

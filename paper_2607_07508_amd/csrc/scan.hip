@@ -19,6 +19,7 @@
 // 8 tokens that it reads and writes with 16-byte vector accesses.
 #include "common.hpp"
 #include "launch.hpp"
+
 #include "../../include/sao.h"
 
 namespace sao {
@@ -126,6 +127,7 @@ __global__ __launch_bounds__(256) void k_check_segments(const int32_t* cu, int32
 
 constexpr int kScanThreads = 256;
 constexpr int kScanPer = 8;                               // tokens per thread per tile
+static_assert(kScanPer % 4 == 0, "whole blocks are read as 16-byte vectors");
 constexpr int kScanTile = kScanThreads * kScanPer;        // tokens per tile
 
 // State after applying map M to (Vn, R, A, G).
@@ -193,13 +195,17 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
     if (full) {
       const f32x4_t* pv = reinterpret_cast<const f32x4_t*>(values + c0);
       const f32x4_t* pr = reinterpret_cast<const f32x4_t*>(rewards + c0);
-      const f32x4_t v0 = pv[0], v1 = pv[1], r0 = pr[0], r1 = pr[1];
-      const uint2 m8 = *reinterpret_cast<const uint2*>(mask + c0);
+      const uint32_t* pm = reinterpret_cast<const uint32_t*>(mask + c0);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        v[j] = v0[j]; v[4 + j] = v1[j]; r[j] = r0[j]; r[4 + j] = r1[j];
-        act[j] = ((m8.x >> (8 * j)) & 0xffu) != 0;
-        act[4 + j] = ((m8.y >> (8 * j)) & 0xffu) != 0;
+      for (int q = 0; q < kScanPer / 4; ++q) {
+        const f32x4_t vq = pv[q], rq = pr[q];
+        const uint32_t mq = pm[q];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          v[4 * q + j] = vq[j];
+          r[4 * q + j] = rq[j];
+          act[4 * q + j] = ((mq >> (8 * j)) & 0xffu) != 0;
+        }
       }
     } else {
 #pragma unroll
@@ -263,10 +269,11 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
     if (full) {
       f32x4_t* qa = reinterpret_cast<f32x4_t*>(adv + c0);
       f32x4_t* qg = reinterpret_cast<f32x4_t*>(ret + c0);
-      qa[0] = f32x4_t{oa[0], oa[1], oa[2], oa[3]};
-      qa[1] = f32x4_t{oa[4], oa[5], oa[6], oa[7]};
-      qg[0] = f32x4_t{og[0], og[1], og[2], og[3]};
-      qg[1] = f32x4_t{og[4], og[5], og[6], og[7]};
+#pragma unroll
+      for (int q = 0; q < kScanPer / 4; ++q) {
+        qa[q] = f32x4_t{oa[4 * q], oa[4 * q + 1], oa[4 * q + 2], oa[4 * q + 3]};
+        qg[q] = f32x4_t{og[4 * q], og[4 * q + 1], og[4 * q + 2], og[4 * q + 3]};
+      }
     } else {
 #pragma unroll
       for (int j = 0; j < kScanPer; ++j) {
