@@ -8,8 +8,7 @@
 // bf16 or 32 fp32 elements) through an LDS ring of kStages x (32 KB of A + 32 KB
 // of B). Slabs are copied global -> LDS directly (global_load_lds_dwordx4: no
 // staging registers, no LDS store instructions), kStages - 1 slabs ahead of the
-// MFMAs; the copies of a slab are spread over the MFMAs of the last K step of
-// the slab before it, right after the barrier that frees their stage.
+// MFMAs.
 //
 // Each operand is stored either K-major ([mn][k], row stride ld) or MN-major
 // ([k][mn], row stride ld), chosen at compile time. A K-major slab sits in LDS
@@ -22,11 +21,18 @@
 // block that the group names), two reads per 8-element fragment, and the
 // XOR keeps the 32 lanes of each read on distinct banks.
 //
-// The fragments of K step s+1 are read from LDS while step s multiplies, and
-// the workgroup barrier of a slab sits before its last K step, so that the
-// first fragments of the next slab are read while that step multiplies. (Deeper rings of shorter slabs measured slower on gfx950: with
-// random bf16 operands the MFMA rate is power-limited, and the extra barriers
-// cost more than the added copy slack gains.)
+// Issue schedule. Each SIMD runs one wave of the workgroup and a wave issues
+// in order, so anything issued in a burst between MFMAs leaves the MFMA pipe
+// idle. The fragments of K step s+1 are therefore read one per MFMA over the
+// first half of step s, in the order step s+1 uses them, and the copies of a
+// slab go one after every other MFMA: half in the last step of the slab two
+// before it (right after the barrier that frees their stage), half in step 0
+// of the slab just before it. The workgroup barrier of a slab sits before its
+// last K step, so the first fragments of the next slab are read while that
+// step multiplies. (Measured at the LM-head forward shape: bursts of reads and
+// copies cost 103k cycles per tile against 65.5k of MFMA work, this schedule
+// 81k. Deeper rings of shorter slabs measured slower: the extra barriers cost
+// more than the added copy slack gains.)
 //
 // Accumulator layout of v_mfma_f32_32x32x{16_bf16,2_f32} (block of 32 x 32):
 // lane l, register r holds row (r & 3) + 8 * (r >> 2) + 4 * (l >> 5), column l & 31.
