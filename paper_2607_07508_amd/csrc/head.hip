@@ -156,15 +156,15 @@ struct EpiLse {
     }
   }
 
-  __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t, int wm, int,
-                                       int lane, void*) {
-    // Rows at or past the vocabulary end (last tile only) read as -inf; the
-    // accumulators themselves are left untouched so they can stay in AGPRs.
-    const int64_t lim64 = M - m0 - wm * (kBM / 2) - 4 * (lane >> 5);
-    const int lim = lim64 > kBM ? kBM : static_cast<int>(lim64);
+  // Running (max, sum exp) per token column over this wave's 128 vocabulary
+  // rows; with kMasked, rows at or past the vocabulary end (last tile only)
+  // read as -inf. The accumulators themselves are left untouched so they can
+  // stay in AGPRs.
+  template <bool kMasked>
+  __device__ __forceinline__ void update(const f32x16_t (&acc)[kMI][kNI], int lim) {
     auto z_at = [&](int mi, int ni, int r) -> float {
       const int off = mi * 32 + (r & 3) + 8 * (r >> 2);
-      return off < lim ? acc[mi][ni][r] : -__builtin_inff();
+      return !kMasked || off < lim ? acc[mi][ni][r] : -__builtin_inff();
     };
 #pragma unroll
     for (int ni = 0; ni < kNI; ++ni) {
@@ -183,6 +183,19 @@ struct EpiLse {
         for (int r = 0; r < 16; ++r) s += fast_exp2(fmaf(z_at(mi, ni, r), kLog2e, -sc));
       rm[ni] = mn;
       rs[ni] = s;
+    }
+  }
+
+  __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t, int wm, int,
+                                       int lane, void*) {
+    // Vocabulary rows from this wave's first row; the lane's rows sit at offsets
+    // up to 123 past it plus 4 (lane >> 5), so 128 rows leave nothing to mask.
+    const int64_t rows = M - m0 - wm * (kBM / 2);
+    if (rows >= kBM / 2) {
+      update<false>(acc, 0);
+    } else {
+      const int64_t lim64 = rows - 4 * (lane >> 5);
+      update<true>(acc, lim64 > kBM ? kBM : static_cast<int>(lim64));
     }
   }
 
@@ -331,6 +344,7 @@ struct EpiDz {
   const int32_t* y_c;
   float gl[kNI], ll[kNI];
   int64_t yl[kNI];
+  int yt[kNI];  // target row of the column's token inside the current tile, or -8 when outside
 
   __device__ __forceinline__ void begin(int64_t n0, int, int wn, int lane) {
 #pragma unroll
@@ -342,14 +356,30 @@ struct EpiDz {
     }
   }
 
-  // dz of accumulator (mi, ni, registers 4j .. 4j+3): four consecutive vocabulary rows v..v+3.
-  __device__ __forceinline__ void dz4(const f32x16_t (&acc)[kMI][kNI], int mi, int ni, int j, int64_t v,
-                                      float (&d)[4]) const {
+  // dz of accumulator (mi, ni, registers 4j .. 4j+3): four consecutive
+  // vocabulary rows starting at tile row vt. dz = g (onehot - p): the target
+  // row of a token lies in a given tile rarely, so the one-hot term is a branch
+  // on yt (the target's tile row, or far outside), and rows at or past the end
+  // of the block (last tile only, kMasked) are zero.
+  template <bool kMasked>
+  __device__ __forceinline__ void dz4(const f32x16_t (&acc)[kMI][kNI], int mi, int ni, int j, int vt,
+                                      int rows, float (&d)[4]) const {
+    float p[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float p = fast_exp2(fmaf(acc[mi][ni][4 * j + e], kLog2e, -ll[ni]));
-      const float oh = (v + e == yl[ni]) ? 1.0f : 0.0f;
-      d[e] = (v + e < m_valid) ? gl[ni] * (oh - p) : 0.0f;
+      p[e] = fast_exp2(fmaf(acc[mi][ni][4 * j + e], kLog2e, -ll[ni]));
+      d[e] = gl[ni] * -p[e];
+    }
+    const unsigned k = static_cast<unsigned>(yt[ni] - vt);
+    if (k < 4u) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (static_cast<unsigned>(e) == k) d[e] = gl[ni] * (1.0f - p[e]);
+    }
+    if constexpr (kMasked) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (vt + e >= rows) d[e] = 0.0f;
     }
   }
 
@@ -360,27 +390,42 @@ struct EpiDz {
 
   __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t n0, int wm, int wn,
                                        int lane, void* smem) {
+    // Valid rows of this tile, and whether all of this wave's 128 rows are.
+    const int64_t rows64 = m_valid - m0;
+    const int rows = rows64 > kBM ? kBM : static_cast<int>(rows64);
+    const bool full = rows >= (wm + 1) * (kBM / 2);
+#pragma unroll
+    for (int ni = 0; ni < kNI; ++ni) {
+      const int64_t y = yl[ni] - m0;
+      yt[ni] = y >= 0 && y < kBM ? static_cast<int>(y) : -8;
+    }
     if constexpr (sizeof(typename E::storage) == 2) {
       // Stage the 256 x 256 bf16 tile in LDS as [t][v] (128 KB), then write it
       // with 16-byte stores.
       v4u* tile16 = static_cast<v4u*>(smem);       // [256 rows][32 chunks]
+      auto stage = [&](auto masked) {
 #pragma unroll
-      for (int ni = 0; ni < kNI; ++ni) {
-        const int t = acc_col(wn, ni, lane);
+        for (int ni = 0; ni < kNI; ++ni) {
+          const int t = acc_col(wn, ni, lane);
 #pragma unroll
-        for (int mi = 0; mi < kMI; ++mi) {
+          for (int mi = 0; mi < kMI; ++mi) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int vl = acc_row(wm, mi, 4 * j, lane);   // multiple of 4
-            float d[4];
-            dz4(acc, mi, ni, j, m0 + vl, d);
-            const uint32_t lo = pack_bf16x2(d[0], d[1]);
-            const uint32_t hi = pack_bf16x2(d[2], d[3]);
-            uint2* p = reinterpret_cast<uint2*>(tile16 + t * 32 + tswz(t, vl >> 3)) + ((vl >> 2) & 1);
-            *p = make_uint2(lo, hi);
+            for (int j = 0; j < 4; ++j) {
+              const int vl = acc_row(wm, mi, 4 * j, lane);   // multiple of 4
+              float d[4];
+              dz4<decltype(masked)::value>(acc, mi, ni, j, vl, rows, d);
+              const uint32_t lo = pack_bf16x2(d[0], d[1]);
+              const uint32_t hi = pack_bf16x2(d[2], d[3]);
+              uint2* p = reinterpret_cast<uint2*>(tile16 + t * 32 + tswz(t, vl >> 3)) + ((vl >> 2) & 1);
+              *p = make_uint2(lo, hi);
+            }
           }
         }
-      }
+      };
+      if (full)
+        stage(std::false_type{});
+      else
+        stage(std::true_type{});
       __syncthreads();
       const int tid = threadIdx.x;
       // [t][v]: thread takes chunk c of row t for 32 (t, c) pairs.
@@ -400,10 +445,10 @@ struct EpiDz {
         for (int mi = 0; mi < kMI; ++mi) {
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const int64_t v = m0 + acc_row(wm, mi, 4 * j, lane);
+            const int vl = acc_row(wm, mi, 4 * j, lane);
             float d[4];
-            dz4(acc, mi, ni, j, v, d);
-            store4<E>(row + v, d);
+            dz4<true>(acc, mi, ni, j, vl, rows, d);
+            store4<E>(row + m0 + vl, d);
           }
         }
       }
