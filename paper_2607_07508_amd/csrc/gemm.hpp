@@ -62,7 +62,7 @@ constexpr int kBM = 256;                        // rows of A per tile
 constexpr int kBN = 256;                        // rows of B per tile
 constexpr int kMI = 4;                          // 32-row MFMA blocks per wave along M
 constexpr int kNI = 4;                          // 32-column MFMA blocks per wave along N
-constexpr int kThreads = 256;                   // 4 waves: 2 along M x 2 along N
+constexpr int kThreads = 256;                   // 4 waves: 2 along M x 2 along N, one per SIMD
 constexpr int kWavesN = 2;
 constexpr int kRowChunks = 8;                   // 16-byte chunks per LDS row (128 bytes of K)
 constexpr int kAChunks = kBM * kRowChunks;      // 32 KB
@@ -303,19 +303,6 @@ __device__ __forceinline__ void read_frags(Frags& f, const v4u* la, const v4u* l
   }
 }
 
-// The MFMAs of row block i of one K step.
-template <class E>
-__device__ __forceinline__ void mma_row(f32x16_t (&acc)[kMI][kNI], const Frags& f, int i) {
-#pragma unroll
-  for (int j = 0; j < kNI; ++j) Mma<E>::run(acc[i][j], f.a[i], f.b[j]);
-}
-
-template <class E>
-__device__ __forceinline__ void mma_step(f32x16_t (&acc)[kMI][kNI], const Frags& f) {
-#pragma unroll
-  for (int i = 0; i < kMI; ++i) mma_row<E>(acc, f, i);
-}
-
 // One K step of one wave: the kMI x kNI MFMAs of `cur`, with the fragments of
 // the next step (read into `nxt` from la / lb) and the hook's copies placed
 // between them. A wave issues in order and each SIMD runs one wave, so the
@@ -425,8 +412,8 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   // row and column in slab 0. Offsets are 32-bit: operands are limited to 2^31
   // elements on the host. Rows (K-major) or columns (MN-major) past the valid
   // range read the last valid one; their results are never stored.
-  constexpr int QA = kAChunks / 64 / 4;  // copies per wave per A slab
-  constexpr int QB = kBChunks / 64 / 4;  // copies per wave per B slab
+  constexpr int QA = kAChunks / 64 / (kThreads / 64);  // copies per wave per A slab
+  constexpr int QB = kBChunks / 64 / (kThreads / 64);  // copies per wave per B slab
   constexpr int kCopiesPerSlab = QA + QB;
   uint32_t offa[QA], offb[QB];
   int lca[QA], lcb[QB];
