@@ -49,7 +49,12 @@
 // (SN x 256/SN), so an M-tile's rows are fetched by one XCD only. The split
 // dimension is dealt out to the XCDs in turn (XCD x takes tiles x, x + 8, ...),
 // so that when only part of it holds valid rows (a device-side count below the
-// host bound) every XCD still gets its share of the work.
+// host bound) every XCD still gets its share of the work. In N-split mode the
+// XCD-to-column assignment rotates by one XCD from one M group to the next.
+// (Measured: with 162 N tiles the forward ran 12 % faster rotated; rotating
+// only the last, partial N group gained nothing, so this is not the tail's
+// balance alone. With 181 N tiles rotation costs about 0.5 %.) M-split keeps
+// the assignment fixed, so that each XCD keeps streaming its own M tiles.
 #pragma once
 
 #include <type_traits>
@@ -368,7 +373,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
     n_tile = (w % nw) * sn + slot % sn;
     mt = (w / nw) * (256 / sn) + (slot / sn) * 8 + xcd;
   } else {
-    n_tile = (w % nw) * 8 * sn + (slot % sn) * 8 + xcd;
+    n_tile = (w % nw) * 8 * sn + (slot % sn) * 8 + (xcd + w / nw) % 8;
     mt = (w / nw) * (32 / sn) + slot / sn;
   }
 
