@@ -403,8 +403,11 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
     for (int j = 0; j < kNI; ++j) acc[i][j] = f32x16_t{};
 
   const int esz = static_cast<int>(sizeof(typename E::storage));
-  const char* a_base = static_cast<const char*>(s.a) + (AMn ? k0 * s.lda : k0) * esz;
-  const char* b_base = static_cast<const char*>(s.b) + (BMn ? k0 * s.ldb : k0) * esz;
+  // The scalar bases point at the tile's first row (K-major) or column
+  // (MN-major) of the K piece, so that a lane's 32-bit offset spans one tile
+  // of rows or one slab of k rows, whatever the operand's size.
+  const char* a_base = static_cast<const char*>(s.a) + (AMn ? k0 * s.lda + m0 : k0 + m0 * s.lda) * esz;
+  const char* b_base = static_cast<const char*>(s.b) + (BMn ? k0 * s.ldb + n0 : k0 + n0 * s.ldb) * esz;
   using G = MnSlab<E>;
   // Every 1 KB copy instruction of a wave fills 64 consecutive LDS chunks (lane l
   // writes chunk l). K-major: copy q covers kRowsPerCopy tile rows from
@@ -414,9 +417,9 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   // rows (k) from (wave * Q + q) * G::kRowsPerCopy, lane l row + l / G::kChunksPerRow
   // at physical chunk l % G::kChunksPerRow, fetching the logical column chunk
   // mn_swz maps there; lc[q] is the slab row and off[q] the byte offset of that
-  // row and column in slab 0. Offsets are 32-bit: operands are limited to 2^31
-  // elements on the host. Rows (K-major) or columns (MN-major) past the valid
-  // range read the last valid one; their results are never stored.
+  // row and column in slab 0. Offsets are relative to the tile's base. Rows
+  // (K-major) or columns (MN-major) past the valid range read the last valid
+  // one; their results are never stored.
   constexpr int QA = kAChunks / 64 / (kThreads / 64);  // copies per wave per A slab
   constexpr int QB = kBChunks / 64 / (kThreads / 64);  // copies per wave per B slab
   constexpr int kCopiesPerSlab = QA + QB;
@@ -426,15 +429,14 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
     if constexpr (decltype(mn_major)::value) {
       const int k = (wave * Q + q) * G::kRowsPerCopy + lane / G::kChunksPerRow;
       const int c = mn_swz(k, lane % G::kChunksPerRow);
-      int64_t col = row0 + static_cast<int64_t>(c) * P;
-      if (col >= valid) col = (valid - 1) / P * P;
+      int64_t col = static_cast<int64_t>(c) * P;                     // from the tile's first column
+      if (row0 + col >= valid) col = (valid - 1) / P * P - row0;    // row0 is a multiple of P
       lc = k;
       off = static_cast<uint32_t>((static_cast<int64_t>(k) * ld + col) * esz);
     } else {
       const int r = (wave * Q + q) * kRowsPerCopy + lane / kRowChunks;
       lc = swz(r, lane % kRowChunks);
-      int64_t row = row0 + r;
-      row = row < valid ? row : valid - 1;
+      const int64_t row = row0 + r < valid ? r : valid - 1 - row0;  // from the tile's first row
       off = static_cast<uint32_t>(row * ld * esz + static_cast<int64_t>(lc) * P * esz);
     }
   };
@@ -443,8 +445,8 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
 #pragma unroll
   for (int q = 0; q < QB; ++q) setup(std::bool_constant<BMn>{}, QB, q, n0, n_valid, s.ldb, offb[q], lcb[q]);
   // Byte offset of slab kt for copy q, and whether that copy's data lies inside K.
-  const uint32_t slab_a = static_cast<uint32_t>(static_cast<int64_t>(G::kRows) * s.lda * esz);
-  const uint32_t slab_b = static_cast<uint32_t>(static_cast<int64_t>(G::kRows) * s.ldb * esz);
+  const int64_t slab_a = static_cast<int64_t>(G::kRows) * s.lda * esz;
+  const int64_t slab_b = static_cast<int64_t>(G::kRows) * s.ldb * esz;
   const uint32_t lds0 = uniform_u32(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0])));
   v4u* lds_flat = &lds[0][0];
   auto copy_one = [&](int q, int kt, int stage) {

@@ -348,3 +348,39 @@ def test_unaligned_per_token_arrays():
     assert np.array_equal(flags.cpu().numpy(), ref["flags"])
     assert np.array_equal(counts.cpu().numpy(), ref["counts"])
     assert np.allclose(loss.cpu().numpy(), ref["loss"], rtol=1e-5, atol=1e-12)
+
+
+
+def test_backward_operand_past_4gib():
+    # About 150k token rows reach the backward, so its bf16 dz scratch (rows x
+    # 16384 vocabulary entries) spans 4.9 GB and the dH product reads a K-major
+    # operand past the reach of a 32-bit byte offset from the operand's start.
+    # Both sides get the same seeded g; the oracle recomputes lse and dH for
+    # sampled rows, taken mostly past compacted row 131072.
+    T, H, V = 150000, 64, 16384
+    cfg = small_config("dz-past-4gib", 41, B=16, T=T, H=H, V=V, act_span=(64, 400), obs_span=(1, 4))
+    b = generate(cfg)
+    rng = np.random.default_rng(41)
+    g = (rng.standard_normal(T) / T).astype(np.float32)
+    g[rng.random(T) < 0.01] = 0.0
+    say(f"case dz-past-4gib: T={T} H={H} V={V}, {int((g != 0).sum())} backward rows")
+    assert int((g != 0).sum()) * V * 2 > 2**32
+    dev = "cuda"
+    hid = torch.from_numpy(bf16_bits(b.hidden)).view(torch.bfloat16).to(dev)
+    w = torch.from_numpy(bf16_bits(b.w_head)).view(torch.bfloat16).to(dev)
+    tgt = torch.from_numpy(b.target).to(dev)
+    _, lse = sao.token_logprob(hid, w, tgt)
+    dh, dw = sao.loss_backward(hid, w, tgt, lse, torch.from_numpy(g).to(dev))
+    torch.cuda.synchronize()
+    live = np.nonzero(g)[0]
+    rows = np.sort(np.concatenate([rng.choice(live[live.size * 9 // 10:], 20, replace=False),
+                                   rng.choice(live[:live.size * 9 // 10], 4, replace=False)]))
+    say(f"case dz-past-4gib: oracle on {rows.size} rows, compacted indices up to {int(np.searchsorted(live, rows[-1]))}")
+    ref_lp, ref_lse = oracle.token_logprob(b.hidden, b.w_head, b.target, rows=rows)
+    got_lse = lse.cpu().numpy()
+    assert np.abs(got_lse[rows] - ref_lse[rows]).max() <= TOL_LOGP
+    ref_dh, _ = oracle.loss_backward(b.hidden, b.w_head, b.target, ref_lse, g, dh_rows=rows, dw_rows=[])
+    got_dh = dh.float().cpu().numpy()
+    check_grad(got_dh[rows], ref_dh[rows], None, "dhidden rows past 4 GiB")
+    assert (got_dh[g == 0] == 0).all()
+    say("case dz-past-4gib: ok")
