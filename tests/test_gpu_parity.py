@@ -384,3 +384,49 @@ def test_backward_operand_past_4gib():
     check_grad(got_dh[rows], ref_dh[rows], None, "dhidden rows past 4 GiB")
     assert (got_dh[g == 0] == 0).all()
     say("case dz-past-4gib: ok")
+
+
+def _padded(x: np.ndarray, pad: int, dtype: str) -> torch.Tensor:
+    """The rows of x in a device buffer whose rows are `pad` elements longer (a strided view)."""
+    rows, cols = x.shape
+    if dtype == "bf16":
+        buf = torch.zeros(rows, cols + pad, dtype=torch.bfloat16)
+        buf[:, :cols] = torch.from_numpy(bf16_bits(x)).view(torch.bfloat16)
+    else:
+        buf = torch.zeros(rows, cols + pad, dtype=torch.float32)
+        buf[:, :cols] = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return buf.to("cuda")[:, :cols]
+
+
+@pytest.mark.parametrize("dtype,H,pad_h,pad_w", [("bf16", 192, 24, 40), ("f32", 96, 8, 32)])
+def test_padded_leading_dimensions(dtype, H, pad_h, pad_w):
+    # hidden and W_head rows with leading dimensions above H: the forward reads
+    # both K-major, the backward reads W MN-major and gathers hidden rows, and
+    # the critic reads hidden rows.
+    cfg = small_config(f"ld-{dtype}", 51, B=3, T=700, H=H, V=2000, dtype=dtype, value_head=True)
+    b = generate(cfg)
+    say(f"case ld-{dtype}: H={H} ld_hidden={H + pad_h} ld_w={H + pad_w}")
+    rng = np.random.default_rng(51)
+    g = np.where((b.mask == 1) & (rng.random(b.T) < 0.7), rng.standard_normal(b.T) / b.T, 0.0).astype(np.float32)
+    ref_lp, ref_lse = oracle.token_logprob(b.hidden, b.w_head, b.target, b.mask)
+    ref_dh, ref_dw = oracle.loss_backward(b.hidden, b.w_head, b.target, ref_lse, g)
+    ref_v = oracle.value_forward(b.hidden, b.w_value)
+    hid, w = _padded(b.hidden, pad_h, dtype), _padded(b.w_head, pad_w, dtype)
+    assert hid.stride(0) == H + pad_h and w.stride(0) == H + pad_w
+    tgt = torch.from_numpy(b.target).cuda()
+    mask = torch.from_numpy(b.mask).cuda()
+    logp, lse = sao.token_logprob(hid, w, tgt, mask)
+    all_lse = sao.token_logprob(hid, w, tgt)[1]
+    dh, dw = sao.loss_backward(hid, w, tgt, all_lse, torch.from_numpy(g).cuda())
+    wv = torch.from_numpy(bf16_bits(b.w_value)).view(torch.bfloat16) if dtype == "bf16" else \
+        torch.from_numpy(np.ascontiguousarray(b.w_value, dtype=np.float32))
+    v = sao.value_forward(hid, wv.cuda())
+    torch.cuda.synchronize()
+    m = b.mask == 1
+    assert np.abs(logp.cpu().numpy()[m] - ref_lp[m]).max() <= TOL_LOGP
+    assert np.abs(lse.cpu().numpy()[m] - ref_lse[m]).max() <= TOL_LOGP
+    check_grad(dh.float().cpu().numpy(), ref_dh, np.nonzero(g == 0)[0], "dhidden")
+    check_grad(dw.cpu().numpy(), ref_dw, None, "dw_head")
+    got_v = v.cpu().numpy()
+    assert (np.abs(got_v - ref_v) <= TOL_V * np.maximum(1.0, np.abs(ref_v))).all()
+    say(f"case ld-{dtype}: ok")
