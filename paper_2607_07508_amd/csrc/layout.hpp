@@ -8,7 +8,8 @@ namespace sao {
 
 constexpr int64_t kTile = 256;
 constexpr int64_t kRowsPerCountBlock = 1024;  // rows per block of the compaction count
-constexpr int64_t kVocabBlock = 16384;        // vocabulary rows per backward dZ block
+constexpr int64_t kVocabBlock = 16384;        // vocabulary rows per backward dZ block (at least)
+constexpr int64_t kVocabBlockMax = 65536;     // ... and at most
 constexpr int kLossThreads = 256;
 constexpr int kLossPerThread = 8;
 constexpr int kLossMaxBlocks = 2048;
@@ -65,11 +66,22 @@ inline int dh_pieces(int64_t T, int64_t H) {
   return static_cast<int>(p);
 }
 
+// Vocabulary rows per backward block: kVocabBlock, doubled up to kVocabBlockMax
+// while one block's dz product would have fewer than 8192 tiles (32 per CU) at
+// the host bound of token rows, so that short token chunks still give each
+// launch many rounds of tiles and take fewer launches.
+inline int64_t vocab_block(int64_t t_pad, int64_t V) {
+  int64_t vc = kVocabBlock;
+  while (vc < kVocabBlockMax && (t_pad / kTile) * (vc / kTile) < 8192) vc *= 2;
+  const int64_t v_all = round_up(V, kTile);
+  return vc < v_all ? vc : v_all;
+}
+
 inline BackwardLayout backward_layout(int64_t T, int64_t H, int64_t V, size_t esize) {
   BackwardLayout L{};
   L.t_pad = round_up(T, kTile);
   L.n_count_blocks = ceil_div(T, kRowsPerCountBlock);
-  L.vc = round_up(V, kTile) < kVocabBlock ? round_up(V, kTile) : kVocabBlock;
+  L.vc = vocab_block(L.t_pad, V);
   L.n_vblocks = ceil_div(V, L.vc);
   L.dh_pieces = dh_pieces(T, H);
   Carve c;

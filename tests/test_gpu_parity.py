@@ -49,7 +49,7 @@ def test_c0_as_bf16():
 @pytest.mark.parametrize("case", [
     dict(name="m1", seed=11, B=5, T=700, H=192, V=2000),            # 8 vocab tiles, ragged tails
     dict(name="m2", seed=12, B=3, T=300, H=64, V=1001),             # V not a multiple of 8
-    dict(name="m3", seed=13, B=4, T=640, H=64, V=40000),            # three backward vocab blocks
+    dict(name="m3", seed=13, B=4, T=640, H=64, V=140000),           # three backward vocab blocks
     dict(name="m4", seed=14, B=2, T=50, H=8, V=300),                # minimum H
     dict(name="m5", seed=15, B=6, T=1100, H=320, V=520, dtype="f32"),
 ])
