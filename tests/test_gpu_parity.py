@@ -148,6 +148,28 @@ def test_target_out_of_range_sets_status():
     assert np.abs(lp[ok] - ref[ok]).max() <= TOL_LOGP
 
 
+@pytest.mark.parametrize("bad", [np.nan, np.inf])
+def test_nonfinite_hidden_sets_status(bad):
+    # a non-finite hidden state makes its row's log-sum-exp non-finite: the row's
+    # log-prob is not finite, the status word gets the non-finite bit, and every
+    # other row is unaffected
+    b = generate(small_config("badh", 29, B=2, T=300, H=64, V=700, dtype="f32"))
+    t_bad = int(np.nonzero(b.mask)[0][5])
+    ref, _ = oracle.token_logprob(b.hidden, b.w_head, b.target, b.mask)
+    b.hidden[t_bad, 7] = bad
+    db = to_device(b)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    logp, lse = sao.token_logprob(db.hidden, db.w_head, db.target, db.mask, status=status)
+    torch.cuda.synchronize()
+    assert int(status) & sao.binding.STATUS_NONFINITE
+    assert not (int(status) & sao.binding.STATUS_TARGET_RANGE)
+    lp, ls = logp.cpu().numpy(), lse.cpu().numpy()
+    assert not np.isfinite(ls[t_bad]) and not np.isfinite(lp[t_bad])
+    ok = (b.mask == 1) & (np.arange(b.T) != t_bad)
+    assert np.isfinite(lp[ok]).all()
+    assert np.abs(lp[ok] - ref[ok]).max() <= TOL_LOGP
+
+
 def test_malformed_segments_set_status():
     b = generate(small_config("badcu", 28, B=3, T=120, H=8, V=16))
     db = to_device(b)
