@@ -96,7 +96,24 @@ def _dtype_code(t: torch.Tensor) -> int:
 def _rows(t: torch.Tensor, name: str) -> int:
     if t.dim() != 2 or t.stride(1) != 1:
         raise ValueError(f"{name} must be a row-major 2-D tensor with unit column stride")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
     return t.stride(0)
+
+
+def _vec(t: Optional[torch.Tensor], name: str, dtype: torch.dtype, n: int, device: torch.device,
+         optional: bool = False) -> None:
+    """A per-token array: on `device`, of `dtype`, contiguous, at least n elements."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, not {t.device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, not {t.dtype}")
+    if not t.is_contiguous() or t.numel() < n:
+        raise ValueError(f"{name} must be contiguous with at least {n} elements")
 
 
 def workspace_size(op: int, T: int, H: int, V: int, dtype: int) -> int:
@@ -109,6 +126,13 @@ def _workspace(nbytes: int, device) -> Optional[torch.Tensor]:
     return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
+def _head_shapes(hidden: torch.Tensor, w_head: torch.Tensor) -> None:
+    if hidden.dim() != 2 or w_head.dim() != 2 or w_head.shape[1] != hidden.shape[1]:
+        raise ValueError("hidden [T, H] and w_head [V, H] must share H")
+    if w_head.device != hidden.device:
+        raise ValueError("hidden and w_head must be on the same device")
+
+
 def token_logprob(hidden: torch.Tensor, w_head: torch.Tensor, target: torch.Tensor,
                   mask: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None,
                   out: Optional[Tuple[torch.Tensor, torch.Tensor]] = None):
@@ -119,8 +143,14 @@ def token_logprob(hidden: torch.Tensor, w_head: torch.Tensor, target: torch.Tens
     if _dtype_code(w_head) != dt:
         raise TypeError("hidden and w_head must share a dtype")
     dev = hidden.device
+    _head_shapes(hidden, w_head)
+    _vec(target, "target", torch.int32, T, dev)
+    _vec(mask, "mask", torch.uint8, T, dev, optional=True)
+    _vec(status, "status", torch.int32, 1, dev, optional=True)
     logp, lse = out if out is not None else (torch.empty(T, dtype=torch.float32, device=dev),
                                              torch.empty(T, dtype=torch.float32, device=dev))
+    _vec(logp, "logp", torch.float32, T, dev)
+    _vec(lse, "lse", torch.float32, T, dev)
     ws = _workspace(workspace_size(OP_LOGPROB, T, H, V, dt), dev)
     _check(lib().sao_token_logprob(
         _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_head), _rows(w_head, "w_head"), _ptr(target),
@@ -136,6 +166,11 @@ def advantage(values: torch.Tensor, rewards: torch.Tensor, mask: torch.Tensor, c
     T = values.shape[0]
     B = cu_seqlens.shape[0] - 1
     dev = values.device
+    _vec(values, "values", torch.float32, T, dev)
+    _vec(rewards, "rewards", torch.float32, T, dev)
+    _vec(mask, "mask", torch.uint8, T, dev)
+    _vec(cu_seqlens, "cu_seqlens", torch.int32, B + 1, dev)
+    _vec(status, "status", torch.int32, 1, dev, optional=True)
     adv = torch.empty(T, dtype=torch.float32, device=dev)
     ret = torch.empty(T, dtype=torch.float32, device=dev)
     n_tok = torch.empty(1, dtype=torch.int64, device=dev) if want_count else None
@@ -153,10 +188,17 @@ def clipped_loss(logp: torch.Tensor, logp_rollout: torch.Tensor, adv: torch.Tens
     """DIS loss: (loss[2] f64 +=, g, flags, counts[5] i64 +=). Zeroed accumulators are made if not given."""
     T = logp.shape[0]
     dev = logp.device
+    _vec(logp, "logp", torch.float32, T, dev)
+    _vec(logp_rollout, "logp_rollout", torch.float32, T, dev)
+    _vec(adv, "adv", torch.float32, T, dev)
+    _vec(mask, "mask", torch.uint8, T, dev)
+    _vec(n_tokens, "n_tokens", torch.int64, 1, dev, optional=True)
     if loss is None:
         loss = torch.zeros(2, dtype=torch.float64, device=dev)
     if counts is None:
         counts = torch.zeros(5, dtype=torch.int64, device=dev)
+    _vec(loss, "loss", torch.float64, 2, dev)
+    _vec(counts, "counts", torch.int64, 5, dev)
     g = torch.empty(T, dtype=torch.float32, device=dev)
     flags = torch.empty(T, dtype=torch.uint8, device=dev)
     ws = _workspace(workspace_size(OP_LOSS, T, 1, 1, SAO_F32), dev)
@@ -174,11 +216,19 @@ def loss_backward(hidden: torch.Tensor, w_head: torch.Tensor, target: torch.Tens
     T, H = hidden.shape
     V = w_head.shape[0]
     dt = _dtype_code(hidden)
+    if _dtype_code(w_head) != dt:
+        raise TypeError("hidden and w_head must share a dtype")
     dev = hidden.device
+    _head_shapes(hidden, w_head)
+    _vec(target, "target", torch.int32, T, dev)
+    _vec(lse, "lse", torch.float32, T, dev)
+    _vec(g, "g", torch.float32, T, dev)
     if dhidden is None:
         dhidden = torch.empty((T, H), dtype=hidden.dtype, device=dev)
     if dw_head is None:
         dw_head = torch.zeros((V, H), dtype=torch.float32, device=dev)
+    _vec(dhidden, "dhidden", hidden.dtype, T * H, dev)
+    _vec(dw_head, "dw_head", torch.float32, V * H, dev)
     ws = _workspace(workspace_size(OP_BACKWARD, T, H, V, dt), dev)
     _check(lib().sao_loss_backward(
         _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_head), _rows(w_head, "w_head"), _ptr(target),
@@ -191,8 +241,10 @@ def value_forward(hidden: torch.Tensor, w_value: torch.Tensor, v: Optional[torch
     """v [T] f32 = hidden . w_value (bias-free critic head)."""
     T, H = hidden.shape
     dev = hidden.device
+    _vec(w_value, "w_value", hidden.dtype, H, dev)
     if v is None:
         v = torch.empty(T, dtype=torch.float32, device=dev)
+    _vec(v, "v", torch.float32, T, dev)
     _check(lib().sao_value_forward(_ptr(hidden), _rows(hidden, "hidden"), _ptr(w_value), T, H,
                                    _dtype_code(hidden), _ptr(v), None, 0, _stream(dev)))
     return v
@@ -206,12 +258,20 @@ def value_loss(hidden: torch.Tensor, w_value: torch.Tensor, v: torch.Tensor, ret
     T, H = hidden.shape
     dt = _dtype_code(hidden)
     dev = hidden.device
+    _vec(w_value, "w_value", hidden.dtype, H, dev)
+    _vec(v, "v", torch.float32, T, dev)
+    _vec(ret, "ret", torch.float32, T, dev)
+    _vec(mask, "mask", torch.uint8, T, dev)
+    _vec(n_tokens, "n_tokens", torch.int64, 1, dev, optional=True)
     if loss is None:
         loss = torch.zeros(1, dtype=torch.float64, device=dev)
     if dw_value is None:
         dw_value = torch.zeros(H, dtype=torch.float32, device=dev)
     if dhidden is None:
         dhidden = torch.empty((T, H), dtype=hidden.dtype, device=dev)
+    _vec(loss, "loss", torch.float64, 1, dev)
+    _vec(dw_value, "dw_value", torch.float32, H, dev)
+    _vec(dhidden, "dhidden", hidden.dtype, T * H, dev)
     ws = _workspace(workspace_size(OP_VALUE, T, H, 1, dt), dev)
     _check(lib().sao_value_loss(
         _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_value), _ptr(v), _ptr(ret), _ptr(mask), T, H,
