@@ -210,11 +210,7 @@ __device__ __forceinline__ void wait_slabs_barrier(int pending) {
 // Instruction order is pinned where it matters: the compiler would otherwise
 // defer the LDS reads of the next K step behind the MFMAs of this one and then
 // wait for them, exposing the LDS latency once per step.
-__device__ __forceinline__ void pin_order() {
-#ifndef NO_PIN
-  __builtin_amdgcn_sched_barrier(0);
-#endif
-}
+__device__ __forceinline__ void pin_order() { __builtin_amdgcn_sched_barrier(0); }
 
 // Fragments of one K16 step (bf16; K8 for fp32): kMI rows of A, kNI rows of B.
 struct Frags {
