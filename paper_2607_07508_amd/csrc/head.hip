@@ -322,13 +322,6 @@ __device__ __forceinline__ void store4<F32>(float* p, const float (&d)[4]) {
 }
 
 
-template <class E>
-__device__ __forceinline__ typename E::storage to_storage(float x);
-template <>
-__device__ __forceinline__ uint16_t to_storage<BF16>(float x) { return f32_to_bf16(x); }
-template <>
-__device__ __forceinline__ float to_storage<F32>(float x) { return x; }
-
 // dz_{t,v} = g_t (1[v = y_t] - exp(z_{t,v} - lse_t)) for one vocabulary block, stored
 // token-major dz[c][v - v0] (row stride ldz). The dH product reads it K-major, the
 // dW product MN-major, so no transposed copy is written. Columns past the block's
