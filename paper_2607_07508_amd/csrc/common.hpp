@@ -8,7 +8,6 @@ namespace sao {
 
 constexpr int kWave = 64;
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
@@ -27,16 +26,9 @@ struct F32 {
   static constexpr int kPerChunk = 4;
 };
 
-__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
-  return __uint_as_float(static_cast<uint32_t>(b) << 16);
-}
-
-// Round to nearest even (gfx950's v_cvt_pk_bf16_f32); NaN stays NaN.
+// Two floats as packed bf16, rounded to nearest even (gfx950's
+// v_cvt_pk_bf16_f32; NaN stays NaN): `lo` in bits 0-15, `hi` in bits 16-31.
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
-}
-// Two floats as packed bf16: `lo` in bits 0-15, `hi` in bits 16-31.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const bf16x2_t v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
   return __builtin_bit_cast(uint32_t, v);
