@@ -16,7 +16,6 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, os.path.dirname(os.path.dirname(HERE)))
 
-from oracle import token_logprob  # noqa: E402
 from synth import CONFIGS, generate  # noqa: E402
 
 
@@ -42,6 +41,7 @@ def load(name: str, batch=None):
 
 
 def main(names):
+    from oracle import token_logprob  # only the writer runs the oracle; readers of the file do not
     for name in names:
         t0 = time.time()
         b = generate(CONFIGS[name])
