@@ -99,3 +99,28 @@ def test_global_token_count_and_empty():
     assert c2[0] == N                                   # counts report this call's tokens
     z = dis_loss(lp, lro, adv, np.zeros_like(b.mask), 0.2, 0.2)
     assert (z[0] == 0).all() and (z[1] == 0).all() and z[3].tolist() == [0, 0, 0, 0, 0]
+
+
+@pytest.mark.parametrize("eps_low,eps_high", [(0.3, 5.0), (0.8, 3.0), (0.2, 0.28)])
+def test_paper_band_pairs(eps_low, eps_high):
+    # The paper's two clip pairs (and the large-head workload's): log-ratios on a grid
+    # across both edges, kept 1e-4 away from them, give flags that follow the ratio
+    # alone; used tokens lie strictly inside (1 - eps_l, 1 + eps_h) and carry
+    # g = -rho A / N, every other token exactly 0.
+    lo = math.log(1.0 - float(np.float32(eps_low)))
+    hi = math.log(1.0 + float(np.float32(eps_high)))
+    d = np.linspace(lo - 1.5, hi + 1.0, 6001)
+    d = d[(np.abs(d - lo) > 1e-4) & (np.abs(d - hi) > 1e-4)]
+    lp = np.full(d.size, -2.0)
+    lro = lp - d
+    adv = np.linspace(-1.0, 1.0, d.size)
+    mask = np.ones(d.size, dtype=np.uint8)
+    _, g, flags, counts = dis_loss(lp, lro, adv, mask, eps_low, eps_high)
+    expect = np.where(d < lo, 2, np.where(d > hi, 3, 1))
+    assert np.array_equal(flags, expect)
+    rho = np.exp(d)
+    used = flags == 1
+    assert ((rho[used] > 1.0 - eps_low - 1e-7) & (rho[used] < 1.0 + eps_high + 1e-7)).all()
+    assert np.allclose(g[used], -rho[used] * adv[used] / d.size, rtol=1e-9, atol=0)
+    assert (g[~used] == 0).all()
+    assert counts.tolist() == [d.size, int(used.sum()), int((d < lo).sum()), int((d > hi).sum()), 0]
