@@ -146,3 +146,38 @@ def test_workspace_sizes(L):
     assert ws(binding.OP_LOSS, 1 << 26, 1, 1, 1) < 1 << 20
     # value loss: per-128-row partials of dw_v, far below the hidden states themselves
     assert 0 < ws(binding.OP_VALUE, 32768, 6144, 1, 0) < 32768 * 6144 * 2 // 16
+
+
+def test_error_message_is_per_thread(L):
+    # Two threads fail with different errors at the same time; each reads its own
+    # message (the library keeps the last message per calling thread).
+    import threading
+    barrier = threading.Barrier(2)
+    seen = {}
+
+    def null_case():
+        for _ in range(200):
+            barrier.wait()
+            code = L.sao_clipped_loss(None, FAKE, FAKE, FAKE, 16, 0.2, 0.2, None, FAKE, FAKE, FAKE, FAKE,
+                                      None, 0, None)
+            barrier.wait()
+            seen.setdefault("null", set()).add((code, L.sao_last_error_message()))
+
+    def value_case():
+        for _ in range(200):
+            barrier.wait()
+            code = L.sao_clipped_loss(FAKE, FAKE, FAKE, FAKE, 16, -1.0, 0.2, None, FAKE, FAKE, FAKE, FAKE,
+                                      None, 0, None)
+            barrier.wait()
+            seen.setdefault("value", set()).add((code, L.sao_last_error_message()))
+
+    threads = [threading.Thread(target=null_case), threading.Thread(target=value_case)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert len(seen["null"]) == 1 and len(seen["value"]) == 1
+    (code_n, msg_n), = seen["null"]
+    (code_v, msg_v), = seen["value"]
+    assert code_n == ERR_NULL and b"required" in msg_n
+    assert code_v == ERR_VALUE and b"eps" in msg_v

@@ -452,3 +452,29 @@ def test_padded_leading_dimensions(dtype, H, pad_h, pad_w):
     got_v = v.cpu().numpy()
     assert (np.abs(got_v - ref_v) <= TOL_V * np.maximum(1.0, np.abs(ref_v))).all()
     say(f"case ld-{dtype}: ok")
+
+
+def test_side_stream_matches_default_stream():
+    # Every launch goes on the caller's current stream: the same calls on a
+    # side stream (default priority) give bit-identical results.
+    b = generate(small_config("stream", 61, B=3, T=900, H=128, V=3000))
+    db = to_device(b)
+    rng = np.random.default_rng(61)
+    g = torch.from_numpy(np.where(b.mask == 1, rng.standard_normal(b.T) / b.T, 0.0).astype(np.float32)).cuda()
+
+    def run():
+        logp, lse = sao.token_logprob(db.hidden, db.w_head, db.target, db.mask)
+        all_lse = sao.token_logprob(db.hidden, db.w_head, db.target)[1]
+        dh, dw = sao.loss_backward(db.hidden, db.w_head, db.target, all_lse, g)
+        return logp, lse, dh, dw
+
+    ref = run()
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        got = run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for a, c in zip(ref, got):
+        assert torch.equal(a, c)
