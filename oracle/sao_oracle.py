@@ -20,6 +20,12 @@ paper states it:
   the head weights through the log-softmax.
 * ``value_forward`` / ``value_loss`` -- a bias-free H->1 critic head and the
   critic's squared-error loss against the returns (Sec. 2, PPO paragraph).
+* ``ppo_loss``       -- the comparison objectives the paper sets DIS against:
+  the clipped surrogate of Sec. 2 (symmetric, or clip-higher with
+  eps_high != eps_low) and the decoupled three-policy form of Sec. 3.1, where
+  pi_old / pi_rollout weighs the clipped term.
+* ``explained_variance`` -- EV = 1 - Var(R - V) / Var(R), the critic diagnostic
+  of Sec. 4.4, over the loss-mask tokens.
 
 Readings where the paper is silent (all listed in the design notes):
   gamma defaults to 1; ``l`` in lambda_policy is the trajectory's token length
@@ -29,7 +35,12 @@ Readings where the paper is silent (all listed in the design notes):
   N = number of loss-mask tokens (clipped ones included); f(r) is a
   stop-gradient weight; the library minimises -L; band edges are strict as in
   Eq. 3 (equality is clipped); a NaN ratio is flagged non-finite and
-  contributes exactly 0.
+  contributes exactly 0. For the comparison objectives: the same token mean
+  and N as DIS; a token is clipped exactly when A > 0 and r > 1 + eps_high or
+  A < 0 and r < 1 - eps_low (strict, as Sec. 3.1 states standard clipping);
+  the pi_old / pi_rollout weight is a stop-gradient constant and is not
+  truncated; EV uses population variances over loss-mask tokens and is NaN
+  when there are none or Var(R) = 0.
 
 Large inputs are processed in blocks of rows only to bound memory: rows are
 independent in every definition here, so the blocking changes no arithmetic.
@@ -303,3 +314,71 @@ def value_loss(hidden, w_value, v, ret, mask, n_tokens: Optional[int] = None):
     dH = dv[:, None] * _f64(w_value)[None, :]
     dw = _f64(hidden).T @ dv
     return L, dH, dw
+
+
+# --------------------------------------------------------------------------- #
+# Comparison objectives: the clipped surrogate of Sec. 2 and decoupled PPO.
+# --------------------------------------------------------------------------- #
+def ppo_loss(logp, logp_old, adv, mask, eps_low, eps_high, n_tokens: Optional[int] = None,
+             logp_behav=None):
+    """Clipped-surrogate loss, its gradient w.r.t. log pi, per-token flags and counts.
+
+    The unified objective of Sec. 2 with separate lower and upper clip widths
+    (eps_low == eps_high is standard PPO, eps_high > eps_low is clip-higher),
+    as a token mean with the same N as the DIS loss. For each loss-mask token:
+        r_t   = exp(log pi_t - log pi_old_t)          (the Sec. 2 ratio)
+        w_t   = exp(log pi_old_t - log pi_behav_t)     (decoupled form of Sec. 3.1; 1 without behav)
+        flag  = 4 if r or w is NaN;
+                3 if A_t > 0 and r_t > 1 + eps_high;  2 if A_t < 0 and r_t < 1 - eps_low;  else 1
+        term  = w_t * min(r_t A_t, clip(r_t, 1 - eps_low, 1 + eps_high) A_t)
+    The min picks the clipped product exactly on flags 2 and 3, where the term
+    is a constant in log pi. Then
+        loss  = -(1/N) sum_t term_t      (minus the objective; flag-4 tokens add 0)
+        g_t   = -[flag 1] w_t r_t A_t / N
+    counts = [sum(mask), unclipped, clipped-low, clipped-high, non-finite].
+    """
+    lp, lold, A = _f64(logp), _f64(logp_old), _f64(adv)
+    m = np.asarray(mask) != 0
+    lo_edge = 1.0 - float(np.float32(eps_low))
+    hi_edge = 1.0 + float(np.float32(eps_high))
+    N = int(m.sum()) if n_tokens is None else int(n_tokens)
+    with np.errstate(over="ignore", invalid="ignore"):
+        r = np.exp(lp - lold)
+        w = np.ones_like(r) if logp_behav is None else np.exp(lold - _f64(logp_behav))
+    bad = np.isnan(r) | np.isnan(w)
+    flags = np.where(bad, FLAG_NONFINITE,
+             np.where((A > 0) & (r > hi_edge), FLAG_HIGH,
+              np.where((A < 0) & (r < lo_edge), FLAG_LOW, FLAG_USED)))
+    flags = np.where(m, flags, FLAG_MASKED).astype(np.uint8)
+    g = np.zeros(lp.shape[0], dtype=np.float64)
+    loss = 0.0
+    if N > 0:
+        terms = []
+        for t in np.nonzero(m & ~bad)[0]:
+            lo_term, hi_term = r[t] * A[t], min(max(r[t], lo_edge), hi_edge) * A[t]
+            terms.append(w[t] * min(lo_term, hi_term))
+        loss = -math.fsum(terms) / N
+        used = flags == FLAG_USED
+        g[used] = -w[used] * r[used] * A[used] / N
+    counts = np.array([int(m.sum()), int((flags == FLAG_USED).sum()), int((flags == FLAG_LOW).sum()),
+                       int((flags == FLAG_HIGH).sum()), int((flags == FLAG_NONFINITE).sum())],
+                      dtype=np.int64)
+    return loss, g, flags, counts
+
+
+# --------------------------------------------------------------------------- #
+# Sec. 4.4: explained variance of the critic against the returns.
+# --------------------------------------------------------------------------- #
+def explained_variance(values, ret, mask):
+    """EV = 1 - Var(R - V) / Var(R) over the loss-mask tokens (population variances).
+
+    NaN when no token has mask 1 or when Var(R) is 0.
+    """
+    m = np.asarray(mask) != 0
+    R, V = _f64(ret)[m], _f64(values)[m]
+    if R.size == 0:
+        return math.nan
+    var_r = float(np.mean((R - R.mean()) ** 2))
+    d = R - V
+    var_d = float(np.mean((d - d.mean()) ** 2))
+    return math.nan if var_r == 0.0 else 1.0 - var_d / var_r
