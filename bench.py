@@ -105,11 +105,14 @@ def vendor_gemm(db, t_act: int, torch, reps: int = 3):
 
 
 def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
-    """Achieved HBM bandwidth of the scan (sao_advantage) and the loss epilogue
-    (sao_clipped_loss) at T = 2^e tokens, B = T/4096 trajectories, c2's span mix.
-    Algorithmic bytes: 17 per token for the scan (values, rewards, mask in; adv,
-    ret out), 18 for the loss (logp, logp_rollout, adv, mask in; g, flags out).
-    One JSON line per size."""
+    """Achieved HBM bandwidth of the scan (sao_advantage), the loss epilogue
+    (sao_clipped_loss), the decoupled clipped surrogate (sao_ppo_loss with
+    logp_behav) and the explained variance (sao_explained_variance) at T = 2^e
+    tokens, B = T/4096 trajectories, c2's span mix. Algorithmic bytes per token:
+    17 for the scan (values, rewards, mask in; adv, ret out), 18 for the loss
+    (logp, logp_rollout, adv, mask in; g, flags out), 22 for the surrogate
+    (logp, logp_old, logp_behav, adv, mask in; g, flags out), 9 for the
+    explained variance (values, ret, mask in). One JSON line per size."""
     import torch
     import paper_2607_07508_amd as sao
     from paper_2607_07508_amd import binding as B
@@ -145,6 +148,7 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
         g = torch.Generator(device="cpu").manual_seed(e)
         logp = (-torch.rand(T, generator=g) * 4.0).to("cuda")
         lro = logp + torch.from_numpy(b.xi).float().to("cuda")
+        lbh = lro + 0.05 * torch.randn(T, generator=g).to("cuda")
         L = sao.lib()
         f32 = dict(dtype=torch.float32, device="cuda")
         adv, ret, g_out = torch.empty(T, **f32), torch.empty(T, **f32), torch.empty(T, **f32)
@@ -152,8 +156,10 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
         n = torch.zeros(1, dtype=torch.int64, device="cuda")
         loss = torch.zeros(2, dtype=torch.float64, device="cuda")
         counts = torch.zeros(5, dtype=torch.int64, device="cuda")
-        ws_bytes = max(B.workspace_size(B.OP_ADVANTAGE, T, 1, 1, B.SAO_F32),
-                       B.workspace_size(B.OP_LOSS, T, 1, 1, B.SAO_F32))
+        moments = torch.zeros(5, dtype=torch.float64, device="cuda")
+        ev = torch.zeros(1, dtype=torch.float64, device="cuda")
+        ws_bytes = max(B.workspace_size(op, T, 1, 1, B.SAO_F32)
+                       for op in (B.OP_ADVANTAGE, B.OP_LOSS, B.OP_PPO_LOSS, B.OP_EXPLAINED_VARIANCE))
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
         st = torch.cuda.current_stream().cuda_stream
         p = lambda t: t.data_ptr()  # noqa: E731
@@ -165,8 +171,16 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
         def epilogue():
             B._check(L.sao_clipped_loss(p(logp), p(lro), p(adv), p(db.mask), T, 0.2, 0.2, p(n), p(loss), p(g_out),
                                         p(flags), p(counts), p(ws), ws_bytes, st))
+        def surrogate():
+            B._check(L.sao_ppo_loss(p(logp), p(lro), p(lbh), p(adv), p(db.mask), T, 0.2, 0.28, p(n), p(loss),
+                                    p(g_out), p(flags), p(counts), p(ws), ws_bytes, st))
+
+        def explained():
+            B._check(L.sao_explained_variance(p(db.values), p(ret), p(db.mask), T, p(moments), p(ev), p(ws), ws_bytes,
+                                              st))
         out = {}
-        for name, fn, nbytes in (("advantage", scan, 17 * T), ("clipped_loss", epilogue, 18 * T)):
+        for name, fn, nbytes in (("advantage", scan, 17 * T), ("clipped_loss", epilogue, 18 * T),
+                                 ("ppo_loss", surrogate, 22 * T), ("explained_variance", explained, 9 * T)):
             for _ in range(3):
                 fn()
             torch.cuda.synchronize()
@@ -180,7 +194,7 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
             out[name] = {"ms": ms, "GB/s": nbytes / ms / 1e6, "frac_hbm": nbytes / ms / 1e6 / PEAK_HBM_GBS,
                          "bytes": nbytes}
         print(json.dumps({"mode": "epilogue_sweep", "T": T, "B": cfg.B, **out}), flush=True)
-        del db, b, logp, lro, adv, ret, g_out, flags, ws
+        del db, b, logp, lro, lbh, adv, ret, g_out, flags, ws
         torch.cuda.empty_cache()
 
 

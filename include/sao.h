@@ -78,7 +78,9 @@ typedef enum {
   SAO_OP_ADVANTAGE = 1,
   SAO_OP_LOSS = 2,
   SAO_OP_BACKWARD = 3,
-  SAO_OP_VALUE = 4
+  SAO_OP_VALUE = 4,
+  SAO_OP_PPO_LOSS = 5,
+  SAO_OP_EXPLAINED_VARIANCE = 6
 } sao_op_t;
 
 /* Bits of the optional device status word. */
@@ -86,7 +88,7 @@ typedef enum {
 #define SAO_STATUS_SEGMENTS     2  /* cu_seqlens is not non-decreasing from 0 to T    */
 #define SAO_STATUS_NONFINITE    4  /* a log-sum-exp came out NaN or infinite          */
 
-/* Per-token flags written by sao_clipped_loss. */
+/* Per-token flags written by sao_clipped_loss (sao_ppo_loss: see there). */
 #define SAO_FLAG_MASKED    0  /* mask == 0                                       */
 #define SAO_FLAG_USED      1  /* 1 - eps_low < rho < 1 + eps_high                 */
 #define SAO_FLAG_LOW       2  /* rho <= 1 - eps_low                               */
@@ -164,6 +166,47 @@ sao_status_t sao_clipped_loss(const float* logp, const float* logp_rollout, cons
                               const uint8_t* mask, int64_t T, float eps_low, float eps_high,
                               const int64_t* n_tokens, double* loss, float* g, uint8_t* flags,
                               int64_t* counts, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * The clipped surrogate the paper compares DIS with: the unified objective of
+ * Sec. 2 with separate clip widths (eps_low == eps_high is standard PPO,
+ * eps_high > eps_low is clip-higher) and, when logp_behav is given, the
+ * decoupled three-policy form of Sec. 3.1. For each token with mask 1 (in float64):
+ *   r_t  = exp(logp[t] - logp_old[t])
+ *   w_t  = exp(logp_old[t] - logp_behav[t])          (1 when logp_behav is NULL;
+ *                                                     a constant, not truncated)
+ *   flag = NONFINITE if r or w is NaN; HIGH if adv > 0 and r > 1+eps_high;
+ *          LOW if adv < 0 and r < 1-eps_low; else USED (unclipped)
+ *   loss[0] += -(1/N) sum_t w_t min(r_t adv_t, clip(r_t, 1-eps_low, 1+eps_high) adv_t)
+ *              over tokens that are not NONFINITE
+ *   g[t]     = -[USED] w_t r_t adv_t / N     (d loss / d logp[t]; overwritten)
+ * Strict comparisons: at r = 1+eps_high or 1-eps_low the two products agree and
+ * the gradient flows. N, flags[T] (overwritten), counts[5] (+=: {sum(mask), USED,
+ * LOW, HIGH, NONFINITE}, so (LOW + HIGH) / N is the clip ratio) and the
+ * workspace follow sao_clipped_loss; loss[1] is float64 (+=). logp_behav is
+ * nullable; every other array is required. Reductions are deterministic.
+ */
+sao_status_t sao_ppo_loss(const float* logp, const float* logp_old, const float* logp_behav,
+                          const float* adv, const uint8_t* mask, int64_t T, float eps_low,
+                          float eps_high, const int64_t* n_tokens, double* loss, float* g,
+                          uint8_t* flags, int64_t* counts, void* ws, size_t ws_bytes,
+                          hipStream_t stream);
+
+/*
+ * Explained variance of the critic, Sec. 4.4, over tokens with mask 1:
+ *   EV = 1 - Var(R - V) / Var(R)        (R = ret of sao_advantage, V = values)
+ * moments[5] (device float64, in/out) is a running state {n, mean of R,
+ * sum of squared deviations of R, mean of R - V, sum of squared deviations of
+ * R - V}; this call's tokens are combined into it, so chunked calls cover the
+ * whole batch (zero it before the first). ev (nullable, device float64,
+ * overwritten) = 1 - moments[4] / moments[2] after the combination, NaN when
+ * n == 0 or Var(R) == 0. Arithmetic is float64; the combination runs in a fixed
+ * order. ws: sao_workspace_size(SAO_OP_EXPLAINED_VARIANCE, T, 1, 1, SAO_F32) bytes.
+ * T == 0 leaves moments and ev untouched.
+ */
+sao_status_t sao_explained_variance(const float* values, const float* ret, const uint8_t* mask,
+                                    int64_t T, double* moments, double* ev, void* ws,
+                                    size_t ws_bytes, hipStream_t stream);
 
 /*
  * Backward of the DIS loss through the log-softmax of Eq. (1)-(2):

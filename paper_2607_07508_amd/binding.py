@@ -16,13 +16,14 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsao.so")
 
 SAO_BF16, SAO_F32 = 0, 1
-OP_LOGPROB, OP_ADVANTAGE, OP_LOSS, OP_BACKWARD, OP_VALUE = 0, 1, 2, 3, 4
+OP_LOGPROB, OP_ADVANTAGE, OP_LOSS, OP_BACKWARD, OP_VALUE, OP_PPO_LOSS, OP_EXPLAINED_VARIANCE = range(7)
 STATUS_TARGET_RANGE, STATUS_SEGMENTS, STATUS_NONFINITE = 1, 2, 4
 FLAG_MASKED, FLAG_USED, FLAG_LOW, FLAG_HIGH, FLAG_NONFINITE = 0, 1, 2, 3, 4
 
 EXPORTS = ("sao_status_string", "sao_last_error_message", "sao_version", "sao_workspace_size",
            "sao_token_logprob", "sao_advantage", "sao_clipped_loss", "sao_loss_backward",
-           "sao_value_forward", "sao_value_loss", "sao_debug_time_kernel")
+           "sao_value_forward", "sao_value_loss", "sao_ppo_loss", "sao_explained_variance",
+           "sao_debug_time_kernel")
 KERNEL_NONE, KERNEL_HEAD_FORWARD = 0, 1
 
 
@@ -51,6 +52,9 @@ _SIGS = {
     "sao_value_forward": (ctypes.c_int, [_p, _i64, _p, _i64, _i64, ctypes.c_int, _p, _p, ctypes.c_size_t, _p]),
     "sao_value_loss": (ctypes.c_int, [_p, _i64, _p, _p, _p, _p, _i64, _i64, _p, ctypes.c_int, _p, _p, _p, _p,
                                       ctypes.c_size_t, _p]),
+    "sao_ppo_loss": (ctypes.c_int, [_p, _p, _p, _p, _p, _i64, ctypes.c_float, ctypes.c_float, _p, _p, _p, _p,
+                                    _p, _p, ctypes.c_size_t, _p]),
+    "sao_explained_variance": (ctypes.c_int, [_p, _p, _p, _i64, _p, _p, _p, ctypes.c_size_t, _p]),
     "sao_debug_time_kernel": (None, [ctypes.c_int, _p, _p]),
 }
 
@@ -152,10 +156,11 @@ def token_logprob(hidden: torch.Tensor, w_head: torch.Tensor, target: torch.Tens
     _vec(logp, "logp", torch.float32, T, dev)
     _vec(lse, "lse", torch.float32, T, dev)
     ws = _workspace(workspace_size(OP_LOGPROB, T, H, V, dt), dev)
-    _check(lib().sao_token_logprob(
-        _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_head), _rows(w_head, "w_head"), _ptr(target),
-        _ptr(mask), T, H, V, dt, _ptr(logp), _ptr(lse), _ptr(status), _ptr(ws),
-        0 if ws is None else ws.numel(), _stream(dev)))
+    if T:  # T == 0 is a no-op: empty tensors carry null pointers
+        _check(lib().sao_token_logprob(
+            _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_head), _rows(w_head, "w_head"), _ptr(target),
+            _ptr(mask), T, H, V, dt, _ptr(logp), _ptr(lse), _ptr(status), _ptr(ws),
+            0 if ws is None else ws.numel(), _stream(dev)))
     return logp, lse
 
 
@@ -173,12 +178,13 @@ def advantage(values: torch.Tensor, rewards: torch.Tensor, mask: torch.Tensor, c
     _vec(status, "status", torch.int32, 1, dev, optional=True)
     adv = torch.empty(T, dtype=torch.float32, device=dev)
     ret = torch.empty(T, dtype=torch.float32, device=dev)
-    n_tok = torch.empty(1, dtype=torch.int64, device=dev) if want_count else None
+    n_tok = torch.zeros(1, dtype=torch.int64, device=dev) if want_count else None
     ws = _workspace(workspace_size(OP_ADVANTAGE, T, 1, 1, SAO_F32), dev)
-    _check(lib().sao_advantage(
-        _ptr(values), _ptr(rewards), _ptr(mask), _ptr(cu_seqlens), B, T, float(gamma), float(lam),
-        float(alpha), _ptr(adv), _ptr(ret), _ptr(n_tok), _ptr(status), _ptr(ws),
-        0 if ws is None else ws.numel(), _stream(dev)))
+    if T:  # T == 0 is a no-op: empty tensors carry null pointers
+        _check(lib().sao_advantage(
+            _ptr(values), _ptr(rewards), _ptr(mask), _ptr(cu_seqlens), B, T, float(gamma), float(lam),
+            float(alpha), _ptr(adv), _ptr(ret), _ptr(n_tok), _ptr(status), _ptr(ws),
+            0 if ws is None else ws.numel(), _stream(dev)))
     return adv, ret, n_tok
 
 
@@ -202,11 +208,64 @@ def clipped_loss(logp: torch.Tensor, logp_rollout: torch.Tensor, adv: torch.Tens
     g = torch.empty(T, dtype=torch.float32, device=dev)
     flags = torch.empty(T, dtype=torch.uint8, device=dev)
     ws = _workspace(workspace_size(OP_LOSS, T, 1, 1, SAO_F32), dev)
-    _check(lib().sao_clipped_loss(
-        _ptr(logp), _ptr(logp_rollout), _ptr(adv), _ptr(mask), T, float(eps_low), float(eps_high),
-        _ptr(n_tokens), _ptr(loss), _ptr(g), _ptr(flags), _ptr(counts), _ptr(ws),
-        0 if ws is None else ws.numel(), _stream(dev)))
+    if T:  # T == 0 is a no-op: empty tensors carry null pointers
+        _check(lib().sao_clipped_loss(
+            _ptr(logp), _ptr(logp_rollout), _ptr(adv), _ptr(mask), T, float(eps_low), float(eps_high),
+            _ptr(n_tokens), _ptr(loss), _ptr(g), _ptr(flags), _ptr(counts), _ptr(ws),
+            0 if ws is None else ws.numel(), _stream(dev)))
     return loss, g, flags, counts
+
+
+def ppo_loss(logp: torch.Tensor, logp_old: torch.Tensor, adv: torch.Tensor, mask: torch.Tensor,
+             eps_low: float, eps_high: float, n_tokens: Optional[torch.Tensor] = None,
+             logp_behav: Optional[torch.Tensor] = None, loss: Optional[torch.Tensor] = None,
+             counts: Optional[torch.Tensor] = None):
+    """Clipped surrogate (standard, clip-higher, or decoupled with logp_behav):
+    (loss[1] f64 +=, g, flags, counts[5] i64 +=). Zeroed accumulators are made if not given."""
+    T = logp.shape[0]
+    dev = logp.device
+    _vec(logp, "logp", torch.float32, T, dev)
+    _vec(logp_old, "logp_old", torch.float32, T, dev)
+    _vec(logp_behav, "logp_behav", torch.float32, T, dev, optional=True)
+    _vec(adv, "adv", torch.float32, T, dev)
+    _vec(mask, "mask", torch.uint8, T, dev)
+    _vec(n_tokens, "n_tokens", torch.int64, 1, dev, optional=True)
+    if loss is None:
+        loss = torch.zeros(1, dtype=torch.float64, device=dev)
+    if counts is None:
+        counts = torch.zeros(5, dtype=torch.int64, device=dev)
+    _vec(loss, "loss", torch.float64, 1, dev)
+    _vec(counts, "counts", torch.int64, 5, dev)
+    g = torch.empty(T, dtype=torch.float32, device=dev)
+    flags = torch.empty(T, dtype=torch.uint8, device=dev)
+    ws = _workspace(workspace_size(OP_PPO_LOSS, T, 1, 1, SAO_F32), dev)
+    if T:  # T == 0 is a no-op: empty tensors carry null pointers
+        _check(lib().sao_ppo_loss(
+            _ptr(logp), _ptr(logp_old), _ptr(logp_behav), _ptr(adv), _ptr(mask), T, float(eps_low), float(eps_high),
+            _ptr(n_tokens), _ptr(loss), _ptr(g), _ptr(flags), _ptr(counts), _ptr(ws),
+            0 if ws is None else ws.numel(), _stream(dev)))
+    return loss, g, flags, counts
+
+
+def explained_variance(values: torch.Tensor, ret: torch.Tensor, mask: torch.Tensor,
+                       moments: Optional[torch.Tensor] = None):
+    """(ev [1] f64, moments [5] f64): EV = 1 - Var(R - V) / Var(R) over mask tokens, with this
+    call's tokens combined into `moments` (zeroed if not given) so chunked calls cover a batch."""
+    T = values.shape[0]
+    dev = values.device
+    _vec(values, "values", torch.float32, T, dev)
+    _vec(ret, "ret", torch.float32, T, dev)
+    _vec(mask, "mask", torch.uint8, T, dev)
+    if moments is None:
+        moments = torch.zeros(5, dtype=torch.float64, device=dev)
+    _vec(moments, "moments", torch.float64, 5, dev)
+    ev = torch.full((1,), float("nan"), dtype=torch.float64, device=dev)
+    ws = _workspace(workspace_size(OP_EXPLAINED_VARIANCE, T, 1, 1, SAO_F32), dev)
+    if T:  # T == 0 is a no-op: empty tensors carry null pointers
+        _check(lib().sao_explained_variance(
+            _ptr(values), _ptr(ret), _ptr(mask), T, _ptr(moments), _ptr(ev), _ptr(ws),
+            0 if ws is None else ws.numel(), _stream(dev)))
+    return ev, moments
 
 
 def loss_backward(hidden: torch.Tensor, w_head: torch.Tensor, target: torch.Tensor, lse: torch.Tensor,
@@ -230,10 +289,11 @@ def loss_backward(hidden: torch.Tensor, w_head: torch.Tensor, target: torch.Tens
     _vec(dhidden, "dhidden", hidden.dtype, T * H, dev)
     _vec(dw_head, "dw_head", torch.float32, V * H, dev)
     ws = _workspace(workspace_size(OP_BACKWARD, T, H, V, dt), dev)
-    _check(lib().sao_loss_backward(
-        _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_head), _rows(w_head, "w_head"), _ptr(target),
-        _ptr(lse), _ptr(g), T, H, V, dt, _ptr(dhidden), _ptr(dw_head), _ptr(ws),
-        0 if ws is None else ws.numel(), _stream(dev)))
+    if T:  # T == 0 is a no-op: empty tensors carry null pointers
+        _check(lib().sao_loss_backward(
+            _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_head), _rows(w_head, "w_head"), _ptr(target),
+            _ptr(lse), _ptr(g), T, H, V, dt, _ptr(dhidden), _ptr(dw_head), _ptr(ws),
+            0 if ws is None else ws.numel(), _stream(dev)))
     return dhidden, dw_head
 
 
@@ -245,8 +305,9 @@ def value_forward(hidden: torch.Tensor, w_value: torch.Tensor, v: Optional[torch
     if v is None:
         v = torch.empty(T, dtype=torch.float32, device=dev)
     _vec(v, "v", torch.float32, T, dev)
-    _check(lib().sao_value_forward(_ptr(hidden), _rows(hidden, "hidden"), _ptr(w_value), T, H,
-                                   _dtype_code(hidden), _ptr(v), None, 0, _stream(dev)))
+    if T:  # T == 0 is a no-op: empty tensors carry null pointers
+        _check(lib().sao_value_forward(_ptr(hidden), _rows(hidden, "hidden"), _ptr(w_value), T, H,
+                                       _dtype_code(hidden), _ptr(v), None, 0, _stream(dev)))
     return v
 
 
@@ -273,10 +334,11 @@ def value_loss(hidden: torch.Tensor, w_value: torch.Tensor, v: torch.Tensor, ret
     _vec(dw_value, "dw_value", torch.float32, H, dev)
     _vec(dhidden, "dhidden", hidden.dtype, T * H, dev)
     ws = _workspace(workspace_size(OP_VALUE, T, H, 1, dt), dev)
-    _check(lib().sao_value_loss(
-        _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_value), _ptr(v), _ptr(ret), _ptr(mask), T, H,
-        _ptr(n_tokens), dt, _ptr(loss), _ptr(dhidden), _ptr(dw_value), _ptr(ws),
-        0 if ws is None else ws.numel(), _stream(dev)))
+    if T:  # T == 0 is a no-op: empty tensors carry null pointers
+        _check(lib().sao_value_loss(
+            _ptr(hidden), _rows(hidden, "hidden"), _ptr(w_value), _ptr(v), _ptr(ret), _ptr(mask), T, H,
+            _ptr(n_tokens), dt, _ptr(loss), _ptr(dhidden), _ptr(dw_value), _ptr(ws),
+            0 if ws is None else ws.numel(), _stream(dev)))
     return loss, dhidden, dw_value
 
 

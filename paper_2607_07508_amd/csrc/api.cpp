@@ -113,6 +113,10 @@ size_t sao_workspace_size(sao_op_t op, int64_t T, int64_t H, int64_t V, sao_dtyp
     case SAO_OP_VALUE:
       if (H < 1) return 0;
       return sao::value_layout(T, H).total;
+    case SAO_OP_PPO_LOSS:
+      return sao::loss_layout(T).total;
+    case SAO_OP_EXPLAINED_VARIANCE:
+      return sao::ev_layout(T).total;
   }
   return 0;
 }
@@ -163,6 +167,33 @@ sao_status_t sao_clipped_loss(const float* logp, const float* logp_rollout, cons
   return device(sao::launch_loss(logp, logp_rollout, adv, mask, T, eps_low, eps_high, n_tokens, loss, g, flags,
                                  counts, ws, stream),
                 "sao_clipped_loss launch");
+}
+
+sao_status_t sao_ppo_loss(const float* logp, const float* logp_old, const float* logp_behav, const float* adv,
+                          const uint8_t* mask, int64_t T, float eps_low, float eps_high, const int64_t* n_tokens,
+                          double* loss, float* g, uint8_t* flags, int64_t* counts, void* ws, size_t ws_bytes,
+                          hipStream_t stream) {
+  if (!logp || !logp_old || !adv || !mask || !loss || !g || !flags || !counts)
+    return fail(SAO_ERR_NULL, "logp, logp_old, adv, mask, loss, g, flags and counts are required");
+  if (T < 0 || T > kMaxRows) return fail(SAO_ERR_SHAPE, "T=%lld out of range", (long long)T);
+  if (!(eps_low >= 0.0f) || !std::isfinite(eps_low) || !(eps_high >= 0.0f) || !std::isfinite(eps_high))
+    return fail(SAO_ERR_VALUE, "eps_low=%g, eps_high=%g must be finite and >= 0", eps_low, eps_high);
+  if (T == 0) return ok();
+  if (sao_status_t s = check_ws(ws, ws_bytes, sao_workspace_size(SAO_OP_PPO_LOSS, T, 1, 1, SAO_F32))) return s;
+  return device(sao::launch_ppo_loss(logp, logp_old, logp_behav, adv, mask, T, eps_low, eps_high, n_tokens, loss,
+                                     g, flags, counts, ws, stream),
+                "sao_ppo_loss launch");
+}
+
+sao_status_t sao_explained_variance(const float* values, const float* ret, const uint8_t* mask, int64_t T,
+                                    double* moments, double* ev, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!values || !ret || !mask || !moments) return fail(SAO_ERR_NULL, "values, ret, mask and moments are required");
+  if (T < 0 || T > kMaxRows) return fail(SAO_ERR_SHAPE, "T=%lld out of range", (long long)T);
+  if (T == 0) return ok();
+  if (sao_status_t s = check_ws(ws, ws_bytes, sao_workspace_size(SAO_OP_EXPLAINED_VARIANCE, T, 1, 1, SAO_F32)))
+    return s;
+  return device(sao::launch_explained_variance(values, ret, mask, T, moments, ev, ws, stream),
+                "sao_explained_variance launch");
 }
 
 sao_status_t sao_loss_backward(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,

@@ -23,6 +23,13 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const float
                        int64_t T, float eps_low, float eps_high, const int64_t* n_tokens, double* loss,
                        float* g, uint8_t* flags, int64_t* counts, void* ws, hipStream_t st);
 
+hipError_t launch_ppo_loss(const float* logp, const float* logp_old, const float* logp_behav, const float* adv,
+                           const uint8_t* mask, int64_t T, float eps_low, float eps_high, const int64_t* n_tokens,
+                           double* loss, float* g, uint8_t* flags, int64_t* counts, void* ws, hipStream_t st);
+
+hipError_t launch_explained_variance(const float* values, const float* ret, const uint8_t* mask, int64_t T,
+                                     double* moments, double* ev, void* ws, hipStream_t st);
+
 hipError_t launch_value_forward(const void* hidden, int64_t ld_hidden, const void* w_v, int64_t T, int64_t H,
                                 bool bf16, float* v, hipStream_t st);
 

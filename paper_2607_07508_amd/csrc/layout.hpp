@@ -123,6 +123,23 @@ inline LossLayout loss_layout(int64_t T) {
   return L;
 }
 
+// sao_ppo_loss shares the loss layout.
+
+// sao_explained_variance: five doubles per block
+struct EvLayout {
+  int64_t blocks;
+  size_t part, total;
+};
+
+inline EvLayout ev_layout(int64_t T) {
+  EvLayout L{};
+  L.blocks = loss_layout(T).blocks;
+  Carve c;
+  L.part = c.take(40 * static_cast<size_t>(L.blocks));
+  L.total = c.off;
+  return L;
+}
+
 // sao_value_loss (sao_value_forward needs none)
 constexpr int kValueThreads = 256;
 constexpr int64_t kValueRows = 128;           // rows per block of the value-loss pass

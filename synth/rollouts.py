@@ -282,5 +282,17 @@ def rollout_logprobs(reference_logp: np.ndarray, xi: np.ndarray) -> np.ndarray:
     return (np.asarray(reference_logp, dtype=np.float64) + xi).astype(np.float32)
 
 
+def comparison_logprobs(cfg: Config, T: int, behav_sigma: float = 0.05):
+    """Per-token log-probs for the comparison objectives, all float32 [T]:
+    the current policy's (exponentially spread below 0), the old policy's (the
+    current ones plus guard-banded drift noise, so every log-ratio stays clear of
+    the clip edges of cfg) and the rollout engine's (the old ones plus small noise)."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([cfg.seed, 7919])))
+    lp = (-rng.exponential(1.0, T)).astype(np.float32)
+    lold = rollout_logprobs(lp, _guard_banded_noise(cfg, T, rng))
+    lb = (lold.astype(np.float64) + rng.normal(0.0, behav_sigma, T)).astype(np.float32)
+    return lp, lold, lb
+
+
 def with_overrides(cfg: Config, **kw) -> Config:
     return replace(cfg, **kw)

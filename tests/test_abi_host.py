@@ -97,6 +97,33 @@ def test_loss_validation(L):
     assert loss(T=0) == OK
 
 
+def test_ppo_loss_validation(L):
+    def ppo(lold=FAKE, behav=None, T=10, el=0.2, eh=0.28, counts=FAKE, ws=FAKE, ws_bytes=1 << 30):
+        return L.sao_ppo_loss(FAKE, lold, behav, FAKE, FAKE, T, el, eh, None, FAKE, FAKE, FAKE, counts, ws,
+                              ws_bytes, None)
+    assert ppo(lold=None) == ERR_NULL
+    assert ppo(counts=None) == ERR_NULL
+    assert ppo(T=-1) == ERR_SHAPE
+    assert ppo(el=float("nan")) == ERR_VALUE
+    assert ppo(eh=-1.0) == ERR_VALUE
+    assert ppo(ws=None) == ERR_NULL
+    assert ppo(ws_bytes=8) == ERR_WORKSPACE
+    assert ppo(T=0) == OK
+    assert ppo(T=0, behav=FAKE) == OK
+
+
+def test_explained_variance_validation(L):
+    def ev(values=FAKE, moments=FAKE, out=FAKE, T=10, ws=FAKE, ws_bytes=1 << 20):
+        return L.sao_explained_variance(values, FAKE, FAKE, T, moments, out, ws, ws_bytes, None)
+    assert ev(values=None) == ERR_NULL
+    assert ev(moments=None) == ERR_NULL
+    assert ev(T=-5) == ERR_SHAPE
+    assert ev(ws=None) == ERR_NULL
+    assert ev(ws_bytes=8) == ERR_WORKSPACE
+    assert ev(ws=FAKE + 8) == ERR_WORKSPACE
+    assert ev(T=0, out=None) == OK
+
+
 def test_backward_validation(L):
     def bwd(dh=FAKE, dw=FAKE, T=16, H=64, V=100, dt=0, ws_bytes=1 << 40):
         return L.sao_loss_backward(FAKE, H, FAKE, H, FAKE, FAKE, FAKE, T, H, V, dt, dh, dw, FAKE, ws_bytes,
@@ -144,6 +171,8 @@ def test_workspace_sizes(L):
     big = ws(binding.OP_BACKWARD, 65536, 2048, 151936, 0)
     assert big < 65536 * 151936 * 2 // 2
     assert ws(binding.OP_LOSS, 1 << 26, 1, 1, 1) < 1 << 20
+    assert ws(binding.OP_PPO_LOSS, 12345, 1, 1, 1) == ws(binding.OP_LOSS, 12345, 1, 1, 1)
+    assert 0 < ws(binding.OP_EXPLAINED_VARIANCE, 1 << 26, 1, 1, 1) < 1 << 20
     # value loss: per-128-row partials of dw_v, far below the hidden states themselves
     assert 0 < ws(binding.OP_VALUE, 32768, 6144, 1, 0) < 32768 * 6144 * 2 // 16
 
