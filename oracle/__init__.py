@@ -7,5 +7,5 @@ HIP library and its Python binding) never imports it and has no CPU fallback.
 from .sao_oracle import (  # noqa: F401
     token_logprob, token_logprob_loop, advantage, dis_loss,
     loss_backward, loss_backward_loop, value_forward, value_loss, surrogate_S,
-    ppo_loss, explained_variance,
+    ppo_loss, explained_variance, step_advantage, steps_of,
 )

@@ -26,6 +26,9 @@ paper states it:
   pi_old / pi_rollout weighs the clipped term.
 * ``explained_variance`` -- EV = 1 - Var(R - V) / Var(R), the critic diagnostic
   of Sec. 4.4, over the loss-mask tokens.
+* ``step_advantage``   -- the step-level GAE of App. A.1: one advantage per
+  agentic step, with the step value as the mean or the last of its token values
+  and lambda scaled by the number of steps.
 
 Readings where the paper is silent (all listed in the design notes):
   gamma defaults to 1; ``l`` in lambda_policy is the trajectory's token length
@@ -40,7 +43,11 @@ Readings where the paper is silent (all listed in the design notes):
   A < 0 and r < 1 - eps_low (strict, as Sec. 3.1 states standard clipping);
   the pi_old / pi_rollout weight is a stop-gradient constant and is not
   truncated; EV uses population variances over loss-mask tokens and is NaN
-  when there are none or Var(R) = 0.
+  when there are none or Var(R) = 0. A step of App. A.1 is a maximal run of
+  consecutive loss-mask tokens inside one trajectory (one model turn); the
+  step reward sums the rewards from the step's first token up to the next
+  step's first token (or the trajectory's end), so observation rewards fold
+  into the preceding step as in the token-level form.
 
 Large inputs are processed in blocks of rows only to bound memory: rows are
 independent in every definition here, so the blocking changes no arithmetic.
@@ -382,3 +389,70 @@ def explained_variance(values, ret, mask):
     d = R - V
     var_d = float(np.mean((d - d.mean()) ** 2))
     return math.nan if var_r == 0.0 else 1.0 - var_d / var_r
+
+
+# --------------------------------------------------------------------------- #
+# App. A.1: step-level GAE (agentic step as the action).
+# --------------------------------------------------------------------------- #
+def steps_of(mask, s: int, e: int):
+    """The steps of trajectory [s, e): maximal runs [a, z) of consecutive mask-1 tokens."""
+    m = np.asarray(mask) != 0
+    runs, t = [], s
+    while t < e:
+        if m[t]:
+            a = t
+            while t < e and m[t]:
+                t += 1
+            runs.append((a, t))
+        else:
+            t += 1
+    return runs
+
+
+def step_advantage(values, rewards, mask, cu_seqlens, gamma: float = 1.0, lam: float = 1.0,
+                   alpha: float = 0.0, step_value: str = "average"):
+    """Step-level GAE of App. A.1 for a packed batch.
+
+    For trajectory b with steps [a_0, z_0), ..., [a_{n-1}, z_{n-1}) (a_n := e_b):
+        V_i   = mean(values[a_i:z_i])  ("average")  or  values[z_i - 1]  ("last")
+        R_i   = sum of rewards[a_i : a_{i+1}]
+        lam_b = lam if alpha <= 0, else max(0, 1 - 1/(alpha * n))   (steps, not tokens)
+        delta_i = R_i + gamma * V_{i+1} - V_i                        (V_n = 0)
+        A_i   = delta_i + gamma * lam_b * A_{i+1}                     (A_n = 0)
+        G_i   = R_i + gamma * G_{i+1}                                 (G_n = 0)
+    Every token of step i gets adv = A_i and ret = G_i; mask-0 tokens get 0.
+    Returns (adv, ret, last, N): last[t] = 1 on each step's final token (the
+    critic's loss mask in the last-token form), N = sum(mask).
+    """
+    if step_value not in ("average", "last"):
+        raise ValueError(step_value)
+    vals, rew = _f64(values), _f64(rewards)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    T = vals.shape[0]
+    adv = np.zeros(T, dtype=np.float64)
+    ret = np.zeros(T, dtype=np.float64)
+    last = np.zeros(T, dtype=np.uint8)
+    for b in range(cu.size - 1):
+        s, e = int(cu[b]), int(cu[b + 1])
+        steps = steps_of(mask, s, e)
+        n = len(steps)
+        if n == 0:
+            continue
+        lam_b = float(lam) if alpha <= 0.0 else max(0.0, 1.0 - 1.0 / (alpha * n))
+        if step_value == "average":
+            V = [math.fsum(vals[a:z]) / (z - a) for a, z in steps]
+        else:
+            V = [vals[z - 1] for a, z in steps]
+        starts = [a for a, _ in steps] + [e]
+        R = [math.fsum(rew[starts[i]:starts[i + 1]]) for i in range(n)]
+        A_next, G_next = 0.0, 0.0
+        for i in range(n - 1, -1, -1):
+            v_next = V[i + 1] if i + 1 < n else 0.0
+            delta = R[i] + gamma * v_next - V[i]
+            A_next = delta + gamma * lam_b * A_next
+            G_next = R[i] + gamma * G_next
+            a, z = steps[i]
+            adv[a:z] = A_next
+            ret[a:z] = G_next
+            last[z - 1] = 1
+    return adv, ret, last, int((np.asarray(mask) != 0).sum())
