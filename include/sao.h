@@ -80,8 +80,15 @@ typedef enum {
   SAO_OP_BACKWARD = 3,
   SAO_OP_VALUE = 4,
   SAO_OP_PPO_LOSS = 5,
-  SAO_OP_EXPLAINED_VARIANCE = 6
+  SAO_OP_EXPLAINED_VARIANCE = 6,
+  SAO_OP_STEP_ADVANTAGE = 7
 } sao_op_t;
+
+/* Step value of sao_step_advantage (App. A.1). */
+typedef enum {
+  SAO_STEP_AVERAGE = 0,  /* mean of the step's token values            */
+  SAO_STEP_LAST = 1      /* value of the step's last token              */
+} sao_step_value_t;
 
 /* Bits of the optional device status word. */
 #define SAO_STATUS_TARGET_RANGE 1  /* a loss-mask token's target is outside [0, V)   */
@@ -145,6 +152,29 @@ sao_status_t sao_advantage(const float* values, const float* rewards, const uint
                            const int32_t* cu_seqlens, int32_t B, int64_t T, double gamma,
                            double lam, double alpha, float* adv, float* ret, int64_t* n_tokens,
                            int32_t* status, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Step-level GAE, App. A.1: one advantage per agentic step instead of per token.
+ * A step is a maximal run of tokens with mask 1 inside a trajectory (one model
+ * turn). For trajectory b with steps [a_0, z_0) ... [a_{n-1}, z_{n-1}) and a_n = end:
+ *   V_i   = mean of values[a_i .. z_i)   (SAO_STEP_AVERAGE)  or  values[z_i - 1]  (SAO_STEP_LAST)
+ *   R_i   = sum of rewards[a_i .. a_{i+1})   (observation rewards fold into the step
+ *           before them; rewards before the first step are dropped)
+ *   delta_i = R_i + gamma * V_{i+1} - V_i    (V_n = 0)
+ *   A_i   = delta_i + gamma * lambda_b * A_{i+1},  G_i = R_i + gamma * G_{i+1}   (critic lambda = 1)
+ * lambda_b = max(0, 1 - 1/(alpha * n)) with n the trajectory's number of steps when
+ * alpha > 0, else `lam`. Every token of step i gets adv = A_i and ret = G_i; tokens
+ * with mask 0 get 0 (overwritten). last (nullable, uint8 [T], overwritten) is 1 on
+ * each step's final token: the critic's loss mask in the last-token form.
+ * n_tokens, status, the segment checks and their NaN outputs follow sao_advantage.
+ * Arithmetic is float64 inside; reductions run in a fixed order.
+ * ws: sao_workspace_size(SAO_OP_STEP_ADVANTAGE, T, 1, 1, SAO_F32) bytes (24 per token).
+ */
+sao_status_t sao_step_advantage(const float* values, const float* rewards, const uint8_t* mask,
+                                const int32_t* cu_seqlens, int32_t B, int64_t T, double gamma,
+                                double lam, double alpha, sao_step_value_t step_value, float* adv,
+                                float* ret, uint8_t* last, int64_t* n_tokens, int32_t* status,
+                                void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Direct double-sided importance sampling and the token-level mean,

@@ -16,13 +16,15 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsao.so")
 
 SAO_BF16, SAO_F32 = 0, 1
-OP_LOGPROB, OP_ADVANTAGE, OP_LOSS, OP_BACKWARD, OP_VALUE, OP_PPO_LOSS, OP_EXPLAINED_VARIANCE = range(7)
+(OP_LOGPROB, OP_ADVANTAGE, OP_LOSS, OP_BACKWARD, OP_VALUE, OP_PPO_LOSS, OP_EXPLAINED_VARIANCE,
+ OP_STEP_ADVANTAGE) = range(8)
+STEP_AVERAGE, STEP_LAST = 0, 1
 STATUS_TARGET_RANGE, STATUS_SEGMENTS, STATUS_NONFINITE = 1, 2, 4
 FLAG_MASKED, FLAG_USED, FLAG_LOW, FLAG_HIGH, FLAG_NONFINITE = 0, 1, 2, 3, 4
 
 EXPORTS = ("sao_status_string", "sao_last_error_message", "sao_version", "sao_workspace_size",
            "sao_token_logprob", "sao_advantage", "sao_clipped_loss", "sao_loss_backward",
-           "sao_value_forward", "sao_value_loss", "sao_ppo_loss", "sao_explained_variance",
+           "sao_value_forward", "sao_value_loss", "sao_ppo_loss", "sao_explained_variance", "sao_step_advantage",
            "sao_debug_time_kernel")
 KERNEL_NONE, KERNEL_HEAD_FORWARD = 0, 1
 
@@ -55,6 +57,9 @@ _SIGS = {
     "sao_ppo_loss": (ctypes.c_int, [_p, _p, _p, _p, _p, _i64, ctypes.c_float, ctypes.c_float, _p, _p, _p, _p,
                                     _p, _p, ctypes.c_size_t, _p]),
     "sao_explained_variance": (ctypes.c_int, [_p, _p, _p, _i64, _p, _p, _p, ctypes.c_size_t, _p]),
+    "sao_step_advantage": (ctypes.c_int, [_p, _p, _p, _p, ctypes.c_int32, _i64, ctypes.c_double, ctypes.c_double,
+                                          ctypes.c_double, ctypes.c_int, _p, _p, _p, _p, _p, _p, ctypes.c_size_t,
+                                          _p]),
     "sao_debug_time_kernel": (None, [ctypes.c_int, _p, _p]),
 }
 
@@ -186,6 +191,34 @@ def advantage(values: torch.Tensor, rewards: torch.Tensor, mask: torch.Tensor, c
             float(alpha), _ptr(adv), _ptr(ret), _ptr(n_tok), _ptr(status), _ptr(ws),
             0 if ws is None else ws.numel(), _stream(dev)))
     return adv, ret, n_tok
+
+
+def step_advantage(values: torch.Tensor, rewards: torch.Tensor, mask: torch.Tensor, cu_seqlens: torch.Tensor,
+                   gamma: float = 1.0, lam: float = 1.0, alpha: float = 0.0, step_value: str = "average",
+                   status: Optional[torch.Tensor] = None, want_last: bool = True, want_count: bool = True):
+    """Step-level GAE: (adv, ret, last or None, n_tokens or None); step_value "average" or "last"."""
+    T = values.shape[0]
+    B = cu_seqlens.shape[0] - 1
+    dev = values.device
+    form = {"average": STEP_AVERAGE, "last": STEP_LAST}.get(step_value)
+    if form is None:
+        raise ValueError(f"step_value must be 'average' or 'last', not {step_value!r}")
+    _vec(values, "values", torch.float32, T, dev)
+    _vec(rewards, "rewards", torch.float32, T, dev)
+    _vec(mask, "mask", torch.uint8, T, dev)
+    _vec(cu_seqlens, "cu_seqlens", torch.int32, B + 1, dev)
+    _vec(status, "status", torch.int32, 1, dev, optional=True)
+    adv = torch.empty(T, dtype=torch.float32, device=dev)
+    ret = torch.empty(T, dtype=torch.float32, device=dev)
+    last = torch.empty(T, dtype=torch.uint8, device=dev) if want_last else None
+    n_tok = torch.zeros(1, dtype=torch.int64, device=dev) if want_count else None
+    ws = _workspace(workspace_size(OP_STEP_ADVANTAGE, T, 1, 1, SAO_F32), dev)
+    if T:  # T == 0 is a no-op: empty tensors carry null pointers
+        _check(lib().sao_step_advantage(
+            _ptr(values), _ptr(rewards), _ptr(mask), _ptr(cu_seqlens), B, T, float(gamma), float(lam),
+            float(alpha), form, _ptr(adv), _ptr(ret), _ptr(last), _ptr(n_tok), _ptr(status), _ptr(ws),
+            0 if ws is None else ws.numel(), _stream(dev)))
+    return adv, ret, last, n_tok
 
 
 def clipped_loss(logp: torch.Tensor, logp_rollout: torch.Tensor, adv: torch.Tensor, mask: torch.Tensor,

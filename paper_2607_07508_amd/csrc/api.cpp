@@ -117,6 +117,8 @@ size_t sao_workspace_size(sao_op_t op, int64_t T, int64_t H, int64_t V, sao_dtyp
       return sao::loss_layout(T).total;
     case SAO_OP_EXPLAINED_VARIANCE:
       return sao::ev_layout(T).total;
+    case SAO_OP_STEP_ADVANTAGE:
+      return sao::step_layout(T).total;
   }
   return 0;
 }
@@ -151,6 +153,28 @@ sao_status_t sao_advantage(const float* values, const float* rewards, const uint
   return device(sao::launch_advantage(values, rewards, mask, cu_seqlens, B, T, gamma, lam, alpha, adv, ret,
                                       n_tokens, status, ws, stream),
                 "sao_advantage launch");
+}
+
+sao_status_t sao_step_advantage(const float* values, const float* rewards, const uint8_t* mask,
+                                const int32_t* cu_seqlens, int32_t B, int64_t T, double gamma, double lam,
+                                double alpha, sao_step_value_t step_value, float* adv, float* ret, uint8_t* last,
+                                int64_t* n_tokens, int32_t* status, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!values || !rewards || !mask || !cu_seqlens || !adv || !ret)
+    return fail(SAO_ERR_NULL, "values, rewards, mask, cu_seqlens, adv and ret are required");
+  if (B < 1) return fail(SAO_ERR_SHAPE, "B=%d must be >= 1", (int)B);
+  if (T < 0 || T > kMaxRows) return fail(SAO_ERR_SHAPE, "T=%lld out of range", (long long)T);
+  if (!(gamma >= 0.0 && gamma <= 1.0)) return fail(SAO_ERR_VALUE, "gamma=%g outside [0,1]", gamma);
+  if (!(lam >= 0.0 && lam <= 1.0)) return fail(SAO_ERR_VALUE, "lam=%g outside [0,1]", lam);
+  if (!std::isfinite(alpha)) return fail(SAO_ERR_VALUE, "alpha must be finite");
+  if (step_value != SAO_STEP_AVERAGE && step_value != SAO_STEP_LAST)
+    return fail(SAO_ERR_VALUE, "unknown step value form %d", (int)step_value);
+  if (T == 0) return ok();
+  if (sao_status_t s = check_ws(ws, ws_bytes, sao_workspace_size(SAO_OP_STEP_ADVANTAGE, T, 1, 1, SAO_F32)))
+    return s;
+  return device(sao::launch_step_advantage(values, rewards, mask, cu_seqlens, B, T, gamma, lam, alpha,
+                                           step_value == SAO_STEP_LAST, adv, ret, last, n_tokens, status, ws,
+                                           stream),
+                "sao_step_advantage launch");
 }
 
 sao_status_t sao_clipped_loss(const float* logp, const float* logp_rollout, const float* adv,

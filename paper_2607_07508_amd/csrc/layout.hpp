@@ -123,6 +123,25 @@ inline LossLayout loss_layout(int64_t T) {
   return L;
 }
 
+// sao_step_advantage: the segments flag, then a step table of T entries (a
+// trajectory's steps sit at its own token offset): start and end (int32), and
+// two doubles (the step's value and reward, later its advantage and return).
+struct StepLayout {
+  size_t bad, tab_a, tab_z, tab_v, tab_r, total;
+};
+
+inline StepLayout step_layout(int64_t T) {
+  StepLayout L{};
+  Carve c;
+  L.bad = c.take(4);
+  L.tab_a = c.take(4 * static_cast<size_t>(T));
+  L.tab_z = c.take(4 * static_cast<size_t>(T));
+  L.tab_v = c.take(8 * static_cast<size_t>(T));
+  L.tab_r = c.take(8 * static_cast<size_t>(T));
+  L.total = c.off;
+  return L;
+}
+
 // sao_ppo_loss shares the loss layout.
 
 // sao_explained_variance: five doubles per block

@@ -19,6 +19,7 @@
 // 8 tokens that it reads and writes with 16-byte vector accesses.
 #include "common.hpp"
 #include "launch.hpp"
+#include "segments.hpp"
 
 #include "../../include/sao.h"
 
@@ -108,23 +109,6 @@ __device__ __forceinline__ Aff wave_scan(Aff S) {
   return S;
 }
 
-// One block: cu_seqlens must rise from 0 to T without decreasing. Sets *bad (0/1),
-// zeroes *n_tokens, and flags the status word.
-__global__ __launch_bounds__(256) void k_check_segments(const int32_t* cu, int32_t B, int64_t T, int32_t* bad,
-                                                        int64_t* n_tokens, int32_t* status) {
-  __shared__ int32_t s_bad;
-  if (threadIdx.x == 0) s_bad = (cu[0] != 0 || static_cast<int64_t>(cu[B]) != T) ? 1 : 0;
-  __syncthreads();
-  for (int32_t i = threadIdx.x; i < B; i += blockDim.x)
-    if (cu[i + 1] < cu[i]) atomicOr(&s_bad, 1);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    *bad = s_bad;
-    if (n_tokens) *n_tokens = 0;
-    if (s_bad && status) atomicOr(status, SAO_STATUS_SEGMENTS);
-  }
-}
-
 constexpr int kScanThreads = 256;
 constexpr int kScanPer = 8;                               // tokens per thread per tile
 static_assert(kScanPer % 4 == 0, "whole blocks are read as 16-byte vectors");
@@ -159,17 +143,7 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
   if (*bad) {
-    // Malformed segments: every output is NaN; block b covers an even slice of [0, T).
-    const int64_t lo = T * b / B, hi = T * (b + 1) / B;
-    int64_t cnt = 0;
-    for (int64_t t = lo + tid; t < hi; t += kScanThreads) {
-      adv[t] = __builtin_nanf("");
-      ret[t] = __builtin_nanf("");
-      cnt += mask[t] != 0 ? 1 : 0;
-    }
-    cnt = wave_sum(cnt);
-    if (lane == 0 && n_tokens && cnt)
-      atomicAdd(reinterpret_cast<unsigned long long*>(n_tokens), static_cast<unsigned long long>(cnt));
+    malformed_slice<kScanThreads>(mask, B, T, adv, ret, nullptr, n_tokens);
     return;
   }
   const int64_t s = cu[b], e = cu[b + 1];
@@ -306,7 +280,7 @@ hipError_t launch_advantage(const float* values, const float* rewards, const uin
                             double alpha, float* adv, float* ret, int64_t* n_tokens, int32_t* status,
                             void* ws, hipStream_t st) {
   int32_t* bad = static_cast<int32_t*>(ws);
-  hipLaunchKernelGGL(k_check_segments, dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, n_tokens, status);
+  hipLaunchKernelGGL(k_check_segments<256>, dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, n_tokens, status);
   // Vector access needs 16-byte aligned float arrays and an 8-byte aligned mask.
   const uintptr_t f = reinterpret_cast<uintptr_t>(values) | reinterpret_cast<uintptr_t>(rewards) |
                       reinterpret_cast<uintptr_t>(adv) | reinterpret_cast<uintptr_t>(ret);

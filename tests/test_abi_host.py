@@ -85,6 +85,23 @@ def test_advantage_validation(L):
     assert adv(T=0) == OK
 
 
+def test_step_advantage_validation(L):
+    def st(vals=FAKE, B=2, T=10, gamma=1.0, lam=1.0, alpha=0.0, form=0, ws=FAKE, ws_bytes=1 << 20):
+        return L.sao_step_advantage(vals, FAKE, FAKE, FAKE, B, T, gamma, lam, alpha, form, FAKE, FAKE, None, None,
+                                    None, ws, ws_bytes, None)
+    assert st(vals=None) == ERR_NULL
+    assert st(B=0) == ERR_SHAPE
+    assert st(T=-1) == ERR_SHAPE
+    assert st(gamma=-0.5) == ERR_VALUE
+    assert st(lam=2.0) == ERR_VALUE
+    assert st(alpha=float("nan")) == ERR_VALUE
+    assert st(form=2) == ERR_VALUE
+    assert st(ws=None) == ERR_NULL
+    assert st(ws_bytes=64) == ERR_WORKSPACE
+    assert st(T=0) == OK
+    assert binding.workspace_size(binding.OP_STEP_ADVANTAGE, 1000, 1, 1, 1) >= 24 * 1000
+
+
 def test_loss_validation(L):
     def loss(T=10, el=0.2, eh=0.2, g=FAKE, ws=FAKE, ws_bytes=1 << 30):
         return L.sao_clipped_loss(FAKE, FAKE, FAKE, FAKE, T, el, eh, None, FAKE, g, FAKE, FAKE, ws, ws_bytes,
