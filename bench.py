@@ -112,7 +112,10 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
     17 for the scan (values, rewards, mask in; adv, ret out), 18 for the loss
     (logp, logp_rollout, adv, mask in; g, flags out), 22 for the surrogate
     (logp, logp_old, logp_behav, adv, mask in; g, flags out), 9 for the
-    explained variance (values, ret, mask in). One JSON line per size."""
+    explained variance (values, ret, mask in), and for the step-level GAE
+    (sao_step_advantage, step averages) 14 per token plus 4 per loss-mask token
+    (mask and rewards in, adv, ret and last out; values only on the steps).
+    One JSON line per size."""
     import torch
     import paper_2607_07508_amd as sao
     from paper_2607_07508_amd import binding as B
@@ -175,12 +178,22 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
             B._check(L.sao_ppo_loss(p(logp), p(lro), p(lbh), p(adv), p(db.mask), T, 0.2, 0.28, p(n), p(loss),
                                     p(g_out), p(flags), p(counts), p(ws), ws_bytes, st))
 
+        last = torch.empty(T, dtype=torch.uint8, device="cuda")
+        step_ws = torch.empty(B.workspace_size(B.OP_STEP_ADVANTAGE, T, 1, 1, B.SAO_F32), dtype=torch.uint8,
+                              device="cuda")
+
+        def step_gae():
+            B._check(L.sao_step_advantage(p(db.values), p(db.rewards), p(db.mask), p(db.cu_seqlens), cfg.B, T, 1.0,
+                                          1.0, 1.5, B.STEP_AVERAGE, p(g_out), p(ret), p(last), p(n), None,
+                                          p(step_ws), step_ws.numel(), st))
+
         def explained():
             B._check(L.sao_explained_variance(p(db.values), p(ret), p(db.mask), T, p(moments), p(ev), p(ws), ws_bytes,
                                               st))
         out = {}
         for name, fn, nbytes in (("advantage", scan, 17 * T), ("clipped_loss", epilogue, 18 * T),
-                                 ("ppo_loss", surrogate, 22 * T), ("explained_variance", explained, 9 * T)):
+                                 ("ppo_loss", surrogate, 22 * T), ("explained_variance", explained, 9 * T),
+                                 ("step_advantage", step_gae, 14 * T + 4 * int(b.mask.sum()))):
             for _ in range(3):
                 fn()
             torch.cuda.synchronize()
@@ -194,7 +207,7 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
             out[name] = {"ms": ms, "GB/s": nbytes / ms / 1e6, "frac_hbm": nbytes / ms / 1e6 / PEAK_HBM_GBS,
                          "bytes": nbytes}
         print(json.dumps({"mode": "epilogue_sweep", "T": T, "B": cfg.B, **out}), flush=True)
-        del db, b, logp, lro, lbh, adv, ret, g_out, flags, ws
+        del db, b, logp, lro, lbh, adv, ret, g_out, flags, ws, last, step_ws
         torch.cuda.empty_cache()
 
 

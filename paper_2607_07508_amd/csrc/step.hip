@@ -7,15 +7,17 @@
 //   A_i = R_i + gamma V_{i+1} - V_i + gamma lambda_b A_{i+1},  G_i = R_i + gamma G_{i+1}
 // with V_n = A_n = G_n = 0 and lambda_b = 1 - 1/(alpha n) when alpha > 0.
 //
-// One workgroup per trajectory, four phases separated by barriers:
-//  1. left to right over 2048-token tiles: step starts and ends, numbered by a
-//     block prefix count, go to a per-trajectory table in the workspace;
-//  2. each wave reduces whole steps (values over the run, rewards over the run
-//     and the observations after it) in a fixed lane order;
-//  3. the recurrence over steps: each thread takes a contiguous chunk of steps,
+// One workgroup per trajectory, three phases separated by barriers:
+//  1. left to right over 2048-token tiles: each token's step starts a new
+//     segment (a step's run and the observations after it); a block scan numbers
+//     the steps and a segmented block scan sums values (on the run) and rewards
+//     (over the segment), with the open segment's sums carried from tile to tile.
+//     Each step's start, end and sums (or last value) go to a per-trajectory
+//     table in the workspace, written once, by the thread holding the token;
+//  2. the recurrence over steps: each thread takes a contiguous chunk of steps,
 //     summarises it as an affine map of the state entering from its right, one
-//     thread chains the 256 maps, and each thread replays its chunk;
-//  4. each wave writes its steps' tokens: A_i and G_i on the run, zeros on the
+//     thread chains the chunk maps, and each thread replays its chunk;
+//  3. each wave writes its steps' tokens: A_i and G_i on the run, zeros on the
 //     observations after it, and the step's last token in `last`.
 // Arithmetic is float64; every reduction runs in a fixed order.
 #include "common.hpp"
@@ -51,11 +53,52 @@ __device__ __forceinline__ int block_exclusive_scan(int x, int* sh, int* total) 
   return before + incl - x;
 }
 
-__global__ __launch_bounds__(kStepThreads) void k_step_advantage(
+// Sums of a segmented scan: `f` marks that a segment starts inside the span, and
+// then v, r cover only the part after the last start.
+struct Seg {
+  int f;
+  double v, r;
+};
+// x then y (x on the left).
+__device__ __forceinline__ Seg seg_combine(const Seg& x, const Seg& y) {
+  return y.f ? y : Seg{x.f, x.v + y.v, x.r + y.r};
+}
+__device__ __forceinline__ Seg seg_shfl_up(const Seg& x, int o) {
+  return Seg{__shfl_up(x.f, o, 64), __shfl_up(x.v, o, 64), __shfl_up(x.r, o, 64)};
+}
+
+// Exclusive segmented scan over the block in thread order, `carry` standing
+// before thread 0; returns the sums entering this thread. `out` gets everything
+// (carry included) for the next tile.
+__device__ __forceinline__ Seg block_segmented_scan(const Seg& x, const Seg& carry, Seg* sh, Seg* out) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  Seg incl = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const Seg y = seg_shfl_up(incl, o);
+    if (lane >= o) incl = seg_combine(y, incl);
+  }
+  Seg excl = seg_shfl_up(incl, 1);
+  if (lane == 0) excl = Seg{0, 0.0, 0.0};
+  __syncthreads();  // earlier readers of sh are done
+  if (lane == 63) sh[wave] = incl;
+  __syncthreads();
+  Seg before = carry;
+  for (int w = 0; w < wave; ++w) before = seg_combine(before, sh[w]);
+  Seg all = carry;
+#pragma unroll
+  for (int w = 0; w < kStepThreads / 64; ++w) all = seg_combine(all, sh[w]);
+  *out = all;
+  return seg_combine(before, excl);
+}
+
+__global__ __launch_bounds__(kStepThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_step_advantage(
     const float* values, const float* rewards, const uint8_t* mask, const int32_t* cu, int32_t B, int64_t T,
     double gamma, double lam, double alpha, bool last_value, float* adv, float* ret, uint8_t* last,
-    int64_t* n_tokens, const int32_t* bad, int32_t* tab_a, int32_t* tab_z, double* tab_v, double* tab_r) {
+    int64_t* n_tokens, const int32_t* bad, int32_t* tab_a, int32_t* tab_z, double* tab_v, double* tab_r,
+    bool vec_ok) {
   __shared__ int s_scan[kStepThreads / 64];
+  __shared__ Seg s_seg[kStepThreads / 64];
   __shared__ double s_map[kStepThreads][4];   // per chunk: A = cA + mA A_in, G = cG + mG G_in
   __shared__ double s_in[kStepThreads][2];    // (A, G) entering each chunk from the right
   __shared__ int64_t s_cnt[kStepThreads / 64];
@@ -74,56 +117,91 @@ __global__ __launch_bounds__(kStepThreads) void k_step_advantage(
   double* tv = tab_v + s;
   double* tr = tab_r + s;
 
-  // Phase 1: step starts and ends (offsets from s), and the mask count.
-  int n = 0, n_end = 0;
+  // Phase 1: step starts, ends and sums (segment i: step i's run and the
+  // observations after it, up to the next step; rewards before the first step
+  // fall in no segment).
+  int n = 0;
+  Seg carry{0, 0.0, 0.0};
   int64_t cnt = 0;
   for (int64_t t0 = s / kStepTile * kStepTile; t0 < e; t0 += kStepTile) {
     const int64_t c0 = t0 + static_cast<int64_t>(tid) * kStepPer;
-    bool m[kStepPer + 2];  // m[0] is token c0 - 1, m[kStepPer + 1] token c0 + kStepPer
+    bool m[kStepPer + 2];  // m[j] is token c0 - 1 + j
+    float v[kStepPer], r[kStepPer];  // v is 0 off the runs
+    m[0] = c0 - 1 >= s && c0 - 1 < e && mask[c0 - 1] != 0;
+    m[kStepPer + 1] = c0 + kStepPer >= s && c0 + kStepPer < e && mask[c0 + kStepPer] != 0;
+    if (vec_ok && c0 >= s && c0 + kStepPer <= e) {
+      const f32x4_t* pv = reinterpret_cast<const f32x4_t*>(values + c0);
+      const f32x4_t* pr = reinterpret_cast<const f32x4_t*>(rewards + c0);
+      const uint64_t m8 = *reinterpret_cast<const uint64_t*>(mask + c0);
 #pragma unroll
-    for (int j = 0; j < kStepPer + 2; ++j) {
-      const int64_t t = c0 - 1 + j;
-      m[j] = t >= s && t < e && mask[t] != 0;
+      for (int q = 0; q < kStepPer / 4; ++q) {
+        const f32x4_t vq = pv[q], rq = pr[q];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int k = 4 * q + j;
+          m[k + 1] = ((m8 >> (8 * k)) & 0xffu) != 0;
+          v[k] = m[k + 1] ? vq[j] : 0.0f;
+          r[k] = rq[j];
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kStepPer; ++j) {
+        const int64_t t = c0 + j;
+        const bool in = t >= s && t < e;
+        m[j + 1] = in && mask[t] != 0;
+        v[j] = m[j + 1] ? values[t] : 0.0f;
+        r[j] = in ? rewards[t] : 0.0f;
+      }
     }
-    int ns = 0, ne = 0;
+    // This thread's starts, and its sums after its last start.
+    int ns = 0;
+    Seg x{0, 0.0, 0.0};
 #pragma unroll
-    for (int j = 1; j <= kStepPer; ++j) {
-      cnt += m[j] ? 1 : 0;
-      ns += (m[j] && !m[j - 1]) ? 1 : 0;
-      ne += (m[j] && !m[j + 1]) ? 1 : 0;
+    for (int j = 0; j < kStepPer; ++j) {
+      const bool st = m[j + 1] && !m[j];
+      cnt += m[j + 1] ? 1 : 0;
+      ns += st ? 1 : 0;
+      if (st) x = Seg{1, 0.0, 0.0};
+      x.v += static_cast<double>(v[j]);
+      x.r += static_cast<double>(r[j]);
     }
-    int tot_s, tot_e;
-    int is = n + block_exclusive_scan(ns, s_scan, &tot_s);
-    int ie = n_end + block_exclusive_scan(ne, s_scan, &tot_e);
+    int tot_s;
+    const int first = n + block_exclusive_scan(ns, s_scan, &tot_s);
+    Seg next_carry;
+    Seg run = block_segmented_scan(x, carry, s_seg, &next_carry);
+    // Replay: `key` is the step whose segment holds the token (-1 before the first).
+    int key = first - 1;
 #pragma unroll
-    for (int j = 1; j <= kStepPer; ++j) {
-      const int32_t off = static_cast<int32_t>(c0 - 1 + j - s);
-      if (m[j] && !m[j - 1]) ta[is++] = off;
-      if (m[j] && !m[j + 1]) tz[ie++] = off + 1;
+    for (int j = 0; j < kStepPer; ++j) {
+      const int64_t t = c0 + j;
+      if (t < s || t >= e) continue;
+      const int32_t off = static_cast<int32_t>(t - s);
+      if (m[j + 1] && !m[j]) {
+        ++key;
+        run = Seg{1, 0.0, 0.0};
+        ta[key] = off;
+      }
+      run.v += static_cast<double>(v[j]);
+      run.r += static_cast<double>(r[j]);
+      if (key < 0) continue;
+      if (m[j + 1] && !m[j + 2]) {
+        tz[key] = off + 1;
+        if (last_value) tv[key] = static_cast<double>(v[j]);
+      }
+      const bool seg_end = t == e - 1 || (m[j + 2] && !m[j + 1]);
+      if (seg_end) {
+        if (!last_value) tv[key] = run.v;
+        tr[key] = run.r;
+      }
     }
     n += tot_s;
-    n_end += tot_e;
+    carry = next_carry;
   }
-  __syncthreads();  // the table is written (n_end == n: every run starts and ends)
+  __syncthreads();  // the table is written
 
-  // Phase 2: V_i and R_i, one wave per step.
-  for (int i = wave; i < n; i += kStepThreads / 64) {
-    const int64_t a = ta[i], z = tz[i], nxt = i + 1 < n ? ta[i + 1] : L;
-    double sv = 0.0, sr = 0.0;
-    if (!last_value)
-      for (int64_t t = a + lane; t < z; t += 64) sv += static_cast<double>(values[s + t]);
-    for (int64_t t = a + lane; t < nxt; t += 64) sr += static_cast<double>(rewards[s + t]);
-    sv = wave_sum(sv);
-    sr = wave_sum(sr);
-    if (lane == 0) {
-      tv[i] = last_value ? static_cast<double>(values[s + z - 1]) : sv / static_cast<double>(z - a);
-      tr[i] = sr;
-    }
-  }
-  __syncthreads();
-
-  // Phase 3: A_i and G_i. Thread j takes steps [p, q); its map sends the state
-  // (A_q, G_q) entering from the right to (A_p, G_p).
+  // Phase 2: A_i and G_i. Thread j takes steps [p, q); its map sends the state
+  // (A_q, G_q) entering from the right to (A_p, G_p). The table then holds them.
   double lam_b = lam;
   if (alpha > 0.0) {
     lam_b = 1.0 - 1.0 / (alpha * static_cast<double>(n));
@@ -132,16 +210,19 @@ __global__ __launch_bounds__(kStepThreads) void k_step_advantage(
   const double kappa = gamma * lam_b;
   const int per = (n + kStepThreads - 1) / kStepThreads;
   const int p = min(n, tid * per), q = min(n, p + per);
-  const double v_right = q < n ? tv[q] : 0.0;   // read before any thread overwrites the table
+  auto step_value = [&](int i) {
+    return last_value ? tv[i] : tv[i] / static_cast<double>(tz[i] - ta[i]);
+  };
+  const double v_right = q < n ? step_value(q) : 0.0;   // read before any thread overwrites the table
   {
     double cA = 0.0, mA = 1.0, cG = 0.0, mG = 1.0, vn = v_right;
     for (int i = q - 1; i >= p; --i) {
-      const double v = tv[i], r = tr[i];
-      cA = fma(kappa, cA, fma(gamma, vn, r - v));
+      const double vi = step_value(i), ri = tr[i];
+      cA = fma(kappa, cA, fma(gamma, vn, ri - vi));
       mA *= kappa;
-      cG = fma(gamma, cG, r);
+      cG = fma(gamma, cG, ri);
       mG *= gamma;
-      vn = v;
+      vn = vi;
     }
     s_map[tid][0] = cA;
     s_map[tid][1] = mA;
@@ -151,7 +232,8 @@ __global__ __launch_bounds__(kStepThreads) void k_step_advantage(
   __syncthreads();
   if (tid == 0) {
     double A = 0.0, G = 0.0;
-    for (int j = kStepThreads - 1; j >= 0; --j) {
+    const int chunks = per > 0 ? (n + per - 1) / per : 0;
+    for (int j = chunks - 1; j >= 0; --j) {
       s_in[j][0] = A;
       s_in[j][1] = G;
       A = fma(s_map[j][1], A, s_map[j][0]);
@@ -159,20 +241,20 @@ __global__ __launch_bounds__(kStepThreads) void k_step_advantage(
     }
   }
   __syncthreads();
-  {
+  if (p < q) {
     double A = s_in[tid][0], G = s_in[tid][1], vn = v_right;
     for (int i = q - 1; i >= p; --i) {
-      const double v = tv[i], r = tr[i];
-      A = fma(kappa, A, fma(gamma, vn, r - v));
-      G = fma(gamma, G, r);
-      vn = v;
-      tv[i] = A;  // the table now holds (A_i, G_i)
+      const double vi = step_value(i), ri = tr[i];
+      A = fma(kappa, A, fma(gamma, vn, ri - vi));
+      G = fma(gamma, G, ri);
+      vn = vi;
+      tv[i] = A;
       tr[i] = G;
     }
   }
   __syncthreads();
 
-  // Phase 4: outputs. Tokens before the first step, and every token of a
+  // Phase 3: outputs. Tokens before the first step, and every token of a
   // trajectory without steps, are zero; each wave then writes its steps' spans.
   const int64_t head = n > 0 ? ta[0] : L;
   for (int64_t t = tid; t < head; t += kStepThreads) {
@@ -210,10 +292,13 @@ hipError_t launch_step_advantage(const float* values, const float* rewards, cons
   char* w8 = static_cast<char*>(ws);
   int32_t* bad = reinterpret_cast<int32_t*>(w8 + Ly.bad);
   hipLaunchKernelGGL(k_check_segments<256>, dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, n_tokens, status);
+  // Whole in-trajectory blocks of 8 tokens use vector loads when the bases allow them.
+  const bool vec_ok = ((reinterpret_cast<uintptr_t>(values) | reinterpret_cast<uintptr_t>(rewards)) & 15u) == 0 &&
+                      (reinterpret_cast<uintptr_t>(mask) & 7u) == 0;
   hipLaunchKernelGGL(k_step_advantage, dim3(B), dim3(kStepThreads), 0, st, values, rewards, mask, cu_seqlens, B, T,
                      gamma, lam, alpha, last_value, adv, ret, last, n_tokens, bad,
                      reinterpret_cast<int32_t*>(w8 + Ly.tab_a), reinterpret_cast<int32_t*>(w8 + Ly.tab_z),
-                     reinterpret_cast<double*>(w8 + Ly.tab_v), reinterpret_cast<double*>(w8 + Ly.tab_r));
+                     reinterpret_cast<double*>(w8 + Ly.tab_v), reinterpret_cast<double*>(w8 + Ly.tab_r), vec_ok);
   return hipGetLastError();
 }
 
