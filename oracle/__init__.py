@@ -8,4 +8,5 @@ from .sao_oracle import (  # noqa: F401
     token_logprob, token_logprob_loop, advantage, dis_loss,
     loss_backward, loss_backward_loop, value_forward, value_loss, surrogate_S,
     ppo_loss, explained_variance, step_advantage, steps_of,
+    trajectory_rewards, group_advantage, running_mean_advantage,
 )

@@ -29,6 +29,11 @@ paper states it:
 * ``step_advantage``   -- the step-level GAE of App. A.1: one advantage per
   agentic step, with the step value as the mean or the last of its token values
   and lambda scaled by the number of steps.
+* ``group_advantage`` / ``running_mean_advantage`` -- the critic-free baselines
+  the paper compares with: GRPO's group-normalised sequence reward (Sec. 2)
+  and a sliding-window running-mean reward baseline (the 8 most recent rewards
+  of each prompt in the Sec. 4.3 ablation, the 128 most recent in the Sec. 4.5
+  online comparison), one advantage per trajectory.
 
 Readings where the paper is silent (all listed in the design notes):
   gamma defaults to 1; ``l`` in lambda_policy is the trajectory's token length
@@ -47,7 +52,13 @@ Readings where the paper is silent (all listed in the design notes):
   consecutive loss-mask tokens inside one trajectory (one model turn); the
   step reward sums the rewards from the step's first token up to the next
   step's first token (or the trajectory's end), so observation rewards fold
-  into the preceding step as in the token-level form.
+  into the preceding step as in the token-level form. For the critic-free
+  baselines: a trajectory's reward is the sum of its token rewards; a group is
+  `group_size` consecutive trajectories; sigma uses the population variance
+  with eps_stab inside the root, as printed; the running-mean window holds the
+  `window` most recent earlier rewards of the same key (prompt), the
+  trajectory's own reward excluded, in arrival order (history first, then the
+  batch in order), and an empty window gives baseline 0.
 
 Large inputs are processed in blocks of rows only to bound memory: rows are
 independent in every definition here, so the blocking changes no arithmetic.
@@ -456,3 +467,60 @@ def step_advantage(values, rewards, mask, cu_seqlens, gamma: float = 1.0, lam: f
             ret[a:z] = G_next
             last[z - 1] = 1
     return adv, ret, last, int((np.asarray(mask) != 0).sum())
+
+
+# --------------------------------------------------------------------------- #
+# Critic-free baselines: GRPO's group normalisation and a running-mean window.
+# --------------------------------------------------------------------------- #
+def trajectory_rewards(rewards, cu_seqlens):
+    """R_b = sum of the token rewards of trajectory b (a sequence-level reward)."""
+    rew = _f64(rewards)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    return np.array([math.fsum(rew[cu[b]:cu[b + 1]]) for b in range(cu.size - 1)], dtype=np.float64)
+
+
+def _broadcast(A, mask, cu_seqlens):
+    m = np.asarray(mask) != 0
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    adv = np.zeros(m.size, dtype=np.float64)
+    for b in range(cu.size - 1):
+        s, e = int(cu[b]), int(cu[b + 1])
+        adv[s:e] = np.where(m[s:e], A[b], 0.0)
+    return adv
+
+
+def group_advantage(rewards, mask, cu_seqlens, group_size: int, eps_stab: float):
+    """GRPO advantage (Sec. 2): trajectories [g G, (g+1) G) answer one prompt;
+        mu_g = (1/G) sum R_j,  sigma_g = sqrt((1/G) sum (R_j - mu_g)^2 + eps_stab),
+        A_b = (R_b - mu_g) / sigma_g   on every loss-mask token of trajectory b.
+    Returns (adv [T], A [B], R [B], N)."""
+    R = trajectory_rewards(rewards, cu_seqlens)
+    B, G = R.size, int(group_size)
+    if G < 1 or B % G != 0:
+        raise ValueError("B must be a multiple of group_size")
+    A = np.zeros(B, dtype=np.float64)
+    for g in range(B // G):
+        Rg = R[g * G:(g + 1) * G]
+        mu = math.fsum(Rg) / G
+        var = math.fsum((Rg - mu) ** 2) / G
+        with np.errstate(divide="ignore", invalid="ignore"):
+            A[g * G:(g + 1) * G] = (Rg - mu) / np.float64(math.sqrt(var + eps_stab))
+    return _broadcast(A, mask, cu_seqlens), A, R, int((np.asarray(mask) != 0).sum())
+
+
+def running_mean_advantage(rewards, mask, cu_seqlens, window: int, history=None, keys=None):
+    """Running-mean baseline: A_b = R_b - mean(the `window` most recent earlier rewards of
+    b's key), the batch read in arrival order after `history` (a dict key -> list of past
+    rewards, oldest first); an empty window gives baseline 0.
+    Returns (adv [T], A [B], R [B], N, history after the batch)."""
+    R = trajectory_rewards(rewards, cu_seqlens)
+    hist = {k: [float(x) for x in v] for k, v in (history or {}).items()}
+    A = np.zeros(R.size, dtype=np.float64)
+    for b in range(R.size):
+        k = 0 if keys is None else int(keys[b])
+        past = hist.setdefault(k, [])
+        win = past[-window:] if window > 0 else []
+        base = math.fsum(win) / len(win) if win else 0.0
+        A[b] = R[b] - base
+        past.append(float(R[b]))
+    return _broadcast(A, mask, cu_seqlens), A, R, int((np.asarray(mask) != 0).sum()), hist
