@@ -81,7 +81,9 @@ typedef enum {
   SAO_OP_VALUE = 4,
   SAO_OP_PPO_LOSS = 5,
   SAO_OP_EXPLAINED_VARIANCE = 6,
-  SAO_OP_STEP_ADVANTAGE = 7
+  SAO_OP_STEP_ADVANTAGE = 7,
+  SAO_OP_GROUP_ADVANTAGE = 8,
+  SAO_OP_RUNNING_MEAN_ADVANTAGE = 9
 } sao_op_t;
 
 /* Step value of sao_step_advantage (App. A.1). */
@@ -94,6 +96,7 @@ typedef enum {
 #define SAO_STATUS_TARGET_RANGE 1  /* a loss-mask token's target is outside [0, V)   */
 #define SAO_STATUS_SEGMENTS     2  /* cu_seqlens is not non-decreasing from 0 to T    */
 #define SAO_STATUS_NONFINITE    4  /* a log-sum-exp came out NaN or infinite          */
+#define SAO_STATUS_KEY_RANGE    8  /* a running-mean key is outside [0, n_keys)        */
 
 /* Per-token flags written by sao_clipped_loss (sao_ppo_loss: see there). */
 #define SAO_FLAG_MASKED    0  /* mask == 0                                       */
@@ -175,6 +178,51 @@ sao_status_t sao_step_advantage(const float* values, const float* rewards, const
                                 double lam, double alpha, sao_step_value_t step_value, float* adv,
                                 float* ret, uint8_t* last, int64_t* n_tokens, int32_t* status,
                                 void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * GRPO's group-normalised advantage, the critic-free baseline of Sec. 2.
+ * Trajectories [g*group_size, (g+1)*group_size) answer one prompt (B must be a
+ * multiple of group_size). With R_b the sum of trajectory b's rewards:
+ *   mu_g = mean of the group's R,  sigma_g = sqrt(population variance + eps_stab),
+ *   traj_adv[b] = (R_b - mu_g) / sigma_g      (eps_stab = 0 and equal rewards: NaN)
+ *   adv[t] = traj_adv[b] on trajectory b's tokens with mask 1, else 0 (overwritten)
+ * traj_reward[B] and traj_adv[B] are float64 outputs (required). n_tokens,
+ * status and the segment checks follow sao_advantage (malformed segments: NaN
+ * everywhere). ws: sao_workspace_size(SAO_OP_GROUP_ADVANTAGE, T, 1, 1, SAO_F32).
+ */
+sao_status_t sao_group_advantage(const float* rewards, const uint8_t* mask, const int32_t* cu_seqlens,
+                                 int32_t B, int64_t T, int32_t group_size, double eps_stab,
+                                 float* adv, double* traj_reward, double* traj_adv,
+                                 int64_t* n_tokens, int32_t* status, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
+/*
+ * Running-mean reward baseline: the 8 most recent rewards of each prompt in the
+ * Sec. 4.3 ablation, the 128 most recent in the Sec. 4.5 online comparison.
+ * Trajectories arrive in batch order; trajectory b has key keys[b] in [0, n_keys)
+ * (its prompt; keys == NULL puts every trajectory under key 0). With R_b the sum
+ * of trajectory b's rewards:
+ *   traj_adv[b] = R_b - mean of the `window` most recent earlier rewards of its key
+ *                 (the history, then earlier trajectories of this batch; the
+ *                 trajectory's own reward excluded; an empty window gives 0)
+ *   adv[t]      = traj_adv[b] on trajectory b's tokens with mask 1, else 0
+ * history (float64 [n_keys][window], in/out) is a ring per key: the reward pushed
+ * as the key's j-th (from 0) sits at slot j mod window; seen (int64 [n_keys],
+ * in/out) counts the rewards pushed per key. Zero both before the first batch.
+ * This call pushes the batch's rewards after computing the baselines. A key
+ * outside [0, n_keys) sets SAO_STATUS_KEY_RANGE, gives that trajectory NaN and
+ * pushes nothing for it. traj_reward and traj_adv are float64 [B] outputs
+ * (required); n_tokens, status and the segment checks follow sao_advantage
+ * (malformed segments: NaN outputs, history untouched).
+ * ws: sao_workspace_size(SAO_OP_RUNNING_MEAN_ADVANTAGE, T, 1, 1, SAO_F32) bytes.
+ */
+sao_status_t sao_running_mean_advantage(const float* rewards, const uint8_t* mask,
+                                        const int32_t* cu_seqlens, int32_t B, int64_t T,
+                                        const int32_t* keys, int32_t n_keys, int32_t window,
+                                        double* history, int64_t* seen, float* adv,
+                                        double* traj_reward, double* traj_adv, int64_t* n_tokens,
+                                        int32_t* status, void* ws, size_t ws_bytes,
+                                        hipStream_t stream);
 
 /*
  * Direct double-sided importance sampling and the token-level mean,

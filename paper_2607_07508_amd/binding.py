@@ -17,14 +17,15 @@ LIB_PATH = os.path.join(_HERE, "libsao.so")
 
 SAO_BF16, SAO_F32 = 0, 1
 (OP_LOGPROB, OP_ADVANTAGE, OP_LOSS, OP_BACKWARD, OP_VALUE, OP_PPO_LOSS, OP_EXPLAINED_VARIANCE,
- OP_STEP_ADVANTAGE) = range(8)
+ OP_STEP_ADVANTAGE, OP_GROUP_ADVANTAGE, OP_RUNNING_MEAN_ADVANTAGE) = range(10)
 STEP_AVERAGE, STEP_LAST = 0, 1
-STATUS_TARGET_RANGE, STATUS_SEGMENTS, STATUS_NONFINITE = 1, 2, 4
+STATUS_TARGET_RANGE, STATUS_SEGMENTS, STATUS_NONFINITE, STATUS_KEY_RANGE = 1, 2, 4, 8
 FLAG_MASKED, FLAG_USED, FLAG_LOW, FLAG_HIGH, FLAG_NONFINITE = 0, 1, 2, 3, 4
 
 EXPORTS = ("sao_status_string", "sao_last_error_message", "sao_version", "sao_workspace_size",
            "sao_token_logprob", "sao_advantage", "sao_clipped_loss", "sao_loss_backward",
            "sao_value_forward", "sao_value_loss", "sao_ppo_loss", "sao_explained_variance", "sao_step_advantage",
+           "sao_group_advantage", "sao_running_mean_advantage",
            "sao_debug_time_kernel")
 KERNEL_NONE, KERNEL_HEAD_FORWARD = 0, 1
 
@@ -60,6 +61,11 @@ _SIGS = {
     "sao_step_advantage": (ctypes.c_int, [_p, _p, _p, _p, ctypes.c_int32, _i64, ctypes.c_double, ctypes.c_double,
                                           ctypes.c_double, ctypes.c_int, _p, _p, _p, _p, _p, _p, ctypes.c_size_t,
                                           _p]),
+    "sao_group_advantage": (ctypes.c_int, [_p, _p, _p, ctypes.c_int32, _i64, ctypes.c_int32, ctypes.c_double, _p, _p,
+                                           _p, _p, _p, _p, ctypes.c_size_t, _p]),
+    "sao_running_mean_advantage": (ctypes.c_int, [_p, _p, _p, ctypes.c_int32, _i64, _p, ctypes.c_int32,
+                                                  ctypes.c_int32, _p, _p, _p, _p, _p, _p, _p, _p, ctypes.c_size_t,
+                                                  _p]),
     "sao_debug_time_kernel": (None, [ctypes.c_int, _p, _p]),
 }
 
@@ -219,6 +225,65 @@ def step_advantage(values: torch.Tensor, rewards: torch.Tensor, mask: torch.Tens
             float(alpha), form, _ptr(adv), _ptr(ret), _ptr(last), _ptr(n_tok), _ptr(status), _ptr(ws),
             0 if ws is None else ws.numel(), _stream(dev)))
     return adv, ret, last, n_tok
+
+
+def _segment_inputs(rewards, mask, cu_seqlens, status):
+    T = rewards.shape[0]
+    B = cu_seqlens.shape[0] - 1
+    dev = rewards.device
+    _vec(rewards, "rewards", torch.float32, T, dev)
+    _vec(mask, "mask", torch.uint8, T, dev)
+    _vec(cu_seqlens, "cu_seqlens", torch.int32, B + 1, dev)
+    _vec(status, "status", torch.int32, 1, dev, optional=True)
+    return T, B, dev
+
+
+def group_advantage(rewards: torch.Tensor, mask: torch.Tensor, cu_seqlens: torch.Tensor, group_size: int,
+                    eps_stab: float, status: Optional[torch.Tensor] = None, want_count: bool = True):
+    """GRPO advantage: (adv [T] f32, traj_adv [B] f64, traj_reward [B] f64, n_tokens or None)."""
+    T, B, dev = _segment_inputs(rewards, mask, cu_seqlens, status)
+    adv = torch.empty(T, dtype=torch.float32, device=dev)
+    traj_reward = torch.empty(B, dtype=torch.float64, device=dev)
+    traj_adv = torch.empty(B, dtype=torch.float64, device=dev)
+    n_tok = torch.zeros(1, dtype=torch.int64, device=dev) if want_count else None
+    ws = _workspace(workspace_size(OP_GROUP_ADVANTAGE, T, 1, 1, SAO_F32), dev)
+    if T:  # T == 0 is a no-op: empty tensors carry null pointers
+        _check(lib().sao_group_advantage(
+            _ptr(rewards), _ptr(mask), _ptr(cu_seqlens), B, T, int(group_size), float(eps_stab), _ptr(adv),
+            _ptr(traj_reward), _ptr(traj_adv), _ptr(n_tok), _ptr(status), _ptr(ws),
+            0 if ws is None else ws.numel(), _stream(dev)))
+    return adv, traj_adv, traj_reward, n_tok
+
+
+def running_mean_state(n_keys: int, window: int, device) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Zeroed (history [n_keys, window] f64, seen [n_keys] i64) for running_mean_advantage."""
+    return (torch.zeros((n_keys, window), dtype=torch.float64, device=device),
+            torch.zeros(n_keys, dtype=torch.int64, device=device))
+
+
+def running_mean_advantage(rewards: torch.Tensor, mask: torch.Tensor, cu_seqlens: torch.Tensor,
+                           history: torch.Tensor, seen: torch.Tensor, keys: Optional[torch.Tensor] = None,
+                           status: Optional[torch.Tensor] = None, want_count: bool = True):
+    """Running-mean baseline over a window of history.shape[1] rewards per key; updates
+    (history, seen) in place. Returns (adv [T] f32, traj_adv [B] f64, traj_reward [B] f64, n_tokens)."""
+    T, B, dev = _segment_inputs(rewards, mask, cu_seqlens, status)
+    if history.dim() != 2:
+        raise ValueError("history must be [n_keys, window]")
+    n_keys, window = history.shape
+    _vec(history, "history", torch.float64, n_keys * window, dev)
+    _vec(seen, "seen", torch.int64, n_keys, dev)
+    _vec(keys, "keys", torch.int32, B, dev, optional=True)
+    adv = torch.empty(T, dtype=torch.float32, device=dev)
+    traj_reward = torch.empty(B, dtype=torch.float64, device=dev)
+    traj_adv = torch.empty(B, dtype=torch.float64, device=dev)
+    n_tok = torch.zeros(1, dtype=torch.int64, device=dev) if want_count else None
+    ws = _workspace(workspace_size(OP_RUNNING_MEAN_ADVANTAGE, T, 1, 1, SAO_F32), dev)
+    if T:  # T == 0 is a no-op: empty tensors carry null pointers
+        _check(lib().sao_running_mean_advantage(
+            _ptr(rewards), _ptr(mask), _ptr(cu_seqlens), B, T, _ptr(keys), n_keys, window, _ptr(history),
+            _ptr(seen), _ptr(adv), _ptr(traj_reward), _ptr(traj_adv), _ptr(n_tok), _ptr(status), _ptr(ws),
+            0 if ws is None else ws.numel(), _stream(dev)))
+    return adv, traj_adv, traj_reward, n_tok
 
 
 def clipped_loss(logp: torch.Tensor, logp_rollout: torch.Tensor, adv: torch.Tensor, mask: torch.Tensor,

@@ -17,7 +17,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsao.so")
 ARCH = os.environ.get("SAO_OFFLOAD_ARCH", "gfx950")
 
-SOURCES = ["api.cpp", "head.hip", "scan.hip", "step.hip", "loss.hip", "ev.hip", "value.hip"]
+SOURCES = ["api.cpp", "head.hip", "scan.hip", "step.hip", "baseline.hip", "loss.hip", "ev.hip", "value.hip"]
 
 
 def hipcc() -> str:

@@ -56,6 +56,15 @@ sao_status_t check_ws(void* ws, size_t ws_bytes, size_t need) {
   return SAO_OK;
 }
 
+// Checks shared by the advantage entry points.
+sao_status_t check_segments_args(const float* rewards, const uint8_t* mask, const int32_t* cu_seqlens, int32_t B,
+                                 int64_t T, const float* adv) {
+  if (!rewards || !mask || !cu_seqlens || !adv) return fail(SAO_ERR_NULL, "rewards, mask, cu_seqlens and adv are required");
+  if (B < 1) return fail(SAO_ERR_SHAPE, "B=%d must be >= 1", (int)B);
+  if (T < 0 || T > kMaxRows) return fail(SAO_ERR_SHAPE, "T=%lld out of range", (long long)T);
+  return SAO_OK;
+}
+
 sao_status_t device(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(SAO_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
   return ok();
@@ -119,6 +128,9 @@ size_t sao_workspace_size(sao_op_t op, int64_t T, int64_t H, int64_t V, sao_dtyp
       return sao::ev_layout(T).total;
     case SAO_OP_STEP_ADVANTAGE:
       return sao::step_layout(T).total;
+    case SAO_OP_GROUP_ADVANTAGE:
+    case SAO_OP_RUNNING_MEAN_ADVANTAGE:
+      return sao::kAdvantageWorkspace;
   }
   return 0;
 }
@@ -175,6 +187,40 @@ sao_status_t sao_step_advantage(const float* values, const float* rewards, const
                                            step_value == SAO_STEP_LAST, adv, ret, last, n_tokens, status, ws,
                                            stream),
                 "sao_step_advantage launch");
+}
+
+sao_status_t sao_group_advantage(const float* rewards, const uint8_t* mask, const int32_t* cu_seqlens, int32_t B,
+                                 int64_t T, int32_t group_size, double eps_stab, float* adv, double* traj_reward,
+                                 double* traj_adv, int64_t* n_tokens, int32_t* status, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  if (sao_status_t s = check_segments_args(rewards, mask, cu_seqlens, B, T, adv)) return s;
+  if (!traj_reward || !traj_adv) return fail(SAO_ERR_NULL, "traj_reward and traj_adv are required");
+  if (group_size < 1 || B % group_size != 0)
+    return fail(SAO_ERR_SHAPE, "B=%d must be a positive multiple of group_size=%d", (int)B, (int)group_size);
+  if (!(eps_stab >= 0.0) || !std::isfinite(eps_stab)) return fail(SAO_ERR_VALUE, "eps_stab must be finite and >= 0");
+  if (T == 0) return ok();
+  if (sao_status_t s = check_ws(ws, ws_bytes, sao_workspace_size(SAO_OP_GROUP_ADVANTAGE, T, 1, 1, SAO_F32))) return s;
+  return device(sao::launch_group_advantage(rewards, mask, cu_seqlens, B, T, group_size, eps_stab, adv, traj_reward,
+                                            traj_adv, n_tokens, status, ws, stream),
+                "sao_group_advantage launch");
+}
+
+sao_status_t sao_running_mean_advantage(const float* rewards, const uint8_t* mask, const int32_t* cu_seqlens,
+                                        int32_t B, int64_t T, const int32_t* keys, int32_t n_keys, int32_t window,
+                                        double* history, int64_t* seen, float* adv, double* traj_reward,
+                                        double* traj_adv, int64_t* n_tokens, int32_t* status, void* ws,
+                                        size_t ws_bytes, hipStream_t stream) {
+  if (sao_status_t s = check_segments_args(rewards, mask, cu_seqlens, B, T, adv)) return s;
+  if (!traj_reward || !traj_adv || !history || !seen)
+    return fail(SAO_ERR_NULL, "traj_reward, traj_adv, history and seen are required");
+  if (n_keys < 1) return fail(SAO_ERR_SHAPE, "n_keys=%d must be >= 1", (int)n_keys);
+  if (window < 1) return fail(SAO_ERR_SHAPE, "window=%d must be >= 1", (int)window);
+  if (T == 0) return ok();
+  if (sao_status_t s = check_ws(ws, ws_bytes, sao_workspace_size(SAO_OP_RUNNING_MEAN_ADVANTAGE, T, 1, 1, SAO_F32)))
+    return s;
+  return device(sao::launch_running_mean_advantage(rewards, mask, cu_seqlens, B, T, keys, n_keys, window, history,
+                                                   seen, adv, traj_reward, traj_adv, n_tokens, status, ws, stream),
+                "sao_running_mean_advantage launch");
 }
 
 sao_status_t sao_clipped_loss(const float* logp, const float* logp_rollout, const float* adv,

@@ -24,6 +24,16 @@ hipError_t launch_step_advantage(const float* values, const float* rewards, cons
                                  double alpha, bool last_value, float* adv, float* ret, uint8_t* last,
                                  int64_t* n_tokens, int32_t* status, void* ws, hipStream_t st);
 
+hipError_t launch_group_advantage(const float* rewards, const uint8_t* mask, const int32_t* cu_seqlens, int32_t B,
+                                  int64_t T, int32_t group_size, double eps_stab, float* adv, double* traj_reward,
+                                  double* traj_adv, int64_t* n_tokens, int32_t* status, void* ws, hipStream_t st);
+
+hipError_t launch_running_mean_advantage(const float* rewards, const uint8_t* mask, const int32_t* cu_seqlens,
+                                         int32_t B, int64_t T, const int32_t* keys, int32_t n_keys, int32_t window,
+                                         double* history, int64_t* seen, float* adv, double* traj_reward,
+                                         double* traj_adv, int64_t* n_tokens, int32_t* status, void* ws,
+                                         hipStream_t st);
+
 hipError_t launch_loss(const float* logp, const float* logp_rollout, const float* adv, const uint8_t* mask,
                        int64_t T, float eps_low, float eps_high, const int64_t* n_tokens, double* loss,
                        float* g, uint8_t* flags, int64_t* counts, void* ws, hipStream_t st);

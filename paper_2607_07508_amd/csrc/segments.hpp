@@ -24,9 +24,9 @@ __global__ __launch_bounds__(THREADS) void k_check_segments(const int32_t* cu, i
   }
 }
 
-// Malformed segments: block blockIdx.x of B writes NaN advantages and returns
-// (and 0 to `last`, when given) over an even slice of [0, T), and adds that
-// slice's mask count to *n_tokens.
+// Malformed segments: block blockIdx.x of B writes NaN advantages (and NaN
+// returns and 0 to `last`, when given) over an even slice of [0, T), and adds
+// that slice's mask count to *n_tokens.
 template <int THREADS>
 __device__ __forceinline__ void malformed_slice(const uint8_t* mask, int32_t B, int64_t T, float* adv, float* ret,
                                                 uint8_t* last, int64_t* n_tokens) {
@@ -35,7 +35,7 @@ __device__ __forceinline__ void malformed_slice(const uint8_t* mask, int32_t B, 
   int64_t cnt = 0;
   for (int64_t t = lo + threadIdx.x; t < hi; t += THREADS) {
     adv[t] = __builtin_nanf("");
-    ret[t] = __builtin_nanf("");
+    if (ret) ret[t] = __builtin_nanf("");
     if (last) last[t] = 0;
     cnt += mask[t] != 0 ? 1 : 0;
   }

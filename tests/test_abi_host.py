@@ -102,6 +102,30 @@ def test_step_advantage_validation(L):
     assert binding.workspace_size(binding.OP_STEP_ADVANTAGE, 1000, 1, 1, 1) >= 24 * 1000
 
 
+def test_baseline_validation(L):
+    def grp(adv=FAKE, B=8, T=100, G=4, eps=1e-6, tr=FAKE, ws=FAKE, ws_bytes=256):
+        return L.sao_group_advantage(FAKE, FAKE, FAKE, B, T, G, eps, adv, tr, FAKE, None, None, ws, ws_bytes, None)
+    assert grp(adv=None) == ERR_NULL
+    assert grp(tr=None) == ERR_NULL
+    assert grp(G=3) == ERR_SHAPE                 # B not a multiple of the group size
+    assert grp(G=0) == ERR_SHAPE
+    assert grp(eps=-1.0) == ERR_VALUE
+    assert grp(eps=float("inf")) == ERR_VALUE
+    assert grp(ws_bytes=0) == ERR_WORKSPACE
+    assert grp(T=0) == OK
+
+    def rm(hist=FAKE, seen=FAKE, n_keys=2, window=8, B=4, T=100, ws=FAKE, ws_bytes=256):
+        return L.sao_running_mean_advantage(FAKE, FAKE, FAKE, B, T, None, n_keys, window, hist, seen, FAKE, FAKE,
+                                            FAKE, None, None, ws, ws_bytes, None)
+    assert rm(hist=None) == ERR_NULL
+    assert rm(seen=None) == ERR_NULL
+    assert rm(n_keys=0) == ERR_SHAPE
+    assert rm(window=0) == ERR_SHAPE
+    assert rm(B=0) == ERR_SHAPE
+    assert rm(ws=None) == ERR_NULL
+    assert rm(T=0) == OK
+
+
 def test_loss_validation(L):
     def loss(T=10, el=0.2, eh=0.2, g=FAKE, ws=FAKE, ws_bytes=1 << 30):
         return L.sao_clipped_loss(FAKE, FAKE, FAKE, FAKE, T, el, eh, None, FAKE, g, FAKE, FAKE, ws, ws_bytes,
