@@ -114,8 +114,10 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
     (logp, logp_old, logp_behav, adv, mask in; g, flags out), 9 for the
     explained variance (values, ret, mask in), and for the step-level GAE
     (sao_step_advantage, step averages) 14 per token plus 4 per loss-mask token
-    (mask and rewards in, adv, ret and last out; values only on the steps).
-    One JSON line per size."""
+    (mask and rewards in, adv, ret and last out; values only on the steps),
+    and 9 for the critic-free baselines (sao_group_advantage with groups of 8,
+    sao_running_mean_advantage with one 128-reward window: rewards and mask in,
+    adv out). One JSON line per size."""
     import torch
     import paper_2607_07508_amd as sao
     from paper_2607_07508_amd import binding as B
@@ -162,7 +164,8 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
         moments = torch.zeros(5, dtype=torch.float64, device="cuda")
         ev = torch.zeros(1, dtype=torch.float64, device="cuda")
         ws_bytes = max(B.workspace_size(op, T, 1, 1, B.SAO_F32)
-                       for op in (B.OP_ADVANTAGE, B.OP_LOSS, B.OP_PPO_LOSS, B.OP_EXPLAINED_VARIANCE))
+                       for op in (B.OP_ADVANTAGE, B.OP_LOSS, B.OP_PPO_LOSS, B.OP_EXPLAINED_VARIANCE,
+                                  B.OP_GROUP_ADVANTAGE, B.OP_RUNNING_MEAN_ADVANTAGE))
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
         st = torch.cuda.current_stream().cuda_stream
         p = lambda t: t.data_ptr()  # noqa: E731
@@ -187,13 +190,28 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
                                           1.0, 1.5, B.STEP_AVERAGE, p(g_out), p(ret), p(last), p(n), None,
                                           p(step_ws), step_ws.numel(), st))
 
+        traj_r = torch.empty(cfg.B, dtype=torch.float64, device="cuda")
+        traj_a = torch.empty(cfg.B, dtype=torch.float64, device="cuda")
+        hist, seen = torch.zeros(128, dtype=torch.float64, device="cuda"), torch.zeros(1, dtype=torch.int64,
+                                                                                        device="cuda")
+
+        def grpo():
+            B._check(L.sao_group_advantage(p(db.rewards), p(db.mask), p(db.cu_seqlens), cfg.B, T, 8, 1e-6, p(g_out),
+                                           p(traj_r), p(traj_a), p(n), None, p(ws), ws_bytes, st))
+
+        def running_mean():
+            B._check(L.sao_running_mean_advantage(p(db.rewards), p(db.mask), p(db.cu_seqlens), cfg.B, T, None, 1, 128,
+                                                  p(hist), p(seen), p(g_out), p(traj_r), p(traj_a), p(n), None,
+                                                  p(ws), ws_bytes, st))
+
         def explained():
             B._check(L.sao_explained_variance(p(db.values), p(ret), p(db.mask), T, p(moments), p(ev), p(ws), ws_bytes,
                                               st))
         out = {}
         for name, fn, nbytes in (("advantage", scan, 17 * T), ("clipped_loss", epilogue, 18 * T),
                                  ("ppo_loss", surrogate, 22 * T), ("explained_variance", explained, 9 * T),
-                                 ("step_advantage", step_gae, 14 * T + 4 * int(b.mask.sum()))):
+                                 ("step_advantage", step_gae, 14 * T + 4 * int(b.mask.sum())),
+                                 ("group_advantage", grpo, 9 * T), ("running_mean_advantage", running_mean, 9 * T)):
             for _ in range(3):
                 fn()
             torch.cuda.synchronize()
@@ -207,7 +225,7 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
             out[name] = {"ms": ms, "GB/s": nbytes / ms / 1e6, "frac_hbm": nbytes / ms / 1e6 / PEAK_HBM_GBS,
                          "bytes": nbytes}
         print(json.dumps({"mode": "epilogue_sweep", "T": T, "B": cfg.B, **out}), flush=True)
-        del db, b, logp, lro, lbh, adv, ret, g_out, flags, ws, last, step_ws
+        del db, b, logp, lro, lbh, adv, ret, g_out, flags, ws, last, step_ws, traj_r, traj_a, hist, seen
         torch.cuda.empty_cache()
 
 
