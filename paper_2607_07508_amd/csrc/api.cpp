@@ -118,7 +118,7 @@ size_t sao_workspace_size(sao_op_t op, int64_t T, int64_t H, int64_t V, sao_dtyp
     case SAO_OP_LOSS:
       return sao::loss_layout(T).total;
     case SAO_OP_ADVANTAGE:
-      return sao::kAdvantageWorkspace;
+      return sao::advantage_workspace();
     case SAO_OP_VALUE:
       if (H < 1) return 0;
       return sao::value_layout(T, H).total;
@@ -130,7 +130,7 @@ size_t sao_workspace_size(sao_op_t op, int64_t T, int64_t H, int64_t V, sao_dtyp
       return sao::step_layout(T).total;
     case SAO_OP_GROUP_ADVANTAGE:
     case SAO_OP_RUNNING_MEAN_ADVANTAGE:
-      return sao::kAdvantageWorkspace;
+      return sao::advantage_workspace();
   }
   return 0;
 }

@@ -12,6 +12,7 @@
 // trajectory.
 #include "common.hpp"
 #include "launch.hpp"
+#include "layout.hpp"
 #include "reduce.hpp"
 #include "segments.hpp"
 
@@ -161,12 +162,13 @@ __global__ __launch_bounds__(kBaseThreads) void k_seen_update(int32_t B, const i
 }
 
 // adv[t] = A_b on trajectory b's loss-mask tokens, 0 elsewhere (one workgroup per
-// trajectory), and the loss-mask count; NaN everywhere with malformed segments.
+// trajectory), and the loss-mask count into the count slots; NaN everywhere with
+// malformed segments.
 __global__ __launch_bounds__(kBaseThreads) void k_broadcast(const uint8_t* mask, const int32_t* cu, int32_t B,
                                                             int64_t T, const double* A, const int32_t* bad,
-                                                            float* adv, int64_t* n_tokens, bool vec_ok) {
+                                                            float* adv, int64_t* slots, bool vec_ok) {
   if (*bad) {
-    malformed_slice<kBaseThreads>(mask, B, T, adv, nullptr, nullptr, n_tokens);
+    malformed_slice<kBaseThreads, kCountSlots>(mask, B, T, adv, nullptr, nullptr, slots);
     return;
   }
   __shared__ int64_t shi[kBaseThreads / 64];
@@ -188,8 +190,7 @@ __global__ __launch_bounds__(kBaseThreads) void k_broadcast(const uint8_t* mask,
         cnt += m ? 1 : 0;
       });
   cnt = block_sum<kBaseThreads>(cnt, shi);
-  if (threadIdx.x == 0 && n_tokens && cnt)
-    atomicAdd(reinterpret_cast<unsigned long long*>(n_tokens), static_cast<unsigned long long>(cnt));
+  if (threadIdx.x == 0) add_count<kCountSlots>(slots, cnt);
 }
 
 namespace {
@@ -205,15 +206,20 @@ bool span_vec_ok(const float* rewards, const uint8_t* mask, const float* adv) {
 hipError_t launch_group_advantage(const float* rewards, const uint8_t* mask, const int32_t* cu_seqlens, int32_t B,
                                   int64_t T, int32_t group_size, double eps_stab, float* adv, double* traj_reward,
                                   double* traj_adv, int64_t* n_tokens, int32_t* status, void* ws, hipStream_t st) {
-  int32_t* bad = static_cast<int32_t*>(ws);
-  hipLaunchKernelGGL(k_check_segments<256>, dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, n_tokens, status);
+  const SegHead H = seg_head();
+  char* w8 = static_cast<char*>(ws);
+  int32_t* bad = reinterpret_cast<int32_t*>(w8 + H.bad);
+  int64_t* slots = reinterpret_cast<int64_t*>(w8 + H.slots);
+  hipLaunchKernelGGL((k_check_segments<256, kCountSlots>), dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, slots,
+                     status);
   const bool vec_ok = span_vec_ok(rewards, mask, adv);
   hipLaunchKernelGGL(k_traj_reward, dim3(B), dim3(kBaseThreads), 0, st, rewards, cu_seqlens, bad, traj_reward,
                      vec_ok);
   hipLaunchKernelGGL(k_group_adv, dim3(blocks_for(B)), dim3(kBaseThreads), 0, st, traj_reward, B, group_size,
                      eps_stab, traj_adv);
   hipLaunchKernelGGL(k_broadcast, dim3(B), dim3(kBaseThreads), 0, st, mask, cu_seqlens, B, T, traj_adv, bad, adv,
-                     n_tokens, vec_ok);
+                     slots, vec_ok);
+  if (n_tokens) hipLaunchKernelGGL(k_slots_total<kCountSlots>, dim3(1), dim3(64), 0, st, slots, n_tokens);
   return hipGetLastError();
 }
 
@@ -222,8 +228,12 @@ hipError_t launch_running_mean_advantage(const float* rewards, const uint8_t* ma
                                          double* history, int64_t* seen, float* adv, double* traj_reward,
                                          double* traj_adv, int64_t* n_tokens, int32_t* status, void* ws,
                                          hipStream_t st) {
-  int32_t* bad = static_cast<int32_t*>(ws);
-  hipLaunchKernelGGL(k_check_segments<256>, dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, n_tokens, status);
+  const SegHead H = seg_head();
+  char* w8 = static_cast<char*>(ws);
+  int32_t* bad = reinterpret_cast<int32_t*>(w8 + H.bad);
+  int64_t* slots = reinterpret_cast<int64_t*>(w8 + H.slots);
+  hipLaunchKernelGGL((k_check_segments<256, kCountSlots>), dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, slots,
+                     status);
   const bool vec_ok = span_vec_ok(rewards, mask, adv);
   hipLaunchKernelGGL(k_traj_reward, dim3(B), dim3(kBaseThreads), 0, st, rewards, cu_seqlens, bad, traj_reward,
                      vec_ok);
@@ -233,7 +243,8 @@ hipError_t launch_running_mean_advantage(const float* rewards, const uint8_t* ma
                      window, history, seen, bad);
   hipLaunchKernelGGL(k_seen_update, dim3(blocks_for(n_keys)), dim3(kBaseThreads), 0, st, B, keys, n_keys, seen, bad);
   hipLaunchKernelGGL(k_broadcast, dim3(B), dim3(kBaseThreads), 0, st, mask, cu_seqlens, B, T, traj_adv, bad, adv,
-                     n_tokens, vec_ok);
+                     slots, vec_ok);
+  if (n_tokens) hipLaunchKernelGGL(k_slots_total<kCountSlots>, dim3(1), dim3(64), 0, st, slots, n_tokens);
   return hipGetLastError();
 }
 

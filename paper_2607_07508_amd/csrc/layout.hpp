@@ -100,8 +100,24 @@ inline BackwardLayout backward_layout(int64_t T, int64_t H, int64_t V, size_t es
   return L;
 }
 
-// sao_advantage: one int32 flag (segments malformed)
-constexpr size_t kAdvantageWorkspace = 256;
+// Head of every advantage kernel's workspace: the int32 segments flag, then
+// kCountSlots int64 slots that spread the loss-mask count's atomic adds (one
+// slot per workgroup, modulo kCountSlots) before a one-block total.
+constexpr int kCountSlots = 64;
+struct SegHead {
+  size_t bad, slots, total;
+};
+inline SegHead seg_head() {
+  SegHead H{};
+  Carve c;
+  H.bad = c.take(4);
+  H.slots = c.take(8 * kCountSlots);
+  H.total = c.off;
+  return H;
+}
+
+// sao_advantage needs only the head.
+inline size_t advantage_workspace() { return seg_head().total; }
 
 // sao_clipped_loss
 struct LossLayout {
@@ -123,17 +139,17 @@ inline LossLayout loss_layout(int64_t T) {
   return L;
 }
 
-// sao_step_advantage: the segments flag, then a step table of T entries (a
-// trajectory's steps sit at its own token offset): start and end (int32), and
-// two doubles (the step's value and reward, later its advantage and return).
+// sao_step_advantage: the head, then a step table of T entries (a trajectory's
+// steps sit at its own token offset): start and end (int32), and two doubles
+// (the step's value and reward, later its advantage and return).
 struct StepLayout {
-  size_t bad, tab_a, tab_z, tab_v, tab_r, total;
+  size_t tab_a, tab_z, tab_v, tab_r, total;
 };
 
 inline StepLayout step_layout(int64_t T) {
   StepLayout L{};
   Carve c;
-  L.bad = c.take(4);
+  c.take(seg_head().total);
   L.tab_a = c.take(4 * static_cast<size_t>(T));
   L.tab_z = c.take(4 * static_cast<size_t>(T));
   L.tab_v = c.take(8 * static_cast<size_t>(T));
@@ -141,6 +157,8 @@ inline StepLayout step_layout(int64_t T) {
   L.total = c.off;
   return L;
 }
+
+// sao_group_advantage / sao_running_mean_advantage need only the head.
 
 // sao_ppo_loss shares the loss layout.
 

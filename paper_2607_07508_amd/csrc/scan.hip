@@ -19,6 +19,7 @@
 // 8 tokens that it reads and writes with 16-byte vector accesses.
 #include "common.hpp"
 #include "launch.hpp"
+#include "layout.hpp"
 #include "segments.hpp"
 
 #include "../../include/sao.h"
@@ -135,7 +136,7 @@ __device__ __forceinline__ St apply(const Aff& M, const St& s) {
 // and each thread replays its tokens from the exact entering state.
 __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_advantage(
     const float* values, const float* rewards, const uint8_t* mask, const int32_t* cu, int32_t B,
-    int64_t T, double gamma, double lam, double alpha, float* adv, float* ret, int64_t* n_tokens,
+    int64_t T, double gamma, double lam, double alpha, float* adv, float* ret, int64_t* slots,
     const int32_t* bad, bool vec_ok) {
   __shared__ Aff s_agg[kScanThreads / 64];
   __shared__ int64_t s_cnt[kScanThreads / 64];
@@ -143,7 +144,7 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
   if (*bad) {
-    malformed_slice<kScanThreads>(mask, B, T, adv, ret, nullptr, n_tokens);
+    malformed_slice<kScanThreads, kCountSlots>(mask, B, T, adv, ret, nullptr, slots);
     return;
   }
   const int64_t s = cu[b], e = cu[b + 1];
@@ -268,10 +269,10 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
   __syncthreads();
   if (lane == 0) s_cnt[wave] = wcnt;
   __syncthreads();
-  if (tid == 0 && n_tokens) {
+  if (tid == 0) {
     int64_t tot = 0;
     for (int w = 0; w < kScanThreads / 64; ++w) tot += s_cnt[w];
-    atomicAdd(reinterpret_cast<unsigned long long*>(n_tokens), static_cast<unsigned long long>(tot));
+    add_count<kCountSlots>(slots, tot);
   }
 }
 
@@ -279,14 +280,19 @@ hipError_t launch_advantage(const float* values, const float* rewards, const uin
                             const int32_t* cu_seqlens, int32_t B, int64_t T, double gamma, double lam,
                             double alpha, float* adv, float* ret, int64_t* n_tokens, int32_t* status,
                             void* ws, hipStream_t st) {
-  int32_t* bad = static_cast<int32_t*>(ws);
-  hipLaunchKernelGGL(k_check_segments<256>, dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, n_tokens, status);
+  const SegHead H = seg_head();
+  char* w8 = static_cast<char*>(ws);
+  int32_t* bad = reinterpret_cast<int32_t*>(w8 + H.bad);
+  int64_t* slots = reinterpret_cast<int64_t*>(w8 + H.slots);
+  hipLaunchKernelGGL((k_check_segments<256, kCountSlots>), dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, slots,
+                     status);
   // Vector access needs 16-byte aligned float arrays and an 8-byte aligned mask.
   const uintptr_t f = reinterpret_cast<uintptr_t>(values) | reinterpret_cast<uintptr_t>(rewards) |
                       reinterpret_cast<uintptr_t>(adv) | reinterpret_cast<uintptr_t>(ret);
   const bool vec_ok = (f & 15u) == 0 && (reinterpret_cast<uintptr_t>(mask) & 7u) == 0;
   hipLaunchKernelGGL(k_advantage, dim3(B), dim3(kScanThreads), 0, st, values, rewards, mask, cu_seqlens,
-                     B, T, gamma, lam, alpha, adv, ret, n_tokens, bad, vec_ok);
+                     B, T, gamma, lam, alpha, adv, ret, slots, bad, vec_ok);
+  if (n_tokens) hipLaunchKernelGGL(k_slots_total<kCountSlots>, dim3(1), dim3(64), 0, st, slots, n_tokens);
   return hipGetLastError();
 }
 

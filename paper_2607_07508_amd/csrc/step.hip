@@ -95,7 +95,7 @@ __device__ __forceinline__ Seg block_segmented_scan(const Seg& x, const Seg& car
 __global__ __launch_bounds__(kStepThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_step_advantage(
     const float* values, const float* rewards, const uint8_t* mask, const int32_t* cu, int32_t B, int64_t T,
     double gamma, double lam, double alpha, bool last_value, float* adv, float* ret, uint8_t* last,
-    int64_t* n_tokens, const int32_t* bad, int32_t* tab_a, int32_t* tab_z, double* tab_v, double* tab_r,
+    int64_t* slots, const int32_t* bad, int32_t* tab_a, int32_t* tab_z, double* tab_v, double* tab_r,
     bool vec_ok) {
   __shared__ int s_scan[kStepThreads / 64];
   __shared__ Seg s_seg[kStepThreads / 64];
@@ -105,7 +105,7 @@ __global__ __launch_bounds__(kStepThreads) __attribute__((amdgpu_waves_per_eu(4)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
   if (*bad) {
-    malformed_slice<kStepThreads>(mask, B, T, adv, ret, last, n_tokens);
+    malformed_slice<kStepThreads, kCountSlots>(mask, B, T, adv, ret, last, slots);
     return;
   }
   const int64_t s = cu[b], e = cu[b + 1];
@@ -277,10 +277,10 @@ __global__ __launch_bounds__(kStepThreads) __attribute__((amdgpu_waves_per_eu(4)
   __syncthreads();
   if (lane == 0) s_cnt[wave] = wcnt;
   __syncthreads();
-  if (tid == 0 && n_tokens) {
+  if (tid == 0) {
     int64_t tot = 0;
     for (int w = 0; w < kStepThreads / 64; ++w) tot += s_cnt[w];
-    atomicAdd(reinterpret_cast<unsigned long long*>(n_tokens), static_cast<unsigned long long>(tot));
+    add_count<kCountSlots>(slots, tot);
   }
 }
 
@@ -290,15 +290,19 @@ hipError_t launch_step_advantage(const float* values, const float* rewards, cons
                                  int64_t* n_tokens, int32_t* status, void* ws, hipStream_t st) {
   const StepLayout Ly = step_layout(T);
   char* w8 = static_cast<char*>(ws);
-  int32_t* bad = reinterpret_cast<int32_t*>(w8 + Ly.bad);
-  hipLaunchKernelGGL(k_check_segments<256>, dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, n_tokens, status);
+  const SegHead H = seg_head();
+  int32_t* bad = reinterpret_cast<int32_t*>(w8 + H.bad);
+  int64_t* slots = reinterpret_cast<int64_t*>(w8 + H.slots);
+  hipLaunchKernelGGL((k_check_segments<256, kCountSlots>), dim3(1), dim3(256), 0, st, cu_seqlens, B, T, bad, slots,
+                     status);
   // Whole in-trajectory blocks of 8 tokens use vector loads when the bases allow them.
   const bool vec_ok = ((reinterpret_cast<uintptr_t>(values) | reinterpret_cast<uintptr_t>(rewards)) & 15u) == 0 &&
                       (reinterpret_cast<uintptr_t>(mask) & 7u) == 0;
   hipLaunchKernelGGL(k_step_advantage, dim3(B), dim3(kStepThreads), 0, st, values, rewards, mask, cu_seqlens, B, T,
-                     gamma, lam, alpha, last_value, adv, ret, last, n_tokens, bad,
+                     gamma, lam, alpha, last_value, adv, ret, last, slots, bad,
                      reinterpret_cast<int32_t*>(w8 + Ly.tab_a), reinterpret_cast<int32_t*>(w8 + Ly.tab_z),
                      reinterpret_cast<double*>(w8 + Ly.tab_v), reinterpret_cast<double*>(w8 + Ly.tab_r), vec_ok);
+  if (n_tokens) hipLaunchKernelGGL(k_slots_total<kCountSlots>, dim3(1), dim3(64), 0, st, slots, n_tokens);
   return hipGetLastError();
 }
 

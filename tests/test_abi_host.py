@@ -203,7 +203,7 @@ def test_value_validation(L):
 
 def test_workspace_sizes(L):
     ws = binding.workspace_size
-    assert ws(binding.OP_ADVANTAGE, 1000, 1, 1, 0) == 256
+    assert ws(binding.OP_ADVANTAGE, 1000, 1, 1, 0) == 768     # segments flag + 64 count slots
     assert ws(binding.OP_LOGPROB, 0, 2048, 151936, 0) == 0
     assert ws(binding.OP_LOGPROB, -1, 2048, 151936, 0) == 0
     small = ws(binding.OP_LOGPROB, 1000, 64, 1000, 1)
