@@ -94,3 +94,85 @@ def test_captured_step_replays_match_eager():
         for k in out:
             assert torch.equal(got[k], eager[k]), (i, k)
         say(f"replay {i}: identical to the eager step")
+
+
+def test_captured_comparison_and_baselines_replay_match_eager():
+    """The clipped surrogate, explained variance, step-level GAE and both critic-free
+    baselines, captured in one graph. The running-mean state is restored eagerly before
+    each replay, so every replay starts from the same history."""
+    cfg = small_config("graph2", 52, B=8, T=4000, H=8, V=8)
+    say(f"case {cfg.name}: T={cfg.T} B={cfg.B}")
+    b = generate(cfg, with_head=False)
+    from synth import comparison_logprobs
+    lp, lold, lb = comparison_logprobs(cfg, b.T)
+    dev = torch.device("cuda")
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)  # noqa: E731
+    values, rewards, mask, cu = t(b.values), t(b.rewards), t(b.mask), t(b.cu_seqlens)
+    lp_d, lold_d, lb_d = t(lp), t(lold), t(lb)
+    T, Bn = b.T, cfg.B
+    L = sao.lib()
+    f32 = dict(dtype=torch.float32, device=dev)
+    f64 = dict(dtype=torch.float64, device=dev)
+    out = dict(adv=torch.empty(T, **f32), ret=torch.empty(T, **f32), n=torch.zeros(1, dtype=torch.int64, device=dev),
+               g=torch.empty(T, **f32), flags=torch.empty(T, dtype=torch.uint8, device=dev),
+               loss=torch.zeros(1, **f64), counts=torch.zeros(5, dtype=torch.int64, device=dev),
+               mom=torch.zeros(5, **f64), ev=torch.zeros(1, **f64),
+               sadv=torch.empty(T, **f32), sret=torch.empty(T, **f32), last=torch.empty(T, dtype=torch.uint8, device=dev),
+               gadv=torch.empty(T, **f32), gR=torch.empty(Bn, **f64), gA=torch.empty(Bn, **f64),
+               radv=torch.empty(T, **f32), rR=torch.empty(Bn, **f64), rA=torch.empty(Bn, **f64))
+    hist0 = torch.rand((2, 4), **f64)
+    seen0 = torch.tensor([3, 9], dtype=torch.int64, device=dev)
+    hist, seen = hist0.clone(), seen0.clone()
+    keys = t((np.arange(Bn) % 2).astype(np.int32))
+    ws_bytes = max(B.workspace_size(op, T, 1, 1, B.SAO_F32) for op in
+                   (B.OP_ADVANTAGE, B.OP_PPO_LOSS, B.OP_EXPLAINED_VARIANCE, B.OP_STEP_ADVANTAGE,
+                    B.OP_GROUP_ADVANTAGE, B.OP_RUNNING_MEAN_ADVANTAGE))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    p = lambda x: x.data_ptr()  # noqa: E731
+    o = out
+
+    def step():
+        st = torch.cuda.current_stream().cuda_stream
+        for k in ("loss", "counts", "mom"):
+            o[k].zero_()
+        B._check(L.sao_advantage(p(values), p(rewards), p(mask), p(cu), Bn, T, 1.0, 1.0, 1.5, p(o["adv"]),
+                                 p(o["ret"]), p(o["n"]), None, p(ws), ws_bytes, st))
+        B._check(L.sao_ppo_loss(p(lp_d), p(lold_d), p(lb_d), p(o["adv"]), p(mask), T, 0.2, 0.28, p(o["n"]),
+                                p(o["loss"]), p(o["g"]), p(o["flags"]), p(o["counts"]), p(ws), ws_bytes, st))
+        B._check(L.sao_explained_variance(p(values), p(o["ret"]), p(mask), T, p(o["mom"]), p(o["ev"]), p(ws),
+                                          ws_bytes, st))
+        B._check(L.sao_step_advantage(p(values), p(rewards), p(mask), p(cu), Bn, T, 1.0, 1.0, 1.5, B.STEP_LAST,
+                                      p(o["sadv"]), p(o["sret"]), p(o["last"]), None, None, p(ws), ws_bytes, st))
+        B._check(L.sao_group_advantage(p(rewards), p(mask), p(cu), Bn, T, 4, 1e-6, p(o["gadv"]), p(o["gR"]),
+                                       p(o["gA"]), None, None, p(ws), ws_bytes, st))
+        B._check(L.sao_running_mean_advantage(p(rewards), p(mask), p(cu), Bn, T, p(keys), 2, 4, p(hist), p(seen),
+                                              p(o["radv"]), p(o["rR"]), p(o["rA"]), None, None, p(ws), ws_bytes, st))
+
+    def snapshot():
+        torch.cuda.synchronize()
+        return {k: v.clone() for k, v in list(out.items()) + [("hist", hist), ("seen", seen)]}
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    hist.copy_(hist0)
+    seen.copy_(seen0)
+    step()
+    eager = snapshot()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for i in range(3):
+        for v in out.values():
+            v.fill_(7)
+        hist.copy_(hist0)
+        seen.copy_(seen0)
+        junk = torch.randn(1 << 20, device=dev).sum()
+        graph.replay()
+        got = snapshot()
+        del junk
+        for k in eager:
+            assert torch.equal(got[k], eager[k]), (i, k)
+        say(f"replay {i}: identical to the eager calls")
