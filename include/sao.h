@@ -5,7 +5,10 @@
  * double-sided importance sampling (DIS): per-token log-probs of the LM head,
  * skip-observation GAE advantages, the DIS ratio against the rollout engine's
  * log-probs with a strict two-sided token mask, a token-level mean, and the
- * backward into the hidden states and the head weights.
+ * backward into the hidden states and the head weights. Next to it are the
+ * objectives and estimators the paper compares DIS and the critic with (the
+ * clipped PPO surrogate and its decoupled form, step-level GAE, GRPO's group
+ * normalisation, a running-mean baseline) and the critic's explained variance.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -39,12 +42,14 @@
  *           T == 0 is a no-op that returns SAO_OK.
  *           Data errors visible only on the device (a target outside [0,V),
  *           cu_seqlens not non-decreasing or not ending at T, a non-finite
- *           log-sum-exp) OR bits into the optional device word `*status`
+ *           log-sum-exp, a running-mean key out of range) OR bits into the
+ *           optional device word `*status`
  *           (SAO_STATUS_*) without a host synchronisation; the affected outputs
  *           are NaN rather than silently valid.
  * Accumulation.  Outputs documented as "+=" accumulate so that chunked calls sum
- *           to the whole batch; the caller zeroes them. All other outputs are
- *           overwritten.
+ *           to the whole batch; the caller zeroes them. The explained-variance
+ *           moments and the running-mean history are in/out states that a call
+ *           combines with or advances. All other outputs are overwritten.
  *
  * Citations name sections and equations of "Single-Rollout Asynchronous
  * Optimization for Agentic Reinforcement Learning" (arXiv 2607.07508).
