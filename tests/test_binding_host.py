@@ -54,3 +54,31 @@ def test_head_calls_reject_host_tensors_and_mismatched_shapes():
         sao.token_logprob(h, w.to(torch.bfloat16), tgt)
     with pytest.raises(ValueError):       # H differs
         sao.loss_backward(h, torch.zeros(10, 8), tgt, torch.zeros(8), torch.zeros(8))
+
+
+def test_comparison_and_estimator_calls_reject_bad_arrays():
+    T = 32
+    lp = torch.zeros(T, dtype=torch.float32)
+    mask = torch.ones(T, dtype=torch.uint8)
+    with pytest.raises(TypeError):        # the decoupled weight's log-probs must be float32
+        sao.ppo_loss(lp, lp, lp, mask, 0.2, 0.28, logp_behav=torch.zeros(T, dtype=torch.float64))
+    with pytest.raises(ValueError):
+        sao.ppo_loss(lp, lp, torch.zeros(T - 1), mask, 0.2, 0.28)
+    with pytest.raises(TypeError):
+        sao.explained_variance(lp, lp, mask, moments=torch.zeros(5, dtype=torch.float32))
+    with pytest.raises(ValueError):
+        sao.explained_variance(lp, lp, mask, moments=torch.zeros(4, dtype=torch.float64))
+    values, rewards, mask, cu = _adv_args()
+    with pytest.raises(ValueError):       # only "average" and "last"
+        sao.step_advantage(values, rewards, mask, cu, step_value="median")
+    with pytest.raises(TypeError):
+        sao.step_advantage(values, rewards, mask.to(torch.int32), cu)
+    with pytest.raises(TypeError):
+        sao.group_advantage(rewards.double(), mask, cu, 2, 1e-6)
+    history, seen = torch.zeros(3, 8, dtype=torch.float64), torch.zeros(3, dtype=torch.int64)
+    with pytest.raises(ValueError):       # history is [n_keys, window]
+        sao.running_mean_advantage(rewards, mask, cu, history.flatten(), seen)
+    with pytest.raises(ValueError):
+        sao.running_mean_advantage(rewards, mask, cu, history, seen[:2])
+    with pytest.raises(TypeError):
+        sao.running_mean_advantage(rewards, mask, cu, history, seen, keys=torch.zeros(2, dtype=torch.int64))
