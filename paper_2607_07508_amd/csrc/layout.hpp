@@ -55,12 +55,14 @@ struct BackwardLayout {
   size_t blk_counts, count, idx, pos, g_c, lse_c, y_c, hg, dh, dz, total;
 };
 
-// K pieces of the dH product: enough that its output tiles (host bound) number
-// at least 512 (two per CU), at most 4.
-constexpr int kMaxDhPieces = 4;
+// K pieces of the dH product: enough that its output tiles number at least 1024
+// (four per CU) at the host bound of token rows, at most 8. Typically about a
+// third of a chunk's rows carry a gradient, so this leaves a short chunk's dH
+// launch with about one tile per CU.
+constexpr int kMaxDhPieces = 8;
 inline int dh_pieces(int64_t T, int64_t H) {
   const int64_t tiles = ceil_div(T, kTile) * ceil_div(H, kTile);
-  int64_t p = ceil_div(512, tiles);
+  int64_t p = ceil_div(1024, tiles);
   if (p < 1) p = 1;
   if (p > kMaxDhPieces) p = kMaxDhPieces;
   return static_cast<int>(p);
