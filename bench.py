@@ -19,6 +19,7 @@ the fp64 oracle timed on this host's cores over a bounded sample of the batch.
 from __future__ import annotations
 
 import argparse
+import contextlib
 import json
 import os
 import sys
@@ -229,6 +230,45 @@ def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
         torch.cuda.empty_cache()
 
 
+def breakdown(step, T, H, V, esz, t_act, t_grad, torch, repeats=3):
+    """`repeats` more steps, after the timed ones, with each library call bracketed
+    by events on the launch stream: per-call device time (summed over chunks, the
+    median over the repeats) and its rate against the roofline that bounds it.
+    Not part of `value`."""
+    runs = []
+    for _ in range(repeats):
+        spans = {}
+
+        @contextlib.contextmanager
+        def span(name):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            yield
+            b.record()
+            spans.setdefault(name, []).append((a, b))
+
+        step(span=span)
+        torch.cuda.synchronize()
+        runs.append({k: sum(a.elapsed_time(b) for a, b in v) for k, v in spans.items()})
+    ms = {k: float(np.median([r[k] for r in runs])) for k in runs[0]}
+    # bytes: the per-token arrays, and for the critic the hidden rows read (and dH_v written)
+    hbm = {"advantage": 17.0 * T, "clipped_loss": 18.0 * T, "value_forward": esz * T * H + 4.0 * T,
+           "value_loss": 2.0 * esz * T * H + 13.0 * T}
+    flops = {"token_logprob": 2.0 * t_act * V * H,
+             "loss_backward": 6.0 * t_grad * V * H}   # logits recomputed, dH, dW
+    out = {}
+    for k, t in ms.items():
+        row = {"ms": t}
+        if k in flops:
+            row.update({"TFLOP/s": flops[k] / (t * 1e-3) / 1e12, "frac": flops[k] / (t * 1e-3) / 1e12 /
+                        PEAK_BF16_TFLOPS, "bound": "mfma"})
+        elif k in hbm:
+            row.update({"GB/s": hbm[k] / (t * 1e-3) / 1e9, "frac": hbm[k] / (t * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                        "bound": "hbm"})
+        out[k] = row
+    return out
+
+
 def log(msg):
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
@@ -342,7 +382,10 @@ def main():
     p = lambda t: t.data_ptr()  # noqa: E731
     fwd_pairs = []   # event pairs bracketing the head-forward launches of the timed steps
 
-    def step(timed_pairs=None):
+    def no_span(name):
+        return contextlib.nullcontext()
+
+    def step(timed_pairs=None, span=no_span):
         loss.zero_()
         counts.zero_()
         if cfg.backward:
@@ -351,28 +394,34 @@ def main():
         if cfg.value_head:
             loss_v.zero_()
             dw_v.zero_()
-            B._check(L.sao_value_forward(p(db.hidden), H, p(db.w_value), T, H, dt, p(v_out), None, 0, st))
+            with span("value_forward"):
+                B._check(L.sao_value_forward(p(db.hidden), H, p(db.w_value), T, H, dt, p(v_out), None, 0, st))
             values = v_out
-        B._check(L.sao_advantage(p(values), p(db.rewards), p(db.mask), p(db.cu_seqlens), cfg.B, T,
-                                 cfg.gamma, cfg.lam, cfg.alpha, p(adv), p(ret), p(n_tok), None, p(ws), ws_bytes,
-                                 st))
+        with span("advantage"):
+            B._check(L.sao_advantage(p(values), p(db.rewards), p(db.mask), p(db.cu_seqlens), cfg.B, T,
+                                     cfg.gamma, cfg.lam, cfg.alpha, p(adv), p(ret), p(n_tok), None, p(ws),
+                                     ws_bytes, st))
         if cfg.value_head:
-            B._check(L.sao_value_loss(p(db.hidden), H, p(db.w_value), p(v_out), p(ret), p(db.mask), T, H,
-                                      p(n_tok), dt, p(loss_v), p(dhid_v), p(dw_v), p(ws), ws_bytes, st))
+            with span("value_loss"):
+                B._check(L.sao_value_loss(p(db.hidden), H, p(db.w_value), p(v_out), p(ret), p(db.mask), T, H,
+                                          p(n_tok), dt, p(loss_v), p(dhid_v), p(dw_v), p(ws), ws_bytes, st))
         for i, (s0, e0) in enumerate(chunks):
             n = e0 - s0
             if timed_pairs is not None:
                 B.time_kernel(B.KERNEL_HEAD_FORWARD, *timed_pairs[i])
-            B._check(L.sao_token_logprob(p(db.hidden) + s0 * H * esz, H, p(db.w_head), H, p(db.target) + 4 * s0,
-                                         p(db.mask) + s0, n, H, V, dt, p(logp) + 4 * s0, p(lse) + 4 * s0, None,
-                                         p(ws), ws_bytes, st))
-            B._check(L.sao_clipped_loss(p(logp) + 4 * s0, p(db.logp_rollout) + 4 * s0, p(adv) + 4 * s0,
-                                        p(db.mask) + s0, n, cfg.eps_low, cfg.eps_high, p(n_tok), p(loss),
-                                        p(g) + 4 * s0, p(flags) + s0, p(counts), p(ws), ws_bytes, st))
+            with span("token_logprob"):
+                B._check(L.sao_token_logprob(p(db.hidden) + s0 * H * esz, H, p(db.w_head), H,
+                                             p(db.target) + 4 * s0, p(db.mask) + s0, n, H, V, dt, p(logp) + 4 * s0,
+                                             p(lse) + 4 * s0, None, p(ws), ws_bytes, st))
+            with span("clipped_loss"):
+                B._check(L.sao_clipped_loss(p(logp) + 4 * s0, p(db.logp_rollout) + 4 * s0, p(adv) + 4 * s0,
+                                            p(db.mask) + s0, n, cfg.eps_low, cfg.eps_high, p(n_tok), p(loss),
+                                            p(g) + 4 * s0, p(flags) + s0, p(counts), p(ws), ws_bytes, st))
             if cfg.backward:
-                B._check(L.sao_loss_backward(p(db.hidden) + s0 * H * esz, H, p(db.w_head), H,
-                                             p(db.target) + 4 * s0, p(lse) + 4 * s0, p(g) + 4 * s0, n, H, V, dt,
-                                             p(dhid) + s0 * H * esz, p(dw), p(ws), ws_bytes, st))
+                with span("loss_backward"):
+                    B._check(L.sao_loss_backward(p(db.hidden) + s0 * H * esz, H, p(db.w_head), H,
+                                                 p(db.target) + 4 * s0, p(lse) + 4 * s0, p(g) + 4 * s0, n, H, V,
+                                                 dt, p(dhid) + s0 * H * esz, p(dw), p(ws), ws_bytes, st))
         if timed_pairs is not None:
             B.time_kernel(B.KERNEL_NONE, None, None)
 
@@ -437,6 +486,7 @@ def main():
                    "arch": getattr(torch.cuda.get_device_properties(dev), "gcnArchName", ""),
                    "compute_units": torch.cuda.get_device_properties(dev).multi_processor_count},
     }
+    out["breakdown"] = breakdown(step, T, H, V, esz, t_act, t_grad, torch)
     if args.vendor_gemm:
         log("vendor GEMM (context)")
         out["vendor_gemm_context"] = vendor_gemm(db, t_act, torch)
