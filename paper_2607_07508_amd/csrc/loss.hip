@@ -106,13 +106,15 @@ __device__ __forceinline__ uint8_t ppo_token(bool active, float lpf, float loldf
   else
     f = SAO_FLAG_USED;
   ++acc.c[f];
-  if (f != SAO_FLAG_NONFINITE && N > 0) {
-    const double w = kWeighted ? exp(e) : 1.0;
-    const double r = f == SAO_FLAG_USED ? exp(d) : (f == SAO_FLAG_HIGH ? bd.hi : bd.lo);
-    const double term = w * (r * A);
-    acc.sL += term;
-    if (f == SAO_FLAG_USED) g = static_cast<float>(-term * invN);
-  }
+  // Both exponentials are evaluated on every lane and the results selected, so
+  // the wave does not branch on the flag.
+  const double w = kWeighted ? exp(e) : 1.0;
+  const double rd = exp(d);
+  const double r = f == SAO_FLAG_USED ? rd : (f == SAO_FLAG_HIGH ? bd.hi : bd.lo);
+  const double term = w * (r * A);
+  const bool counted = f != SAO_FLAG_NONFINITE && N > 0;
+  acc.sL += counted ? term : 0.0;
+  if (counted && f == SAO_FLAG_USED) g = static_cast<float>(-term * invN);
   return f;
 }
 
