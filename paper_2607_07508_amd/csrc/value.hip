@@ -96,18 +96,32 @@ __global__ __launch_bounds__(kValueThreads) void k_value_rows(
   widen(reinterpret_cast<const v4u*>(w)[c], wf, E{});
 #pragma unroll
   for (int e = 0; e < P; ++e) acc[e] = 0.0f;
-  for (int i = 0; i < nrows; ++i) {
-    const float d = s_dv[i];
-    const int64_t t = r0 + i;
-    float o[P];
+  // Rows in groups of four: the four rows' hidden chunks are loaded before any
+  // is used, so that four loads are in flight per thread (rows with dv = 0 are
+  // not read; their dH_v chunk is zero).
+  for (int i0 = 0; i0 < nrows; i0 += 4) {
+    v4u hr[4];
+    float dd[4];
 #pragma unroll
-    for (int e = 0; e < P; ++e) o[e] = d == 0.0f ? 0.0f : d * wf[e];
-    reinterpret_cast<v4u*>(dhidden + t * H)[c] = narrow(o, E{});
-    if (d != 0.0f) {  // uniform over the block
-      float h[P];
-      widen(reinterpret_cast<const v4u*>(hidden + t * ld)[c], h, E{});
+    for (int u = 0; u < 4; ++u) {
+      dd[u] = i0 + u < nrows ? s_dv[i0 + u] : 0.0f;
+      if (dd[u] != 0.0f)  // uniform over the block
+        hr[u] = reinterpret_cast<const v4u*>(hidden + (r0 + i0 + u) * ld)[c];
+    }
 #pragma unroll
-      for (int e = 0; e < P; ++e) acc[e] = fmaf(d, h[e], acc[e]);
+    for (int u = 0; u < 4; ++u) {
+      if (i0 + u >= nrows) break;
+      const float d = dd[u];
+      float o[P];
+#pragma unroll
+      for (int e = 0; e < P; ++e) o[e] = d == 0.0f ? 0.0f : d * wf[e];
+      reinterpret_cast<v4u*>(dhidden + (r0 + i0 + u) * H)[c] = narrow(o, E{});
+      if (d != 0.0f) {
+        float h[P];
+        widen(hr[u], h, E{});
+#pragma unroll
+        for (int e = 0; e < P; ++e) acc[e] = fmaf(d, h[e], acc[e]);
+      }
     }
   }
   float* out = part_dw + static_cast<int64_t>(blockIdx.x) * H + c * P;
