@@ -142,3 +142,26 @@ def test_running_mean_key_out_of_range_and_malformed_segments():
     adv, ta, tr, n = sao.group_advantage(_t(rewards), _t(b.mask), _t(bad), 4, 1e-6, status=status)
     torch.cuda.synchronize()
     assert torch.isnan(adv).all() and torch.isnan(ta).all() and torch.isnan(tr).all()
+
+
+def test_loss_mask_count_with_many_trajectories():
+    """Thousands of workgroups add their loss-mask counts into the shared count slots:
+    every advantage entry point still reports N exactly, and the advantages match."""
+    b = generate(small_config("many", 138, B=5000, T=120000, H=8, V=8))
+    N = int(b.mask.sum())
+    args = (_t(b.values), _t(b.rewards), _t(b.mask), _t(b.cu_seqlens))
+    adv, ret, n = sao.advantage(*args, 1.0, 0.9, 1.5)
+    sadv, sret, last, sn = sao.step_advantage(*args, 1.0, 0.9, 1.5, "average")
+    gadv, ga, gr, gn = sao.group_advantage(_t(b.rewards), _t(b.mask), _t(b.cu_seqlens), 8, 1e-6)
+    history, seen = sao.running_mean_state(1, 128, "cuda")
+    radv, ra, rr, rn = sao.running_mean_advantage(_t(b.rewards), _t(b.mask), _t(b.cu_seqlens), history, seen)
+    torch.cuda.synchronize()
+    assert [int(x.item()) for x in (n, sn, gn, rn)] == [N] * 4
+    r_adv, r_ret, r_n = oracle.advantage(b.values, b.rewards, b.mask, b.cu_seqlens, 1.0, 0.9, 1.5)
+    _check_tokens(adv, r_adv)
+    s_adv, s_ret, s_last, _ = oracle.step_advantage(b.values, b.rewards, b.mask, b.cu_seqlens, 1.0, 0.9, 1.5,
+                                                    "average")
+    _check_tokens(sadv, s_adv)
+    assert np.array_equal(last.cpu().numpy(), s_last)
+    _close(ga.cpu().numpy(), oracle.group_advantage(b.rewards, b.mask, b.cu_seqlens, 8, 1e-6)[1])
+    _close(ra.cpu().numpy(), oracle.running_mean_advantage(b.rewards, b.mask, b.cu_seqlens, 128)[1])
