@@ -4,7 +4,6 @@ and rejects invalid arguments synchronously before any device work.
 No call here reaches a kernel launch: every case fails validation or is the
 T == 0 no-op, so the pointers passed are never dereferenced.
 """
-import ctypes
 import os
 import re
 

@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import paper_2607_07508_amd as sao
-from synth import CONFIGS, bf16_bits, bf16_round, generate, rollout_logprobs, small_config, with_overrides
+from synth import CONFIGS, bf16_bits, bf16_round, generate, small_config, with_overrides
 from synth.device import to_device
 from tests.gpu_common import (TOL_LOGP, TOL_LOSS, TOL_V, check_grad, compare_all, gpu_pass, oracle_pass, say)
 
