@@ -218,7 +218,9 @@ sao_status_t sao_group_advantage(const float* rewards, const uint8_t* mask, cons
  * outside [0, n_keys) sets SAO_STATUS_KEY_RANGE, gives that trajectory NaN and
  * pushes nothing for it. traj_reward and traj_adv are float64 [B] outputs
  * (required); n_tokens, status and the segment checks follow sao_advantage
- * (malformed segments: NaN outputs, history untouched).
+ * (malformed segments: NaN outputs, history untouched). With keys, finding a
+ * trajectory's earlier same-key trajectories scans the batch, so the work grows
+ * as B^2 / 64 per call (negligible for batches of rollouts, B in the hundreds).
  * ws: sao_workspace_size(SAO_OP_RUNNING_MEAN_ADVANTAGE, T, 1, 1, SAO_F32) bytes.
  */
 sao_status_t sao_running_mean_advantage(const float* rewards, const uint8_t* mask,
