@@ -11,12 +11,17 @@
 // starting from s = 0 after the last token (no bootstrap after the last action;
 // rewards before the first action leave through the left end and are dropped).
 // Every such map, and every composition of them, has the form
-//   Vn' = pV Vn + cV,  R' = pR R + cR,  A' = aV Vn + aR R + aA A + cA,  G' = gR R + gG G + cG,
-// so a thread summarises its contiguous tokens by 11 numbers, the block scans the
-// summaries (DPP lane moves inside each wave, then across waves through LDS), and
-// each thread replays its tokens from the exact state that enters it. Arithmetic
-// is float64. Tiles of 2048 tokens aligned to the global index give every thread
-// 8 tokens that it reads and writes with 16-byte vector accesses.
+//   Vn' = z Vn + cV,  R' = z R + cR,
+//   A'  = cA + X (R + gamma Vn) + (kappa X + z) A,   kappa = gamma lambda_b,
+//   G'  = cG + Y R + (gamma Y + z) G,
+// where z = 1 for a run of observations only (then cV = cA = cG = X = Y = 0) and
+// z = 0 once the run holds an action (then X = kappa^(n-1) and Y = gamma^(n-1) for
+// its n actions). So a thread summarises its contiguous tokens by 7 numbers, the
+// block scans the summaries (DPP lane moves inside each wave, then across waves
+// through LDS), and each thread replays its tokens from the exact state that
+// enters it. Arithmetic is float64. Tiles of 2048 tokens aligned to the global
+// index give every thread 8 tokens that it reads and writes with 16-byte vector
+// accesses.
 #include "common.hpp"
 #include "launch.hpp"
 #include "layout.hpp"
@@ -27,44 +32,37 @@
 namespace sao {
 
 struct Aff {
-  double pV, cV, pR, cR, aV, aR, aA, cA, gR, gG, cG;
+  double z, cV, cR, X, cA, Y, cG;
 };
 
-__device__ __forceinline__ Aff aff_identity() {
-  return Aff{1.0, 0.0, 1.0, 0.0, 0.0, 0.0, 1.0, 0.0, 0.0, 1.0, 0.0};
-}
+__device__ __forceinline__ Aff aff_identity() { return Aff{1.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0}; }
 
-// (F o G)(s) = F(G(s)).
-__device__ __forceinline__ Aff compose(const Aff& F, const Aff& G) {
+// (F o G)(s) = F(G(s)). The coefficients of A and G in F are kappa F.X + F.z and
+// gamma F.Y + F.z; products of them with G's come out in the same form.
+__device__ __forceinline__ Aff compose(const Aff& F, const Aff& G, double gamma, double kappa) {
+  const double fa = fma(kappa, F.X, F.z), fg = fma(gamma, F.Y, F.z);
   Aff r;
-  r.pV = F.pV * G.pV;
-  r.cV = fma(F.pV, G.cV, F.cV);
-  r.pR = F.pR * G.pR;
-  r.cR = fma(F.pR, G.cR, F.cR);
-  r.aV = fma(F.aV, G.pV, F.aA * G.aV);
-  r.aR = fma(F.aR, G.pR, F.aA * G.aR);
-  r.aA = F.aA * G.aA;
-  r.cA = fma(F.aV, G.cV, fma(F.aR, G.cR, fma(F.aA, G.cA, F.cA)));
-  r.gR = fma(F.gR, G.pR, F.gG * G.gR);
-  r.gG = F.gG * G.gG;
-  r.cG = fma(F.gR, G.cR, fma(F.gG, G.cG, F.cG));
+  r.z = F.z * G.z;
+  r.cV = fma(F.z, G.cV, F.cV);
+  r.cR = fma(F.z, G.cR, F.cR);
+  r.X = fma(F.X, G.z, fa * G.X);
+  r.cA = fma(F.X, fma(gamma, G.cV, G.cR), fma(fa, G.cA, F.cA));
+  r.Y = fma(F.Y, G.z, fg * G.Y);
+  r.cG = fma(F.Y, G.cR, fma(fg, G.cG, F.cG));
   return r;
 }
 
 // M o F for the map M of one token, F covering the tokens to its right
-// (the general compose() with M's constants substituted).
+// (compose() with M's constants substituted: an action is z = 0, cV = v, cR = 0,
+// X = Y = 1, cA = r - v, cG = r; an observation is the identity plus cR = r).
 __device__ __forceinline__ void push_action(Aff& F, double v, double r, double gamma, double kappa) {
   const Aff G = F;
-  F.pV = 0.0;
+  F.z = 0.0;
   F.cV = v;
-  F.pR = 0.0;
   F.cR = 0.0;
-  F.aV = fma(gamma, G.pV, kappa * G.aV);
-  F.aR = fma(kappa, G.aR, G.pR);
-  F.aA = kappa * G.aA;
+  F.X = fma(kappa, G.X, G.z);
   F.cA = fma(kappa, G.cA, fma(gamma, G.cV, G.cR + (r - v)));
-  F.gR = fma(gamma, G.gR, G.pR);
-  F.gG = gamma * G.gG;
+  F.Y = fma(gamma, G.Y, G.z);
   F.cG = fma(gamma, G.cG, G.cR + r);
 }
 __device__ __forceinline__ void push_observation(Aff& F, double r) { F.cR += r; }
@@ -81,16 +79,12 @@ __device__ __forceinline__ double dpp_f64(double old, double x) {
 template <int CTRL, int ROW_MASK>
 __device__ __forceinline__ Aff dpp_aff(const Aff& x) {
   Aff o;
-  o.pV = dpp_f64<CTRL, ROW_MASK>(1.0, x.pV);
+  o.z = dpp_f64<CTRL, ROW_MASK>(1.0, x.z);
   o.cV = dpp_f64<CTRL, ROW_MASK>(0.0, x.cV);
-  o.pR = dpp_f64<CTRL, ROW_MASK>(1.0, x.pR);
   o.cR = dpp_f64<CTRL, ROW_MASK>(0.0, x.cR);
-  o.aV = dpp_f64<CTRL, ROW_MASK>(0.0, x.aV);
-  o.aR = dpp_f64<CTRL, ROW_MASK>(0.0, x.aR);
-  o.aA = dpp_f64<CTRL, ROW_MASK>(1.0, x.aA);
+  o.X = dpp_f64<CTRL, ROW_MASK>(0.0, x.X);
   o.cA = dpp_f64<CTRL, ROW_MASK>(0.0, x.cA);
-  o.gR = dpp_f64<CTRL, ROW_MASK>(0.0, x.gR);
-  o.gG = dpp_f64<CTRL, ROW_MASK>(1.0, x.gG);
+  o.Y = dpp_f64<CTRL, ROW_MASK>(0.0, x.Y);
   o.cG = dpp_f64<CTRL, ROW_MASK>(0.0, x.cG);
   return o;
 }
@@ -100,13 +94,13 @@ __device__ __forceinline__ Aff dpp_aff(const Aff& x) {
 // of row 0 into row 1 and of row 2 into row 3 (row_bcast:15), then lane 31 into
 // rows 2 and 3 (row_bcast:31). DPP moves are VALU operations, so no step waits
 // on the LDS crossbar.
-__device__ __forceinline__ Aff wave_scan(Aff S) {
-  S = compose(S, dpp_aff<0x111, 0xf>(S));
-  S = compose(S, dpp_aff<0x112, 0xf>(S));
-  S = compose(S, dpp_aff<0x114, 0xf>(S));
-  S = compose(S, dpp_aff<0x118, 0xf>(S));
-  S = compose(S, dpp_aff<0x142, 0xa>(S));
-  S = compose(S, dpp_aff<0x143, 0xc>(S));
+__device__ __forceinline__ Aff wave_scan(Aff S, double gamma, double kappa) {
+  S = compose(S, dpp_aff<0x111, 0xf>(S), gamma, kappa);
+  S = compose(S, dpp_aff<0x112, 0xf>(S), gamma, kappa);
+  S = compose(S, dpp_aff<0x114, 0xf>(S), gamma, kappa);
+  S = compose(S, dpp_aff<0x118, 0xf>(S), gamma, kappa);
+  S = compose(S, dpp_aff<0x142, 0xa>(S), gamma, kappa);
+  S = compose(S, dpp_aff<0x143, 0xc>(S), gamma, kappa);
   return S;
 }
 
@@ -119,12 +113,12 @@ constexpr int kScanTile = kScanThreads * kScanPer;        // tokens per tile
 struct St {
   double Vn, R, A, G;
 };
-__device__ __forceinline__ St apply(const Aff& M, const St& s) {
+__device__ __forceinline__ St apply(const Aff& M, const St& s, double gamma, double kappa) {
   St o;
-  o.Vn = fma(M.pV, s.Vn, M.cV);
-  o.R = fma(M.pR, s.R, M.cR);
-  o.A = fma(M.aV, s.Vn, fma(M.aR, s.R, fma(M.aA, s.A, M.cA)));
-  o.G = fma(M.gR, s.R, fma(M.gG, s.G, M.cG));
+  o.Vn = fma(M.z, s.Vn, M.cV);
+  o.R = fma(M.z, s.R, M.cR);
+  o.A = fma(M.X, fma(gamma, s.Vn, s.R), fma(fma(kappa, M.X, M.z), s.A, M.cA));
+  o.G = fma(M.Y, s.R, fma(fma(gamma, M.Y, M.z), s.G, M.cG));
   return o;
 }
 
@@ -134,13 +128,18 @@ __device__ __forceinline__ St apply(const Aff& M, const St& s) {
 // tile on the left enters the next tile from the right. Inside a tile each
 // thread composes the maps of its tokens, the block scans the compositions,
 // and each thread replays its tokens from the exact entering state.
-__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_advantage(
+__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(6))) void k_advantage(
     const float* values, const float* rewards, const uint8_t* mask, const int32_t* cu, int32_t B,
     int64_t T, double gamma, double lam, double alpha, float* adv, float* ret, int64_t* slots,
     const int32_t* bad, bool vec_ok) {
   __shared__ Aff s_agg[kScanThreads / 64];
   __shared__ int64_t s_cnt[kScanThreads / 64];
-  __shared__ St s_carry;
+  // The state entering the next tile from the right, double-buffered so that a
+  // tile's writer never waits for the previous tile's readers.
+  __shared__ St s_carry[2];
+  // Each thread's values and rewards wait here, in its own slots, while the block
+  // scans: holding them in registers instead would cost a wave per SIMD.
+  __shared__ f32x4_t s_in[2 * kScanPer / 4][kScanThreads];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
   if (*bad) {
@@ -158,7 +157,8 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
   const double kappa = gamma * lam_b;
   const int64_t first = s / kScanTile * kScanTile;           // aligned tile containing s
   int64_t total = 0;
-  St carry{0.0, 0.0, 0.0, 0.0};                               // nothing after the last token
+  if (tid == 0) s_carry[0] = St{0.0, 0.0, 0.0, 0.0};         // nothing after the last token
+  int buf = 0;
   // Thread i takes block 255 - i of each tile, so lane order runs right to left
   // and the reverse scan over tokens is a forward scan over lanes. Whole blocks
   // inside [s, e) use vector access (when the array bases allow it).
@@ -192,6 +192,11 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
         act[j] = in && mask[t] != 0;
       }
     }
+#pragma unroll
+    for (int q = 0; q < kScanPer / 4; ++q) {
+      s_in[q][tid] = f32x4_t{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+      s_in[kScanPer / 4 + q][tid] = f32x4_t{r[4 * q], r[4 * q + 1], r[4 * q + 2], r[4 * q + 3]};
+    }
     // Pass 1: this thread's tokens as one map (tokens outside [s, e) are identities).
     Aff F = aff_identity();
     int64_t cnt = 0;
@@ -207,17 +212,25 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
       }
     }
     total += cnt;
-    const Aff S = wave_scan(F);                     // this lane and the lanes to its right
+    const Aff S = wave_scan(F, gamma, kappa);                     // this lane and the lanes to its right
     const Aff E = dpp_aff<0x138, 0xf>(S);          // wave_shr:1, the lanes to its right only
-    __syncthreads();  // the previous tile's readers of s_agg / s_carry are done
+    __syncthreads();  // the previous tile's readers of s_agg are done; its carry is visible
     if (lane == 63) s_agg[wave] = S;
-    if (tid == 0) s_carry = carry;
     __syncthreads();
     // State entering this wave: the carry through the waves to its right (lower waves).
-    St sw = s_carry;
-    for (int w = 0; w < wave; ++w) sw = apply(s_agg[w], sw);
-    St st = apply(E, sw);
+    St sw = s_carry[buf];
+    for (int w = 0; w < wave; ++w) sw = apply(s_agg[w], sw, gamma, kappa);
+    St st = apply(E, sw, gamma, kappa);
     // Pass 2: replay the tokens from that state and write the outputs.
+#pragma unroll
+    for (int q = 0; q < kScanPer / 4; ++q) {
+      const f32x4_t vq = s_in[q][tid], rq = s_in[kScanPer / 4 + q][tid];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[4 * q + j] = vq[j];
+        r[4 * q + j] = rq[j];
+      }
+    }
     float oa[kScanPer], og[kScanPer];
 #pragma unroll
     for (int j = kScanPer - 1; j >= 0; --j) {
@@ -259,11 +272,10 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
         }
       }
     }
-    // The state leaving this tile on the left (the last thread's final state) is the next carry.
-    __syncthreads();
-    if (tid == kScanThreads - 1) s_carry = st;
-    __syncthreads();
-    carry = s_carry;
+    // The state leaving this tile on the left (the last thread's final state) enters
+    // the next tile; the other buffer's readers finished before this tile's barriers.
+    buf ^= 1;
+    if (tid == kScanThreads - 1) s_carry[buf] = st;
   }
   const int64_t wcnt = wave_sum(total);
   __syncthreads();
