@@ -348,6 +348,25 @@ def test_scan_one_long_trajectory():
     _check_scan(got, a, r, n)
 
 
+@pytest.mark.parametrize("gamma,lam", [(0.0, 0.0), (0.0, 1.0), (1.0, 0.0), (1.0, 1.0)])
+def test_scan_degenerate_discounts(gamma, lam):
+    """gamma and lambda at 0 and 1 (fixed lambda): the scan's composed maps then carry
+    zero or unit coefficients through many tiles; rewards also sit on observations."""
+    T = 40000
+    cu = [0, 9000, 9001, 26000, 26000, T]                 # multi-tile, one-token and empty trajectories
+    def obs_rewards(b):
+        obs = b.mask == 0
+        b.rewards[obs] = np.random.default_rng(73).normal(0.0, 0.5, int(obs.sum())).astype(np.float32)
+    b = generate(small_config("scan-deg", 74, B=5, T=T, H=8, V=16))
+    b.cu_seqlens[:] = np.asarray(cu, dtype=np.int32)
+    obs_rewards(b)
+    a, r, n = oracle.advantage(b.values, b.rewards, b.mask, b.cu_seqlens, gamma, lam, 0.0)
+    db = to_device(b)
+    got = sao.advantage(db.values, db.rewards, db.mask, db.cu_seqlens, gamma, lam, 0.0)
+    torch.cuda.synchronize()
+    _check_scan(got, a, r, n)
+
+
 def test_unaligned_per_token_arrays():
     """Slices at odd offsets take the scalar paths of the scan and the loss."""
     b = generate(small_config("unaligned", 73, B=5, T=3001, H=64, V=200))
