@@ -28,6 +28,9 @@ __device__ __forceinline__ void walk_span(int64_t s, int64_t e, bool vec_ok, Bod
   const int64_t b0 = vec_ok ? min(e, (s + 3) / 4 * 4) : e;
   const int64_t b1 = vec_ok ? max(b0, e / 4 * 4) : e;
   for (int64_t t = s + threadIdx.x; t < b0; t += kBaseThreads) one(t);
+  // Unrolled so that a thread's loads of successive blocks are in flight together;
+  // the bodies still run, and accumulate, in token order.
+#pragma unroll 4
   for (int64_t t = b0 + 4 * static_cast<int64_t>(threadIdx.x); t < b1; t += 4 * kBaseThreads) body(t);
   for (int64_t t = b1 + threadIdx.x; t < e; t += kBaseThreads) one(t);
 }
