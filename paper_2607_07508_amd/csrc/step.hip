@@ -96,7 +96,7 @@ __global__ __launch_bounds__(kStepThreads) __attribute__((amdgpu_waves_per_eu(4)
     const float* values, const float* rewards, const uint8_t* mask, const int32_t* cu, int32_t B, int64_t T,
     double gamma, double lam, double alpha, bool last_value, float* adv, float* ret, uint8_t* last,
     int64_t* slots, const int32_t* bad, int32_t* tab_a, int32_t* tab_z, double* tab_v, double* tab_r,
-    bool vec_ok) {
+    bool vec_ok, bool out_vec) {
   __shared__ int s_scan[kStepThreads / 64];
   __shared__ Seg s_seg[kStepThreads / 64];
   __shared__ double s_map[kStepThreads][4];   // per chunk: A = cA + mA A_in, G = cG + mG G_in
@@ -263,14 +263,29 @@ __global__ __launch_bounds__(kStepThreads) __attribute__((amdgpu_waves_per_eu(4)
     if (last) last[s + t] = 0;
   }
   for (int i = wave; i < n; i += kStepThreads / 64) {
-    const int64_t a = ta[i], z = tz[i], nxt = i + 1 < n ? ta[i + 1] : L;
+    const int64_t a = s + ta[i], z = s + tz[i], nxt = s + (i + 1 < n ? ta[i + 1] : L);  // global indices
     const float A = static_cast<float>(tv[i]), G = static_cast<float>(tr[i]);
-    for (int64_t t = a + lane; t < nxt; t += 64) {
+    auto one = [&](int64_t t) {
       const bool in = t < z;
-      adv[s + t] = in ? A : 0.0f;
-      ret[s + t] = in ? G : 0.0f;
-      if (last) last[s + t] = t == z - 1 ? 1 : 0;
+      adv[t] = in ? A : 0.0f;
+      ret[t] = in ? G : 0.0f;
+      if (last) last[t] = t == z - 1 ? 1 : 0;
+    };
+    // The span's 4-aligned interior with 16-byte stores (4-byte ones for `last`),
+    // its edges token by token.
+    const int64_t b0 = out_vec ? min(nxt, (a + 3) / 4 * 4) : nxt;
+    const int64_t b1 = out_vec ? max(b0, nxt / 4 * 4) : nxt;
+    for (int64_t t = a + lane; t < b0; t += 64) one(t);
+    for (int64_t t = b0 + 4 * static_cast<int64_t>(lane); t < b1; t += 4 * 64) {
+      const bool i0 = t < z, i1 = t + 1 < z, i2 = t + 2 < z, i3 = t + 3 < z;
+      *reinterpret_cast<f32x4_t*>(adv + t) = f32x4_t{i0 ? A : 0.0f, i1 ? A : 0.0f, i2 ? A : 0.0f, i3 ? A : 0.0f};
+      *reinterpret_cast<f32x4_t*>(ret + t) = f32x4_t{i0 ? G : 0.0f, i1 ? G : 0.0f, i2 ? G : 0.0f, i3 ? G : 0.0f};
+      if (last) {
+        const int64_t k = z - 1 - t;  // byte k of this block is the step's last token
+        *reinterpret_cast<uint32_t*>(last + t) = (k >= 0 && k < 4) ? (1u << (8 * k)) : 0u;
+      }
     }
+    for (int64_t t = b1 + lane; t < nxt; t += 64) one(t);
   }
 
   const int64_t wcnt = wave_sum(cnt);
@@ -298,10 +313,14 @@ hipError_t launch_step_advantage(const float* values, const float* rewards, cons
   // Whole in-trajectory blocks of 8 tokens use vector loads when the bases allow them.
   const bool vec_ok = ((reinterpret_cast<uintptr_t>(values) | reinterpret_cast<uintptr_t>(rewards)) & 15u) == 0 &&
                       (reinterpret_cast<uintptr_t>(mask) & 7u) == 0;
+  // The output spans use 16-byte stores when adv and ret are 16-byte aligned and `last` (if given) 4-byte aligned.
+  const bool out_vec = ((reinterpret_cast<uintptr_t>(adv) | reinterpret_cast<uintptr_t>(ret)) & 15u) == 0 &&
+                       (reinterpret_cast<uintptr_t>(last) & 3u) == 0;
   hipLaunchKernelGGL(k_step_advantage, dim3(B), dim3(kStepThreads), 0, st, values, rewards, mask, cu_seqlens, B, T,
                      gamma, lam, alpha, last_value, adv, ret, last, slots, bad,
                      reinterpret_cast<int32_t*>(w8 + Ly.tab_a), reinterpret_cast<int32_t*>(w8 + Ly.tab_z),
-                     reinterpret_cast<double*>(w8 + Ly.tab_v), reinterpret_cast<double*>(w8 + Ly.tab_r), vec_ok);
+                     reinterpret_cast<double*>(w8 + Ly.tab_v), reinterpret_cast<double*>(w8 + Ly.tab_r), vec_ok,
+                     out_vec);
   if (n_tokens) hipLaunchKernelGGL(k_slots_total<kCountSlots>, dim3(1), dim3(64), 0, st, slots, n_tokens);
   return hipGetLastError();
 }
