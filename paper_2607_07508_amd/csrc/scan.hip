@@ -128,7 +128,7 @@ __device__ __forceinline__ St apply(const Aff& M, const St& s, double gamma, dou
 // tile on the left enters the next tile from the right. Inside a tile each
 // thread composes the maps of its tokens, the block scans the compositions,
 // and each thread replays its tokens from the exact entering state.
-__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(6))) void k_advantage(
+__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_advantage(
     const float* values, const float* rewards, const uint8_t* mask, const int32_t* cu, int32_t B,
     int64_t T, double gamma, double lam, double alpha, float* adv, float* ret, int64_t* slots,
     const int32_t* bad, bool vec_ok) {

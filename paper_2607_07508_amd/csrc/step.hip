@@ -31,15 +31,34 @@ constexpr int kStepThreads = 256;
 constexpr int kStepPer = 8;                               // tokens per thread per tile
 constexpr int kStepTile = kStepThreads * kStepPer;
 
+namespace {
+// Lane moves by DPP (CTRL, ROW_MASK): VALU operations, no LDS crossbar. Lanes
+// without a source, and rows outside ROW_MASK, keep `old`. A wave's inclusive
+// scan in lane order takes row_shr 1, 2, 4, 8 (0x111..0x118, all rows), then
+// row_bcast:15 (0x142, rows 1 and 3) and row_bcast:31 (0x143, rows 2 and 3);
+// wave_shr:1 (0x138) turns it into the exclusive one.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp_i32(int old, int x) {
+  return __builtin_amdgcn_update_dpp(old, x, CTRL, ROW_MASK, 0xf, false);
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_f64(double old, double x) {
+  const uint2 o = __builtin_bit_cast(uint2, old), v = __builtin_bit_cast(uint2, x);
+  return __builtin_bit_cast(double, make_uint2(static_cast<uint32_t>(dpp_i32<CTRL, ROW_MASK>(static_cast<int>(o.x), static_cast<int>(v.x))),
+                                               static_cast<uint32_t>(dpp_i32<CTRL, ROW_MASK>(static_cast<int>(o.y), static_cast<int>(v.y)))));
+}
+}  // namespace
+
 // Exclusive prefix sum over the block in thread order; *total gets the block's sum.
 __device__ __forceinline__ int block_exclusive_scan(int x, int* sh, int* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int incl = x;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += y;
-  }
+  incl += dpp_i32<0x111, 0xf>(0, incl);
+  incl += dpp_i32<0x112, 0xf>(0, incl);
+  incl += dpp_i32<0x114, 0xf>(0, incl);
+  incl += dpp_i32<0x118, 0xf>(0, incl);
+  incl += dpp_i32<0x142, 0xa>(0, incl);
+  incl += dpp_i32<0x143, 0xc>(0, incl);
   __syncthreads();  // earlier readers of sh are done
   if (lane == 63) sh[wave] = incl;
   __syncthreads();
@@ -63,8 +82,10 @@ struct Seg {
 __device__ __forceinline__ Seg seg_combine(const Seg& x, const Seg& y) {
   return y.f ? y : Seg{x.f, x.v + y.v, x.r + y.r};
 }
-__device__ __forceinline__ Seg seg_shfl_up(const Seg& x, int o) {
-  return Seg{__shfl_up(x.f, o, 64), __shfl_up(x.v, o, 64), __shfl_up(x.r, o, 64)};
+// The sums of another lane (the empty sums where there is none).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ Seg dpp_seg(const Seg& x) {
+  return Seg{dpp_i32<CTRL, ROW_MASK>(0, x.f), dpp_f64<CTRL, ROW_MASK>(0.0, x.v), dpp_f64<CTRL, ROW_MASK>(0.0, x.r)};
 }
 
 // Exclusive segmented scan over the block in thread order, `carry` standing
@@ -72,14 +93,14 @@ __device__ __forceinline__ Seg seg_shfl_up(const Seg& x, int o) {
 // (carry included) for the next tile.
 __device__ __forceinline__ Seg block_segmented_scan(const Seg& x, const Seg& carry, Seg* sh, Seg* out) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  Seg incl = x;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const Seg y = seg_shfl_up(incl, o);
-    if (lane >= o) incl = seg_combine(y, incl);
-  }
-  Seg excl = seg_shfl_up(incl, 1);
-  if (lane == 0) excl = Seg{0, 0.0, 0.0};
+  Seg incl = x;  // the empty sums on the left change nothing
+  incl = seg_combine(dpp_seg<0x111, 0xf>(incl), incl);
+  incl = seg_combine(dpp_seg<0x112, 0xf>(incl), incl);
+  incl = seg_combine(dpp_seg<0x114, 0xf>(incl), incl);
+  incl = seg_combine(dpp_seg<0x118, 0xf>(incl), incl);
+  incl = seg_combine(dpp_seg<0x142, 0xa>(incl), incl);
+  incl = seg_combine(dpp_seg<0x143, 0xc>(incl), incl);
+  const Seg excl = dpp_seg<0x138, 0xf>(incl);
   __syncthreads();  // earlier readers of sh are done
   if (lane == 63) sh[wave] = incl;
   __syncthreads();
