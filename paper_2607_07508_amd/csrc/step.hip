@@ -49,48 +49,27 @@ __device__ __forceinline__ double dpp_f64(double old, double x) {
 }
 }  // namespace
 
-// Exclusive prefix sum over the block in thread order; *total gets the block's sum.
-__device__ __forceinline__ int block_exclusive_scan(int x, int* sh, int* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int incl = x;
-  incl += dpp_i32<0x111, 0xf>(0, incl);
-  incl += dpp_i32<0x112, 0xf>(0, incl);
-  incl += dpp_i32<0x114, 0xf>(0, incl);
-  incl += dpp_i32<0x118, 0xf>(0, incl);
-  incl += dpp_i32<0x142, 0xa>(0, incl);
-  incl += dpp_i32<0x143, 0xc>(0, incl);
-  __syncthreads();  // earlier readers of sh are done
-  if (lane == 63) sh[wave] = incl;
-  __syncthreads();
-  int before = 0, all = 0;
-#pragma unroll
-  for (int w = 0; w < kStepThreads / 64; ++w) {
-    before += w < wave ? sh[w] : 0;
-    all += sh[w];
-  }
-  *total = all;
-  return before + incl - x;
-}
-
-// Sums of a segmented scan: `f` marks that a segment starts inside the span, and
-// then v, r cover only the part after the last start.
+// Sums of a segmented scan: n counts the segments that start inside the span; if
+// there are any, v and r cover only the part after the last start.
 struct Seg {
-  int f;
+  int n;
   double v, r;
 };
 // x then y (x on the left).
 __device__ __forceinline__ Seg seg_combine(const Seg& x, const Seg& y) {
-  return y.f ? y : Seg{x.f, x.v + y.v, x.r + y.r};
+  return y.n ? Seg{x.n + y.n, y.v, y.r} : Seg{x.n, x.v + y.v, x.r + y.r};
 }
 // The sums of another lane (the empty sums where there is none).
 template <int CTRL, int ROW_MASK>
 __device__ __forceinline__ Seg dpp_seg(const Seg& x) {
-  return Seg{dpp_i32<CTRL, ROW_MASK>(0, x.f), dpp_f64<CTRL, ROW_MASK>(0.0, x.v), dpp_f64<CTRL, ROW_MASK>(0.0, x.r)};
+  return Seg{dpp_i32<CTRL, ROW_MASK>(0, x.n), dpp_f64<CTRL, ROW_MASK>(0.0, x.v), dpp_f64<CTRL, ROW_MASK>(0.0, x.r)};
 }
 
-// Exclusive segmented scan over the block in thread order, `carry` standing
-// before thread 0; returns the sums entering this thread. `out` gets everything
-// (carry included) for the next tile.
+// Exclusive segmented scan over the block in thread order, the sums `carry`
+// standing before thread 0; returns the sums entering this thread, with n the
+// starts before it in this call. `out` gets everything (carry's sums included,
+// n = the call's starts) for the next call. Successive calls alternate between
+// the two halves of `sh`, so no call waits for the previous one's readers.
 __device__ __forceinline__ Seg block_segmented_scan(const Seg& x, const Seg& carry, Seg* sh, Seg* out) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   Seg incl = x;  // the empty sums on the left change nothing
@@ -101,14 +80,12 @@ __device__ __forceinline__ Seg block_segmented_scan(const Seg& x, const Seg& car
   incl = seg_combine(dpp_seg<0x142, 0xa>(incl), incl);
   incl = seg_combine(dpp_seg<0x143, 0xc>(incl), incl);
   const Seg excl = dpp_seg<0x138, 0xf>(incl);
-  __syncthreads();  // earlier readers of sh are done
   if (lane == 63) sh[wave] = incl;
   __syncthreads();
-  Seg before = carry;
+  Seg before{0, carry.v, carry.r};
   for (int w = 0; w < wave; ++w) before = seg_combine(before, sh[w]);
-  Seg all = carry;
-#pragma unroll
-  for (int w = 0; w < kStepThreads / 64; ++w) all = seg_combine(all, sh[w]);
+  Seg all = before;
+  for (int w = wave; w < kStepThreads / 64; ++w) all = seg_combine(all, sh[w]);
   *out = all;
   return seg_combine(before, excl);
 }
@@ -118,8 +95,7 @@ __global__ __launch_bounds__(kStepThreads) __attribute__((amdgpu_waves_per_eu(4)
     double gamma, double lam, double alpha, bool last_value, float* adv, float* ret, uint8_t* last,
     int64_t* slots, const int32_t* bad, int32_t* tab_a, int32_t* tab_z, double* tab_v, double* tab_r,
     bool vec_ok, bool out_vec) {
-  __shared__ int s_scan[kStepThreads / 64];
-  __shared__ Seg s_seg[kStepThreads / 64];
+  __shared__ Seg s_seg[2][kStepThreads / 64];  // alternate tiles use alternate halves
   __shared__ double s_map[kStepThreads][4];   // per chunk: A = cA + mA A_in, G = cG + mG G_in
   __shared__ double s_in[kStepThreads][2];    // (A, G) entering each chunk from the right
   __shared__ int64_t s_cnt[kStepThreads / 64];
@@ -144,7 +120,8 @@ __global__ __launch_bounds__(kStepThreads) __attribute__((amdgpu_waves_per_eu(4)
   int n = 0;
   Seg carry{0, 0.0, 0.0};
   int64_t cnt = 0;
-  for (int64_t t0 = s / kStepTile * kStepTile; t0 < e; t0 += kStepTile) {
+  int tile = 0;
+  for (int64_t t0 = s / kStepTile * kStepTile; t0 < e; t0 += kStepTile, ++tile) {
     const int64_t c0 = t0 + static_cast<int64_t>(tid) * kStepPer;
     bool m[kStepPer + 2];  // m[j] is token c0 - 1 + j
     float v[kStepPer], r[kStepPer];  // v is 0 off the runs
@@ -183,14 +160,14 @@ __global__ __launch_bounds__(kStepThreads) __attribute__((amdgpu_waves_per_eu(4)
       const bool st = m[j + 1] && !m[j];
       cnt += m[j + 1] ? 1 : 0;
       ns += st ? 1 : 0;
-      if (st) x = Seg{1, 0.0, 0.0};
+      if (st) x = Seg{0, 0.0, 0.0};
       x.v += static_cast<double>(v[j]);
       x.r += static_cast<double>(r[j]);
     }
-    int tot_s;
-    const int first = n + block_exclusive_scan(ns, s_scan, &tot_s);
+    x.n = ns;
     Seg next_carry;
-    Seg run = block_segmented_scan(x, carry, s_seg, &next_carry);
+    Seg run = block_segmented_scan(x, carry, s_seg[tile & 1], &next_carry);
+    const int first = n + run.n, tot_s = next_carry.n;
     // Replay: `key` is the step whose segment holds the token (-1 before the first).
     int key = first - 1;
 #pragma unroll
