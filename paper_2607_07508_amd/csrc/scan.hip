@@ -132,7 +132,7 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
     const float* values, const float* rewards, const uint8_t* mask, const int32_t* cu, int32_t B,
     int64_t T, double gamma, double lam, double alpha, float* adv, float* ret, int64_t* slots,
     const int32_t* bad, bool vec_ok) {
-  __shared__ Aff s_agg[kScanThreads / 64];
+  __shared__ Aff s_agg[2][kScanThreads / 64];  // alternate tiles use alternate halves
   __shared__ int64_t s_cnt[kScanThreads / 64];
   // The state entering the next tile from the right, double-buffered so that a
   // tile's writer never waits for the previous tile's readers.
@@ -214,12 +214,13 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
     total += cnt;
     const Aff S = wave_scan(F, gamma, kappa);                     // this lane and the lanes to its right
     const Aff E = dpp_aff<0x138, 0xf>(S);          // wave_shr:1, the lanes to its right only
-    __syncthreads();  // the previous tile's readers of s_agg are done; its carry is visible
-    if (lane == 63) s_agg[wave] = S;
+    // One barrier per tile: the half of s_agg written here was last read two tiles
+    // ago, and the carry written at the end of the previous tile is published by it.
+    if (lane == 63) s_agg[buf][wave] = S;
     __syncthreads();
     // State entering this wave: the carry through the waves to its right (lower waves).
     St sw = s_carry[buf];
-    for (int w = 0; w < wave; ++w) sw = apply(s_agg[w], sw, gamma, kappa);
+    for (int w = 0; w < wave; ++w) sw = apply(s_agg[buf][w], sw, gamma, kappa);
     St st = apply(E, sw, gamma, kappa);
     // Pass 2: replay the tokens from that state and write the outputs.
 #pragma unroll
@@ -273,7 +274,7 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
       }
     }
     // The state leaving this tile on the left (the last thread's final state) enters
-    // the next tile; the other buffer's readers finished before this tile's barriers.
+    // the next tile; the other buffer's readers finished before this tile's barrier.
     buf ^= 1;
     if (tid == kScanThreads - 1) s_carry[buf] = st;
   }
