@@ -13,8 +13,9 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  * Memory.   Every array argument is a DEVICE pointer owned by the caller. The
- *           library never allocates or frees caller-visible memory and keeps no
- *           mutable global state. Scratch space is the caller's `ws` buffer of
+ *           library never allocates or frees caller-visible memory. Its only
+ *           mutable host state is per calling thread: the last error message and
+ *           the measurement hook of sao_debug_time_kernel. Scratch space is the caller's `ws` buffer of
  *           `ws_bytes` bytes (device memory, 256-byte aligned), at least
  *           sao_workspace_size(...) bytes; its contents on entry are ignored.
  * Streams.  All work is enqueued on `stream` (a hipStream_t; NULL = the null
@@ -24,7 +25,8 @@
  * Layouts.  Token-major, row-major. `hidden` is T rows of H elements with row
  *           stride `ld_hidden` elements; `w_head` is V rows of H elements with
  *           row stride `ld_w`. Strides must be >= H and multiples of 8, H must
- *           be a multiple of 8, and the two bases 16-byte aligned. Per-token
+ *           be a multiple of 8, and the two bases 16-byte aligned. A row stride may
+ *           span at most 2^24 bytes (8,388,608 bf16 or 4,194,304 fp32 elements). Per-token
  *           arrays are dense, length T, aligned so that hidden[t] predicts
  *           target[t] and logp_rollout[t], values[t], rewards[t], mask[t]
  *           describe the same action a_t.
@@ -36,7 +38,7 @@
  *           work is enqueued: SAO_ERR_NULL (required pointer NULL), SAO_ERR_SHAPE
  *           (negative size, H or V < 1, bad stride/alignment, B < 1),
  *           SAO_ERR_VALUE (epsilon negative or non-finite, gamma or lambda
- *           outside [0,1], alpha non-finite), SAO_ERR_DTYPE, SAO_ERR_WORKSPACE
+ *           outside [0,1], alpha negative or non-finite), SAO_ERR_DTYPE, SAO_ERR_WORKSPACE
  *           (ws too small or misaligned), SAO_ERR_DEVICE (a HIP launch failed).
  *           sao_last_error_message() gives a thread-local detail string.
  *           T == 0 is a no-op that returns SAO_OK.
@@ -105,8 +107,8 @@ typedef enum {
 
 /* Per-token flags written by sao_clipped_loss (sao_ppo_loss: see there). */
 #define SAO_FLAG_MASKED    0  /* mask == 0                                       */
-#define SAO_FLAG_USED      1  /* 1 - eps_low < rho < 1 + eps_high                 */
-#define SAO_FLAG_LOW       2  /* rho <= 1 - eps_low                               */
+#define SAO_FLAG_USED      1  /* max(0, 1 - eps_low) < rho < 1 + eps_high         */
+#define SAO_FLAG_LOW       2  /* rho <= max(0, 1 - eps_low)                       */
 #define SAO_FLAG_HIGH      3  /* rho >= 1 + eps_high                              */
 #define SAO_FLAG_NONFINITE 4  /* rho is NaN                                       */
 
@@ -148,7 +150,8 @@ sao_status_t sao_token_logprob(const void* hidden, int64_t ld_hidden, const void
  *   adv[tau_k] = delta_k + gamma * lambda_b * adv[tau_{k+1}]
  *   ret[tau_k] = r~_k + gamma * ret[tau_{k+1}]                   (critic lambda = 1)
  * lambda_b = max(0, 1 - 1/(alpha * L_b)) with L_b the trajectory's token count
- * when alpha > 0 (length-adaptive GAE, Sec. 4.1), else `lam`.
+ * when alpha > 0 (length-adaptive GAE, Sec. 4.1); alpha == 0 selects the fixed
+ * `lam` (alpha < 0 is SAO_ERR_VALUE).
  * Arithmetic is float64 inside; adv/ret are float32, 0 where mask == 0
  * (overwritten). n_tokens (nullable, device int64) receives sum(mask), the
  * token-mean denominator N of sao_clipped_loss (overwritten).
@@ -171,8 +174,8 @@ sao_status_t sao_advantage(const float* values, const float* rewards, const uint
  *   delta_i = R_i + gamma * V_{i+1} - V_i    (V_n = 0)
  *   A_i   = delta_i + gamma * lambda_b * A_{i+1},  G_i = R_i + gamma * G_{i+1}   (critic lambda = 1)
  * lambda_b = max(0, 1 - 1/(alpha * n)) with n the trajectory's number of steps when
- * alpha > 0, else `lam`. Every token of step i gets adv = A_i and ret = G_i; tokens
- * with mask 0 get 0 (overwritten). last (nullable, uint8 [T], overwritten) is 1 on
+ * alpha > 0, else (alpha == 0) `lam`; alpha < 0 is SAO_ERR_VALUE. Every token of
+ * step i gets adv = A_i and ret = G_i; tokens with mask 0 get 0 (overwritten). last (nullable, uint8 [T], overwritten) is 1 on
  * each step's final token: the critic's loss mask in the last-token form.
  * n_tokens, status, the segment checks and their NaN outputs follow sao_advantage.
  * Arithmetic is float64 inside; reductions run in a fixed order.
@@ -235,8 +238,10 @@ sao_status_t sao_running_mean_advantage(const float* rewards, const uint8_t* mas
  * Direct double-sided importance sampling and the token-level mean,
  * Sec. 3.1, Eq. (1)-(3). For each token with mask 1 (in float64):
  *   rho_t = exp(logp[t] - logp_rollout[t])                         Eq. (2)
- *   flag  = NONFINITE if rho is NaN, LOW if rho <= 1-eps_low,
+ *   flag  = NONFINITE if rho is NaN, LOW if rho <= max(0, 1-eps_low),
  *           HIGH if rho >= 1+eps_high, else USED                   Eq. (3), strict
+ *           (a ratio is never negative: with eps_low >= 1 only rho = 0, i.e.
+ *           log pi = -inf or an underflowing exp, is clipped low)
  *   loss[0] += -(1/N) sum_{USED} rho_t adv_t logp_t    (minus Eq. (1))
  *   loss[1] += -(1/N) sum_{USED} rho_t adv_t           (same gradient)
  *   g[t]     = -[USED] rho_t adv_t / N                 (d loss / d logp[t]; exactly 0

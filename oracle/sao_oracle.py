@@ -198,8 +198,11 @@ def dis_loss(logp, logp_rollout, adv, mask, eps_low, eps_high, n_tokens: Optiona
     eps_low/eps_high are the float32 values the library receives, widened to
     float64. For each loss-mask token:
         rho_t = exp(log pi_t - log pi_rollout_t)                         Eq. (2)
-        flag  = 4 if rho is NaN; 2 if rho <= 1-eps_low; 3 if rho >= 1+eps_high; else 1
+        flag  = 4 if rho is NaN; 2 if rho <= lo; 3 if rho >= 1+eps_high; else 1
         c_t   = [flag == 1]                    (strict band of f, Eq. (3))
+    with lo = max(0, 1 - eps_low): a ratio is never negative, so eps_low >= 1 leaves
+    only rho = 0 (pi = 0, or exp underflow) below the band, and that token is
+    clipped low like any ratio at the edge rather than weighting log pi = -inf by 0.
     With N the token-mean denominator:
         loss[0] = -(1/N) sum_t c_t rho_t A_t log pi_t    (minus Eq. (1))
         loss[1] = -(1/N) sum_t c_t rho_t A_t             (same gradient, f as stop-gradient)
@@ -208,7 +211,7 @@ def dis_loss(logp, logp_rollout, adv, mask, eps_low, eps_high, n_tokens: Optiona
     """
     lp, lro, A = _f64(logp), _f64(logp_rollout), _f64(adv)
     m = np.asarray(mask) != 0
-    lo_edge = 1.0 - float(np.float32(eps_low))
+    lo_edge = max(0.0, 1.0 - float(np.float32(eps_low)))
     hi_edge = 1.0 + float(np.float32(eps_high))
     N = int(m.sum()) if n_tokens is None else int(n_tokens)
     with np.errstate(over="ignore", invalid="ignore"):

@@ -40,9 +40,12 @@ struct Band {
     ln_lo = lo > 0.0 ? log(lo) : 0.0;
     ln_hi = log(hi);
   }
-  __device__ bool le_lo(double d) const {  // r <= lo
+  // r <= max(lo, 0), the lower edge of the DIS band. A ratio is never negative,
+  // so with eps_low >= 1 only r = 0 (log pi = -inf, or exp underflow) falls below
+  // the band; it is clipped low like a ratio at the edge.
+  __device__ bool le_lo(double d) const {
     if (lo > 0.0) return near_edge(d, ln_lo) ? exp(d) <= lo : d < ln_lo;
-    return d < -700.0 ? exp(d) <= lo : false;  // r > 0 unless exp underflows
+    return d < -700.0 ? exp(d) <= 0.0 : false;  // r > 0 unless exp underflows
   }
   __device__ bool lt_lo(double d) const {  // r < lo
     if (lo > 0.0) return near_edge(d, ln_lo) ? exp(d) < lo : d < ln_lo;
@@ -259,7 +262,7 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 }  // namespace
 
-hipError_t launch_loss(const float* logp, const float* logp_rollout, const float* adv, const uint8_t* mask,
+int launch_loss(const float* logp, const float* logp_rollout, const float* adv, const uint8_t* mask,
                        int64_t T, float eps_low, float eps_high, const int64_t* n_tokens, double* loss,
                        float* g, uint8_t* flags, int64_t* counts, void* ws, hipStream_t st) {
   const LossLayout L = loss_layout(T);
@@ -277,7 +280,7 @@ hipError_t launch_loss(const float* logp, const float* logp_rollout, const float
   return hipGetLastError();
 }
 
-hipError_t launch_ppo_loss(const float* logp, const float* logp_old, const float* logp_behav, const float* adv,
+int launch_ppo_loss(const float* logp, const float* logp_old, const float* logp_behav, const float* adv,
                            const uint8_t* mask, int64_t T, float eps_low, float eps_high, const int64_t* n_tokens,
                            double* loss, float* g, uint8_t* flags, int64_t* counts, void* ws, hipStream_t st) {
   const LossLayout L = loss_layout(T);

@@ -90,6 +90,26 @@ def test_nonfinite_and_extreme_ratios():
     assert counts.tolist() == [5, 0, 2, 1, 2]
 
 
+def test_lower_edge_past_one():
+    """eps_low > 1 puts 1 - eps_low below 0. A ratio is never negative, so the lower
+    edge is 0: every positive ratio below 1 + eps_high is used, and rho = 0 (log pi =
+    -inf, or a log-ratio so low that exp underflows) is clipped low. The token's
+    term is then left out rather than being 0 * -inf."""
+    lp = np.array([-np.inf, -800.0, -0.5, -30.0], np.float64)
+    lro = np.zeros(4)
+    adv = np.array([1.0, -2.0, 3.0, 0.5])
+    loss, g, flags, counts = dis_loss(lp, lro, adv, np.ones(4, np.uint8), 1.5, 0.2)
+    assert flags.tolist() == [2, 2, 1, 1]
+    assert counts.tolist() == [4, 2, 2, 0, 0]
+    r2, r3 = math.exp(-0.5), math.exp(-30.0)
+    # hand-worked: -(1/4)(r2 * 3 * -0.5 + r3 * 0.5 * -30)
+    assert loss[0] == pytest.approx(-(r2 * 3 * -0.5 + r3 * 0.5 * -30.0) / 4, rel=1e-14)
+    assert loss[1] == pytest.approx(-(r2 * 3 + r3 * 0.5) / 4, rel=1e-14)
+    assert np.isfinite(loss).all() and g[0] == 0 and g[1] == 0
+    # eps_low = 1 gives the same edge
+    assert dis_loss(lp, lro, adv, np.ones(4, np.uint8), 1.0, 0.2)[2].tolist() == flags.tolist()
+
+
 def test_global_token_count_and_empty():
     b, lp, adv, N = _c0()
     lro = rollout_logprobs(lp, b.xi)
