@@ -17,7 +17,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsao.so")
 ARCH = os.environ.get("SAO_OFFLOAD_ARCH", "gfx950")
 
-SOURCES = ["api.cpp", "head.hip", "scan.hip", "step.hip", "baseline.hip", "loss.hip", "ev.hip", "value.hip"]
+SOURCES = ["api.cpp", "runtime.cpp", "head.hip", "scan.hip", "step.hip", "baseline.hip", "loss.hip", "ev.hip", "value.hip"]
 
 
 def hipcc() -> str:
@@ -58,6 +58,28 @@ def build(extra=(), verbose: bool = False) -> str:
     if verbose:
         print(f"built {LIB}")
     return LIB
+
+
+# The argument-validation layer alone (api.cpp, which includes no HIP header) with
+# host stand-ins for the launchers (host_stub.cpp): a GPU-free library for running
+# the host ABI tests under the sanitizers. Never used by the product path.
+HOST_CHECK_LIB = os.path.join(BUILD, "libsao_hostcheck.so")
+
+
+def build_host_check(sanitize: bool = True) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    gxx = shutil.which("g++")
+    if gxx is None:
+        raise RuntimeError("g++ not found")
+    san = ["-fsanitize=address,undefined", "-fno-omit-frame-pointer", "-fno-sanitize-recover=undefined"] \
+        if sanitize else []
+    cmd = [gxx, "-O1", "-g", "-std=c++17", "-fPIC", "-shared", "-Wall", "-Wextra", "-Werror", *san,
+           "-I", os.path.join(ROOT, "include"), "-I", CSRC, os.path.join(CSRC, "api.cpp"),
+           os.path.join(CSRC, "host_stub.cpp"), "-o", HOST_CHECK_LIB]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"host-check build failed\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    return HOST_CHECK_LIB
 
 
 if __name__ == "__main__":

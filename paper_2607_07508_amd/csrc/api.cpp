@@ -1,7 +1,8 @@
-// C ABI of the SAO loss pass: host-side validation, workspace sizing, launch.
-// Every check below runs before any HIP call, so argument errors never touch the device.
-#include <hip/hip_runtime.h>
-
+// C ABI of the SAO loss pass: host-side validation, workspace sizing, dispatch to
+// the launchers. Every check below runs before any HIP call, so argument errors
+// never touch the device. This translation unit includes no HIP header: it builds
+// with a plain host compiler too, which is how the validation layer is run under
+// the address and undefined-behaviour sanitizers on a machine without a GPU.
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -32,6 +33,9 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 size_t esize_of(sao_dtype_t d) { return d == SAO_BF16 ? 2 : 4; }
 
 constexpr int64_t kMaxRows = (int64_t{1} << 31) - 1024;
+// The MFMA tile engine forms each lane's copy offset in 32 bits as
+// row * ld * element size with row < 256, so a row stride may span at most 2^24 bytes.
+constexpr int64_t kMaxRowBytes = int64_t{1} << 24;
 
 sao_status_t check_head(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w, int64_t T,
                         int64_t H, int64_t V, sao_dtype_t dtype) {
@@ -43,6 +47,10 @@ sao_status_t check_head(const void* hidden, int64_t ld_hidden, const void* w_hea
     return fail(SAO_ERR_SHAPE, "ld_hidden=%lld must be >= H and a multiple of 8", (long long)ld_hidden);
   if (ld_w < H || ld_w % 8 != 0)
     return fail(SAO_ERR_SHAPE, "ld_w=%lld must be >= H and a multiple of 8", (long long)ld_w);
+  const int64_t es = static_cast<int64_t>(esize_of(dtype));
+  if (ld_hidden > kMaxRowBytes / es || ld_w > kMaxRowBytes / es)
+    return fail(SAO_ERR_SHAPE, "ld_hidden=%lld, ld_w=%lld: row strides are limited to %lld elements",
+                (long long)ld_hidden, (long long)ld_w, (long long)(kMaxRowBytes / es));
   if (!aligned16(hidden) || !aligned16(w_head))
     return fail(SAO_ERR_SHAPE, "hidden and w_head must be 16-byte aligned");
   return SAO_OK;
@@ -65,19 +73,20 @@ sao_status_t check_segments_args(const float* rewards, const uint8_t* mask, cons
   return SAO_OK;
 }
 
-sao_status_t device(hipError_t e, const char* what) {
-  if (e != hipSuccess) return fail(SAO_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+sao_status_t device(int e, const char* what) {
+  if (e != 0) return fail(SAO_ERR_DEVICE, "%s: %s", what, sao::device_error_string(e));
   return ok();
 }
 
-}  // namespace
-
-namespace sao {
-KernelTimer& kernel_timer() {
-  thread_local KernelTimer t;
-  return t;
+// alpha > 0 selects the length-adaptive lambda, alpha == 0 the fixed one.
+sao_status_t check_discounts(double gamma, double lam, double alpha) {
+  if (!(gamma >= 0.0 && gamma <= 1.0)) return fail(SAO_ERR_VALUE, "gamma=%g outside [0,1]", gamma);
+  if (!(lam >= 0.0 && lam <= 1.0)) return fail(SAO_ERR_VALUE, "lam=%g outside [0,1]", lam);
+  if (!std::isfinite(alpha) || alpha < 0.0) return fail(SAO_ERR_VALUE, "alpha=%g must be finite and >= 0", alpha);
+  return SAO_OK;
 }
-}  // namespace sao
+
+}  // namespace
 
 extern "C" {
 
@@ -97,13 +106,6 @@ const char* sao_status_string(sao_status_t s) {
 const char* sao_last_error_message(void) { return g_msg; }
 
 const char* sao_version(void) { return "0.1.0"; }
-
-void sao_debug_time_kernel(int kernel, void* start_event, void* stop_event) {
-  sao::KernelTimer& t = sao::kernel_timer();
-  t.kernel = (start_event && stop_event) ? kernel : SAO_KERNEL_NONE;
-  t.start = static_cast<hipEvent_t>(start_event);
-  t.stop = static_cast<hipEvent_t>(stop_event);
-}
 
 size_t sao_workspace_size(sao_op_t op, int64_t T, int64_t H, int64_t V, sao_dtype_t dtype) {
   if (T < 0 || (dtype != SAO_BF16 && dtype != SAO_F32)) return 0;
@@ -157,9 +159,7 @@ sao_status_t sao_advantage(const float* values, const float* rewards, const uint
     return fail(SAO_ERR_NULL, "values, rewards, mask, cu_seqlens, adv and ret are required");
   if (B < 1) return fail(SAO_ERR_SHAPE, "B=%d must be >= 1", (int)B);
   if (T < 0 || T > kMaxRows) return fail(SAO_ERR_SHAPE, "T=%lld out of range", (long long)T);
-  if (!(gamma >= 0.0 && gamma <= 1.0)) return fail(SAO_ERR_VALUE, "gamma=%g outside [0,1]", gamma);
-  if (!(lam >= 0.0 && lam <= 1.0)) return fail(SAO_ERR_VALUE, "lam=%g outside [0,1]", lam);
-  if (!std::isfinite(alpha)) return fail(SAO_ERR_VALUE, "alpha must be finite");
+  if (sao_status_t s = check_discounts(gamma, lam, alpha)) return s;
   if (T == 0) return ok();
   if (sao_status_t s = check_ws(ws, ws_bytes, sao_workspace_size(SAO_OP_ADVANTAGE, T, 1, 1, SAO_F32))) return s;
   return device(sao::launch_advantage(values, rewards, mask, cu_seqlens, B, T, gamma, lam, alpha, adv, ret,
@@ -175,9 +175,7 @@ sao_status_t sao_step_advantage(const float* values, const float* rewards, const
     return fail(SAO_ERR_NULL, "values, rewards, mask, cu_seqlens, adv and ret are required");
   if (B < 1) return fail(SAO_ERR_SHAPE, "B=%d must be >= 1", (int)B);
   if (T < 0 || T > kMaxRows) return fail(SAO_ERR_SHAPE, "T=%lld out of range", (long long)T);
-  if (!(gamma >= 0.0 && gamma <= 1.0)) return fail(SAO_ERR_VALUE, "gamma=%g outside [0,1]", gamma);
-  if (!(lam >= 0.0 && lam <= 1.0)) return fail(SAO_ERR_VALUE, "lam=%g outside [0,1]", lam);
-  if (!std::isfinite(alpha)) return fail(SAO_ERR_VALUE, "alpha must be finite");
+  if (sao_status_t s = check_discounts(gamma, lam, alpha)) return s;
   if (step_value != SAO_STEP_AVERAGE && step_value != SAO_STEP_LAST)
     return fail(SAO_ERR_VALUE, "unknown step value form %d", (int)step_value);
   if (T == 0) return ok();

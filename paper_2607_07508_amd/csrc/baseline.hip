@@ -206,7 +206,7 @@ bool span_vec_ok(const float* rewards, const uint8_t* mask, const float* adv) {
 }
 }  // namespace
 
-hipError_t launch_group_advantage(const float* rewards, const uint8_t* mask, const int32_t* cu_seqlens, int32_t B,
+int launch_group_advantage(const float* rewards, const uint8_t* mask, const int32_t* cu_seqlens, int32_t B,
                                   int64_t T, int32_t group_size, double eps_stab, float* adv, double* traj_reward,
                                   double* traj_adv, int64_t* n_tokens, int32_t* status, void* ws, hipStream_t st) {
   const SegHead H = seg_head();
@@ -226,7 +226,7 @@ hipError_t launch_group_advantage(const float* rewards, const uint8_t* mask, con
   return hipGetLastError();
 }
 
-hipError_t launch_running_mean_advantage(const float* rewards, const uint8_t* mask, const int32_t* cu_seqlens,
+int launch_running_mean_advantage(const float* rewards, const uint8_t* mask, const int32_t* cu_seqlens,
                                          int32_t B, int64_t T, const int32_t* keys, int32_t n_keys, int32_t window,
                                          double* history, int64_t* seen, float* adv, double* traj_reward,
                                          double* traj_adv, int64_t* n_tokens, int32_t* status, void* ws,

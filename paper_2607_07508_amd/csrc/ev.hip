@@ -118,7 +118,7 @@ __global__ __launch_bounds__(kLossThreads) void k_ev_final(const Moments* part, 
   }
 }
 
-hipError_t launch_explained_variance(const float* values, const float* ret, const uint8_t* mask, int64_t T,
+int launch_explained_variance(const float* values, const float* ret, const uint8_t* mask, int64_t T,
                                      double* moments, double* ev, void* ws, hipStream_t st) {
   const EvLayout L = ev_layout(T);
   Moments* part = reinterpret_cast<Moments*>(static_cast<char*>(ws) + L.part);

@@ -14,6 +14,7 @@
 #include "gemm.hpp"
 #include "launch.hpp"
 #include "layout.hpp"
+#include "timer.hpp"
 #include "../../include/sao.h"
 
 namespace sao {
@@ -651,7 +652,7 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
   return hipGetLastError();
 }
 
-hipError_t launch_logprob(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
+int launch_logprob(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
                           const int32_t* target, const uint8_t* mask, int64_t T, int64_t H, int64_t V,
                           bool bf16, float* logp, float* lse, int32_t* status, void* ws, hipStream_t st) {
   return bf16 ? logprob_impl<BF16>(hidden, ld_hidden, w_head, ld_w, target, mask, T, H, V, logp, lse,
@@ -660,7 +661,7 @@ hipError_t launch_logprob(const void* hidden, int64_t ld_hidden, const void* w_h
                                   status, ws, st);
 }
 
-hipError_t launch_backward(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
+int launch_backward(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
                            const int32_t* target, const float* lse, const float* g, int64_t T, int64_t H,
                            int64_t V, bool bf16, void* dhidden, float* dw, void* ws, hipStream_t st) {
   return bf16 ? backward_impl<BF16>(hidden, ld_hidden, w_head, ld_w, target, lse, g, T, H, V, dhidden, dw,

@@ -289,7 +289,7 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(4)
   }
 }
 
-hipError_t launch_advantage(const float* values, const float* rewards, const uint8_t* mask,
+int launch_advantage(const float* values, const float* rewards, const uint8_t* mask,
                             const int32_t* cu_seqlens, int32_t B, int64_t T, double gamma, double lam,
                             double alpha, float* adv, float* ret, int64_t* n_tokens, int32_t* status,
                             void* ws, hipStream_t st) {

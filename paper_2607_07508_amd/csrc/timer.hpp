@@ -1,0 +1,18 @@
+// Per-thread measurement hook of sao_debug_time_kernel: the caller's event pair
+// and the kernel it brackets.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace sao {
+
+struct KernelTimer {
+  int kernel = 0;
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
+// The calling thread's hook (thread-local state, the library's only mutable host state).
+KernelTimer& kernel_timer();
+
+}  // namespace sao

@@ -149,7 +149,7 @@ __global__ __launch_bounds__(kValueThreads) void k_value_final(const float* part
   dw_v[col] += s;
 }
 
-hipError_t launch_value_forward(const void* hidden, int64_t ld_hidden, const void* w_v, int64_t T, int64_t H,
+int launch_value_forward(const void* hidden, int64_t ld_hidden, const void* w_v, int64_t T, int64_t H,
                                 bool bf16, float* v, hipStream_t st) {
   const dim3 grid(static_cast<unsigned>(ceil_div(T, kValueThreads / 64)));
   if (bf16)
@@ -161,7 +161,7 @@ hipError_t launch_value_forward(const void* hidden, int64_t ld_hidden, const voi
   return hipGetLastError();
 }
 
-hipError_t launch_value_loss(const void* hidden, int64_t ld_hidden, const void* w_v, const float* v,
+int launch_value_loss(const void* hidden, int64_t ld_hidden, const void* w_v, const float* v,
                              const float* ret, const uint8_t* mask, int64_t T, int64_t H, const int64_t* n_tokens,
                              bool bf16, double* loss_v, void* dhidden_v, float* dw_v, void* ws, hipStream_t st) {
   const ValueLayout L = value_layout(T, H);

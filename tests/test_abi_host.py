@@ -64,6 +64,12 @@ def test_logprob_validation(L):
     assert logprob(L, ws=None) == ERR_NULL
     assert logprob(L, ws=FAKE + 16) == ERR_WORKSPACE               # not 256-byte aligned
     assert logprob(L, T=0) == OK                                    # no-op
+    # row strides: the tile engine's 32-bit lane offsets allow 2^24 bytes per row
+    assert logprob(L, ldh=(1 << 23) + 8) == ERR_SHAPE                # bf16
+    assert logprob(L, ldw=(1 << 23) + 8) == ERR_SHAPE
+    assert logprob(L, ldw=1 << 23, ws_bytes=16) == ERR_WORKSPACE     # the largest stride passes the shape checks
+    assert logprob(L, ldh=(1 << 22) + 8, dt=1) == ERR_SHAPE          # fp32
+    assert logprob(L, ldh=1 << 22, dt=1, ws_bytes=16) == ERR_WORKSPACE
     assert b"workspace" in L.sao_last_error_message() or L.sao_last_error_message() == b""
 
 
@@ -79,6 +85,8 @@ def test_advantage_validation(L):
     assert adv(gamma=float("nan")) == ERR_VALUE
     assert adv(lam=-0.1) == ERR_VALUE
     assert adv(alpha=float("inf")) == ERR_VALUE
+    assert adv(alpha=-1.5) == ERR_VALUE                               # alpha == 0 selects the fixed lambda
+    assert adv(alpha=0.0, ws_bytes=4) == ERR_WORKSPACE
     assert adv(ws=None) == ERR_NULL
     assert adv(ws_bytes=4) == ERR_WORKSPACE
     assert adv(T=0) == OK
@@ -94,6 +102,7 @@ def test_step_advantage_validation(L):
     assert st(gamma=-0.5) == ERR_VALUE
     assert st(lam=2.0) == ERR_VALUE
     assert st(alpha=float("nan")) == ERR_VALUE
+    assert st(alpha=-0.5) == ERR_VALUE
     assert st(form=2) == ERR_VALUE
     assert st(ws=None) == ERR_NULL
     assert st(ws_bytes=64) == ERR_WORKSPACE
@@ -173,6 +182,8 @@ def test_backward_validation(L):
     assert bwd(H=0) == ERR_SHAPE
     assert bwd(dt=2) == ERR_DTYPE
     assert bwd(ws_bytes=100) == ERR_WORKSPACE
+    assert L.sao_loss_backward(FAKE, 64, FAKE, (1 << 23) + 8, FAKE, FAKE, FAKE, 16, 64, 100, 0, FAKE, FAKE, FAKE,
+                               1 << 40, None) == ERR_SHAPE
     assert bwd(T=0) == OK
 
 
