@@ -68,15 +68,18 @@ inline int dh_pieces(int64_t T, int64_t H) {
   return static_cast<int>(p);
 }
 
-// Vocabulary rows per backward block: kVocabBlock, doubled up to kVocabBlockMax
-// while one block's dz product would have fewer than 8192 tiles (32 per CU) at
-// the host bound of token rows, so that short token chunks still give each
-// launch many rounds of tiles and take fewer launches.
+// Vocabulary rows per backward block. The target size is kVocabBlock, doubled up
+// to kVocabBlockMax while one block's dz product would have fewer than 8192 tiles
+// (32 per CU) at the host bound of token rows, so that short token chunks still
+// give each launch many rounds of tiles and take fewer launches. V is then cut
+// into as many blocks as that target size needs, of equal size rounded up to a
+// whole tile, so that no block is a short remainder whose launches cannot fill
+// the GPU (only the last block is shorter, by less than one tile per block).
 inline int64_t vocab_block(int64_t t_pad, int64_t V) {
   int64_t vc = kVocabBlock;
   while (vc < kVocabBlockMax && (t_pad / kTile) * (vc / kTile) < 8192) vc *= 2;
-  const int64_t v_all = round_up(V, kTile);
-  return vc < v_all ? vc : v_all;
+  const int64_t blocks = ceil_div(V, vc);
+  return round_up(ceil_div(V, blocks), kTile);
 }
 
 inline BackwardLayout backward_layout(int64_t T, int64_t H, int64_t V, size_t esize) {
@@ -140,6 +143,12 @@ inline LossLayout loss_layout(int64_t T) {
   L.total = c.off;
   return L;
 }
+
+// The largest sao_clipped_loss workspace (kLossMaxBlocks blocks; the three pieces
+// are 256-byte multiples), the size of sao_clipped_loss_noalloc's static scratch.
+// Every T fits, since the block count is capped.
+constexpr size_t kLossScratchBytes = 16 * kLossMaxBlocks + 40 * kLossMaxBlocks + 256;
+static_assert((16 * kLossMaxBlocks) % 256 == 0 && (40 * kLossMaxBlocks) % 256 == 0, "pieces stay aligned");
 
 // sao_step_advantage: the head, then a step table of T entries (a trajectory's
 // steps sit at its own token offset): start and end (int32), and two doubles
