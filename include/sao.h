@@ -14,8 +14,9 @@
  * ---------------------------------------
  * Memory.   Every array argument is a DEVICE pointer owned by the caller. The
  *           library never allocates or frees caller-visible memory. Its only
- *           mutable host state is per calling thread: the last error message and
- *           the measurement hook of sao_debug_time_kernel. Scratch space is the caller's `ws` buffer of
+ *           mutable host state is per calling thread (the last error message and
+ *           the measurement hook of sao_debug_time_kernel), plus, per device, the
+ *           address of sao_clipped_loss_noalloc's static scratch. Scratch space is the caller's `ws` buffer of
  *           `ws_bytes` bytes (device memory, 256-byte aligned), at least
  *           sao_workspace_size(...) bytes; its contents on entry are ignored.
  * Streams.  All work is enqueued on `stream` (a hipStream_t; NULL = the null
@@ -256,6 +257,28 @@ sao_status_t sao_clipped_loss(const float* logp, const float* logp_rollout, cons
                               const uint8_t* mask, int64_t T, float eps_low, float eps_high,
                               const int64_t* n_tokens, double* loss, float* g, uint8_t* flags,
                               int64_t* counts, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * sao_clipped_loss without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation). Same arguments, outputs, accumulation and
+ * results as sao_clipped_loss (the same kernels; bit-identical outputs), minus
+ * ws and ws_bytes. The kernels' scratch (per-block partials and the mask count)
+ * is a static array of 114,944 bytes in device memory, one per GPU, which the
+ * library obtains on its first call on each device (with that device current)
+ * and holds until the process ends; no call allocates or frees anything. That
+ * maximum covers every T, since the loss uses at most 2048 blocks of partials;
+ * a T whose scratch would not fit is rejected with SAO_ERR_WORKSPACE. `stream`
+ * must belong to the current device (else SAO_ERR_DEVICE). Every call on a GPU
+ * shares that GPU's array, and each call writes every part of the scratch it
+ * reads, so nothing carries over between calls; but calls that overlap on one
+ * GPU (on different streams, or from different host threads without ordering)
+ * race on it and must not be issued.
+ */
+sao_status_t sao_clipped_loss_noalloc(const float* logp, const float* logp_rollout, const float* adv,
+                                      const uint8_t* mask, int64_t T, float eps_low, float eps_high,
+                                      const int64_t* n_tokens, double* loss, float* g, uint8_t* flags,
+                                      int64_t* counts, hipStream_t stream);
 
 /*
  * The clipped surrogate the paper compares DIS with: the unified objective of

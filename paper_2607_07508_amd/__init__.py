@@ -8,8 +8,8 @@ explained-variance diagnostic the paper reports. This
 package holds the build script and a thin ctypes binding whose functions mirror
 the C entry points.
 """
-from .binding import (SaoError, advantage, clipped_loss, explained_variance, group_advantage,  # noqa: F401
-                      lib, loss_backward, ppo_loss, running_mean_advantage, running_mean_state, step_advantage,
-                      token_logprob, value_forward, value_loss, workspace_size)
+from .binding import (SaoError, advantage, clipped_loss, clipped_loss_noalloc,  # noqa: F401
+                      explained_variance, group_advantage, lib, loss_backward, ppo_loss, running_mean_advantage,
+                      running_mean_state, step_advantage, token_logprob, value_forward, value_loss, workspace_size)
 
 __version__ = "0.1.0"

@@ -25,7 +25,7 @@ FLAG_MASKED, FLAG_USED, FLAG_LOW, FLAG_HIGH, FLAG_NONFINITE = 0, 1, 2, 3, 4
 EXPORTS = ("sao_status_string", "sao_last_error_message", "sao_version", "sao_workspace_size",
            "sao_token_logprob", "sao_advantage", "sao_clipped_loss", "sao_loss_backward",
            "sao_value_forward", "sao_value_loss", "sao_ppo_loss", "sao_explained_variance", "sao_step_advantage",
-           "sao_group_advantage", "sao_running_mean_advantage",
+           "sao_group_advantage", "sao_running_mean_advantage", "sao_clipped_loss_noalloc",
            "sao_debug_time_kernel")
 KERNEL_NONE, KERNEL_HEAD_FORWARD = 0, 1
 
@@ -50,6 +50,8 @@ _SIGS = {
                                      ctypes.c_size_t, _p]),
     "sao_clipped_loss": (ctypes.c_int, [_p, _p, _p, _p, _i64, ctypes.c_float, ctypes.c_float, _p, _p,
                                         _p, _p, _p, _p, ctypes.c_size_t, _p]),
+    "sao_clipped_loss_noalloc": (ctypes.c_int, [_p, _p, _p, _p, _i64, ctypes.c_float, ctypes.c_float, _p, _p,
+                                                _p, _p, _p, _p]),
     "sao_loss_backward": (ctypes.c_int, [_p, _i64, _p, _i64, _p, _p, _p, _i64, _i64, _i64,
                                          ctypes.c_int, _p, _p, _p, ctypes.c_size_t, _p]),
     "sao_value_forward": (ctypes.c_int, [_p, _i64, _p, _i64, _i64, ctypes.c_int, _p, _p, ctypes.c_size_t, _p]),
@@ -311,6 +313,33 @@ def clipped_loss(logp: torch.Tensor, logp_rollout: torch.Tensor, adv: torch.Tens
             _ptr(logp), _ptr(logp_rollout), _ptr(adv), _ptr(mask), T, float(eps_low), float(eps_high),
             _ptr(n_tokens), _ptr(loss), _ptr(g), _ptr(flags), _ptr(counts), _ptr(ws),
             0 if ws is None else ws.numel(), _stream(dev)))
+    return loss, g, flags, counts
+
+
+def clipped_loss_noalloc(logp: torch.Tensor, logp_rollout: torch.Tensor, adv: torch.Tensor, mask: torch.Tensor,
+                         eps_low: float, eps_high: float, n_tokens: Optional[torch.Tensor] = None,
+                         loss: Optional[torch.Tensor] = None, counts: Optional[torch.Tensor] = None):
+    """clipped_loss through sao_clipped_loss_noalloc: the library's static per-device
+    scratch instead of a workspace. Same results; calls that overlap on one GPU race."""
+    T = logp.shape[0]
+    dev = logp.device
+    _vec(logp, "logp", torch.float32, T, dev)
+    _vec(logp_rollout, "logp_rollout", torch.float32, T, dev)
+    _vec(adv, "adv", torch.float32, T, dev)
+    _vec(mask, "mask", torch.uint8, T, dev)
+    _vec(n_tokens, "n_tokens", torch.int64, 1, dev, optional=True)
+    if loss is None:
+        loss = torch.zeros(2, dtype=torch.float64, device=dev)
+    if counts is None:
+        counts = torch.zeros(5, dtype=torch.int64, device=dev)
+    _vec(loss, "loss", torch.float64, 2, dev)
+    _vec(counts, "counts", torch.int64, 5, dev)
+    g = torch.empty(T, dtype=torch.float32, device=dev)
+    flags = torch.empty(T, dtype=torch.uint8, device=dev)
+    if T:
+        _check(lib().sao_clipped_loss_noalloc(
+            _ptr(logp), _ptr(logp_rollout), _ptr(adv), _ptr(mask), T, float(eps_low), float(eps_high),
+            _ptr(n_tokens), _ptr(loss), _ptr(g), _ptr(flags), _ptr(counts), _stream(dev)))
     return loss, g, flags, counts
 
 

@@ -237,6 +237,25 @@ sao_status_t sao_clipped_loss(const float* logp, const float* logp_rollout, cons
                 "sao_clipped_loss launch");
 }
 
+sao_status_t sao_clipped_loss_noalloc(const float* logp, const float* logp_rollout, const float* adv,
+                                      const uint8_t* mask, int64_t T, float eps_low, float eps_high,
+                                      const int64_t* n_tokens, double* loss, float* g, uint8_t* flags,
+                                      int64_t* counts, hipStream_t stream) {
+  if (!logp || !logp_rollout || !adv || !mask || !loss || !g || !flags || !counts)
+    return fail(SAO_ERR_NULL, "logp, logp_rollout, adv, mask, loss, g, flags and counts are required");
+  if (T < 0 || T > kMaxRows) return fail(SAO_ERR_SHAPE, "T=%lld out of range", (long long)T);
+  if (!(eps_low >= 0.0f) || !std::isfinite(eps_low) || !(eps_high >= 0.0f) || !std::isfinite(eps_high))
+    return fail(SAO_ERR_VALUE, "eps_low=%g, eps_high=%g must be finite and >= 0", eps_low, eps_high);
+  if (T == 0) return ok();
+  const size_t need = sao::loss_layout(T).total;
+  if (need > sao::kLossScratchBytes)
+    return fail(SAO_ERR_WORKSPACE, "T=%lld needs %zu bytes of scratch, more than the static %zu", (long long)T,
+                need, sao::kLossScratchBytes);
+  return device(sao::launch_loss_noalloc(logp, logp_rollout, adv, mask, T, eps_low, eps_high, n_tokens, loss, g,
+                                         flags, counts, stream),
+                "sao_clipped_loss_noalloc launch");
+}
+
 sao_status_t sao_ppo_loss(const float* logp, const float* logp_old, const float* logp_behav, const float* adv,
                           const uint8_t* mask, int64_t T, float eps_low, float eps_high, const int64_t* n_tokens,
                           double* loss, float* g, uint8_t* flags, int64_t* counts, void* ws, size_t ws_bytes,

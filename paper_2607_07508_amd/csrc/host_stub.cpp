@@ -44,6 +44,10 @@ int launch_loss(const float*, const float*, const float*, const uint8_t*, int64_
                 double*, float*, uint8_t*, int64_t*, void*, hipStream_t) {
   return kNoDevice;
 }
+int launch_loss_noalloc(const float*, const float*, const float*, const uint8_t*, int64_t, float, float,
+                        const int64_t*, double*, float*, uint8_t*, int64_t*, hipStream_t) {
+  return kNoDevice;
+}
 int launch_ppo_loss(const float*, const float*, const float*, const float*, const uint8_t*, int64_t, float, float,
                     const int64_t*, double*, float*, uint8_t*, int64_t*, void*, hipStream_t) {
   return kNoDevice;

@@ -3,6 +3,7 @@
 // argument-validation layer that calls them needs no HIP header.
 #pragma once
 
+#include <stddef.h>
 #include <stdint.h>
 
 #include "../../include/sao.h"
@@ -40,6 +41,12 @@ int launch_running_mean_advantage(const float* rewards, const uint8_t* mask, con
 int launch_loss(const float* logp, const float* logp_rollout, const float* adv, const uint8_t* mask,
                        int64_t T, float eps_low, float eps_high, const int64_t* n_tokens, double* loss,
                        float* g, uint8_t* flags, int64_t* counts, void* ws, hipStream_t st);
+
+// The DIS loss with its workspace in a static per-device array of
+// kLossScratchBytes (no allocation); the stream must belong to the current device.
+int launch_loss_noalloc(const float* logp, const float* logp_rollout, const float* adv, const uint8_t* mask,
+                        int64_t T, float eps_low, float eps_high, const int64_t* n_tokens, double* loss, float* g,
+                        uint8_t* flags, int64_t* counts, hipStream_t st);
 
 int launch_ppo_loss(const float* logp, const float* logp_old, const float* logp_behav, const float* adv,
                            const uint8_t* mask, int64_t T, float eps_low, float eps_high, const int64_t* n_tokens,

@@ -5,6 +5,8 @@
 // float64, g = d loss / d logp, and per-block partial sums (loss terms in float64,
 // counts in int64) reduced in a fixed order by a one-block final kernel, so
 // results do not depend on scheduling.
+#include <mutex>
+
 #include "common.hpp"
 #include "launch.hpp"
 #include "layout.hpp"
@@ -278,6 +280,57 @@ int launch_loss(const float* logp, const float* logp_rollout, const float* adv, 
   hipLaunchKernelGGL(k_loss_final, dim3(1), dim3(kLossThreads), 0, st, part_f, part_i, nblk, n_ptr, 2, loss,
                      counts);
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------- //
+// sao_clipped_loss_noalloc: the same kernels with their workspace in a static
+// device array instead of the caller's buffer, for callers that cannot allocate.
+// ------------------------------------------------------------------------- //
+
+// kLossScratchBytes: the loss layout at its largest. One copy per device (each GPU holds its own, at its own address, until the
+// process ends). Host code never uses this name as an address: on the host it is
+// only a handle for hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[kLossScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+struct ScratchSlot {
+  std::once_flag once;
+  void* ptr = nullptr;
+  hipError_t err = hipSuccess;
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+}  // namespace
+
+int launch_loss_noalloc(const float* logp, const float* logp_rollout, const float* adv, const uint8_t* mask,
+                        int64_t T, float eps_low, float eps_high, const int64_t* n_tokens, double* loss, float* g,
+                        uint8_t* flags, int64_t* counts, hipStream_t st) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  if (st != nullptr) {
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(st, &sdev);
+    if (e != hipSuccess) return e;
+    if (sdev != dev) return hipErrorInvalidDevice;  // the stream must belong to the current device
+  }
+  // First call on this device (with it current): the device address of its copy.
+  ScratchSlot& slot = g_scratch[dev];
+  std::call_once(slot.once, [&] {
+    void* p = nullptr;
+    slot.err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (slot.err == hipSuccess) slot.ptr = p;
+  });
+  if (slot.err != hipSuccess) return slot.err;
+  if (loss_layout(T).total > kLossScratchBytes) return hipErrorInvalidValue;  // the caller checked this
+  // Every piece of the layout is written before it is read (block partials, then
+  // the mask count when n_tokens is NULL), so nothing needs clearing between calls.
+  return launch_loss(logp, logp_rollout, adv, mask, T, eps_low, eps_high, n_tokens, loss, g, flags, counts,
+                     slot.ptr, st);
 }
 
 int launch_ppo_loss(const float* logp, const float* logp_old, const float* logp_behav, const float* adv,

@@ -146,6 +146,17 @@ def test_loss_validation(L):
     assert loss(T=0) == OK
 
 
+def test_loss_noalloc_validation(L):
+    def loss(T=10, el=0.2, eh=0.2, g=FAKE, lp=FAKE):
+        return L.sao_clipped_loss_noalloc(lp, FAKE, FAKE, FAKE, T, el, eh, None, FAKE, g, FAKE, FAKE, None)
+    assert loss(g=None) == ERR_NULL
+    assert loss(lp=None) == ERR_NULL
+    assert loss(T=-1) == ERR_SHAPE
+    assert loss(el=-0.1) == ERR_VALUE
+    assert loss(eh=float("nan")) == ERR_VALUE
+    assert loss(T=0) == OK
+
+
 def test_ppo_loss_validation(L):
     def ppo(lold=FAKE, behav=None, T=10, el=0.2, eh=0.28, counts=FAKE, ws=FAKE, ws_bytes=1 << 30):
         return L.sao_ppo_loss(FAKE, lold, behav, FAKE, FAKE, T, el, eh, None, FAKE, FAKE, FAKE, counts, ws,
