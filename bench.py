@@ -84,25 +84,118 @@ def copy_calibration(nbytes: int = 1 << 30):
     print(json.dumps({"copy_bytes": nbytes, "launches": 3}), flush=True)
 
 
-def vendor_gemm(db, t_act: int, torch, reps: int = 3):
-    """torch.matmul (hipBLASLt) in bf16 at the forward's shape (T_act x H) . (H x V), bf16 out: a
-    library GEMM on the same operands, for context only (it is run, never inspected)."""
-    h = db.hidden[:t_act].contiguous()
-    w_t = db.w_head.t().contiguous()
-    out = torch.matmul(h, w_t)
-    torch.cuda.synchronize()
-    a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    for _ in range(reps):
-        torch.matmul(h, w_t, out=out)
-    z.record()
-    torch.cuda.synchronize()
-    ms = a.elapsed_time(z) / reps
-    flops = 2.0 * t_act * w_t.shape[1] * h.shape[1]
-    del out, w_t, h
+def backward_vocab_block(T: int, V: int) -> int:
+    """Vocabulary rows per block of sao_loss_backward for T token rows (the rule of
+    csrc/layout.hpp: a 16,384-row target, doubled up to 65,536 while the dz product
+    has fewer than 8192 tiles, then V cut into that many equal 256-row multiples)."""
+    tiles_t = -(-T // 256)
+    vc = 16384
+    while vc < 65536 and tiles_t * (vc // 256) < 8192:
+        vc *= 2
+    blocks = -(-V // vc)
+    return -(-(-(-V // blocks)) // 256) * 256
+
+
+class ClockSampler:
+    """The GPU's graphics clock (mean over its XCDs) and socket power, sampled every
+    ~10 ms in a thread while the timed steps run (amdsmi; None where it is not
+    available)."""
+
+    def __init__(self, index: int = 0, period: float = 0.01):
+        import threading
+        self.samples, self.period, self.err = [], period, None
+        self._stop = threading.Event()
+        self._thread = None
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            self._smi = amdsmi
+            self._h = amdsmi.amdsmi_get_processor_handles()[index]
+            self._read()
+        except Exception as e:  # noqa: BLE001 - the clock is a reported extra, never required
+            self._smi, self.err = None, repr(e)[:200]
+
+    def _read(self):
+        m = self._smi.amdsmi_get_gpu_metrics_info(self._h)
+        clks = [float(c) for c in m["current_gfxclks"] if isinstance(c, (int, float))]
+        power = m.get("current_socket_power")
+        return (sum(clks) / len(clks), float(power) if isinstance(power, (int, float)) else float("nan"))
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                self.samples.append(self._read())
+            except Exception as e:  # noqa: BLE001
+                self.err = repr(e)[:200]
+                return
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        import threading
+        if self._smi is not None:
+            self._thread = threading.Thread(target=self._run, daemon=True)
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self._thread is not None:
+            self._thread.join()
+        return False
+
+    def summary(self):
+        if not self.samples:
+            return {"gfx_clock_mhz": None, "note": self.err or "no samples"}
+        a = np.asarray(self.samples)
+        clk, pw = a[:, 0], a[:, 1]
+        return {"gfx_clock_mhz": {"median": float(np.median(clk)), "min": float(clk.min()), "max": float(clk.max()),
+                                  "samples": int(clk.size)},
+                "socket_power_w": {"median": float(np.nanmedian(pw)) if np.isfinite(pw).any() else None},
+                "note": "amdsmi GPU metrics, sampled every 10 ms over the timed steps: current graphics clock "
+                        "(mean over the 8 XCDs) and socket power"}
+
+
+def vendor_gemm(db, t_act: int, t_grad: int, vc: int, torch, reps: int = 3):
+    """torch.matmul (hipBLASLt) in bf16 at the four head-contraction shapes the
+    library runs on MFMA, for context only (run, never inspected):
+      forward       (T_act x H) . (H x V)       on the batch's hidden rows and W_head
+      dz recompute  (T_grad x H) . (H x Vb)     one backward vocabulary block of W_head
+      dH            (T_grad x Vb) . (Vb x H)
+      dW            (Vb x T_grad) . (T_grad x H)
+    Vb is the library's full backward block. Every operand is contiguous (no
+    transposed views); the dz operands are random, scaled like small gradients.
+    The library kernels' own times come from the kernel trace of the same run."""
+    H = db.hidden.shape[1]
+    w = db.w_head
+    gen = torch.Generator(device=db.hidden.device).manual_seed(7)
+    hg = db.hidden[:t_grad].contiguous()
+    dz = (torch.randn(t_grad, vc, generator=gen, device=db.hidden.device) * 1e-4).to(torch.bfloat16)
+    shapes = {
+        "forward": (lambda: db.hidden[:t_act].contiguous(), lambda: w.t().contiguous(), t_act, w.shape[0], H),
+        "dz_recompute": (lambda: hg, lambda: w[:vc].t().contiguous(), t_grad, vc, H),
+        "dH": (lambda: dz, lambda: w[:vc].contiguous(), t_grad, H, vc),
+        "dW": (lambda: dz.t().contiguous(), lambda: hg, vc, H, t_grad),
+    }
+    out = {}
+    for name, (fa, fb, M, N, K) in shapes.items():
+        a, b = fa(), fb()
+        c = torch.matmul(a, b)
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(reps):
+            torch.matmul(a, b, out=c)
+        ev1.record()
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / reps
+        flops = 2.0 * M * N * K
+        out[name] = {"op": f"torch.matmul bf16 ({M} x {K}) . ({K} x {N})", "M": M, "N": N, "K": K, "ms": ms,
+                     "TFLOP/s": flops / ms / 1e9, "frac": flops / ms / 1e9 / PEAK_BF16_TFLOPS}
+        del a, b, c
+        torch.cuda.empty_cache()
+    del hg, dz
     torch.cuda.empty_cache()
-    return {"op": "torch.matmul bf16 (T_act x H) @ (H x V)", "ms": ms, "TFLOP/s": flops / ms / 1e9,
-            "frac": flops / ms / 1e9 / PEAK_BF16_TFLOPS}
+    return out
 
 
 def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
@@ -274,20 +367,23 @@ def log(msg):
 
 
 def cpu_baseline(batch, ref_logp, rows: int, seed: int = 0):
-    """The oracle on a bounded sample: `rows` loss-mask tokens through the head pass
-    (forward, and backward for those with g != 0), plus the whole-batch scan and
-    loss; scaled to the whole batch by the share of loss-mask tokens sampled."""
+    """The oracle on a bounded sample: `rows` loss-mask tokens (default: a quarter of
+    them) through the head pass (forward, and backward for those with g != 0), plus
+    the whole-batch scan and loss; scaled to the whole batch by the share of
+    loss-mask tokens sampled."""
     import oracle
     from synth import rollout_logprobs
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        blas = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
+        blas = None
+    cores = len(os.sched_getaffinity(0))
     cfg = batch.cfg
     act = np.nonzero(batch.mask)[0]
     rng = np.random.default_rng(seed)
-    sample = np.sort(rng.choice(act, size=min(rows, act.size), replace=False))
+    n = act.size // 4 if rows <= 0 else min(rows, act.size)
+    sample = np.sort(rng.choice(act, size=n, replace=False))
     t0 = time.perf_counter()
     w64 = batch.w_head.astype(np.float64)
     adv, ret, N = oracle.advantage(batch.values, batch.rewards, batch.mask, batch.cu_seqlens, cfg.gamma,
@@ -302,10 +398,11 @@ def cpu_baseline(batch, ref_logp, rows: int, seed: int = 0):
     oracle.loss_backward(batch.hidden, None, batch.target, lse, g, w64=w64)
     t_head = time.perf_counter() - t1
     est = t_scan + t_head * act.size / sample.size
-    return {"value": batch.T / est, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{sample.size} of {act.size} loss-mask tokens through the fp64 head forward+backward "
-                      f"({t_head:.1f} s, scaled by {act.size / sample.size:.1f}) plus the whole-batch "
-                      f"scan and loss ({t_scan:.1f} s); W_head widening to fp64 excluded"}
+    return {"value": batch.T / est, "unit": "tokens/s", "cores": cores, "blas_threads": blas, "kind": "oracle",
+            "sample": f"{sample.size} of {act.size} loss-mask tokens ({sample.size / act.size:.0%}) through the "
+                      f"fp64 head forward+backward ({t_head:.1f} s, scaled by {act.size / sample.size:.2f}) plus "
+                      f"the whole-batch scan and loss ({t_scan:.1f} s); W_head widening to fp64 excluded; "
+                      f"{cores} host cores visible, BLAS on {blas} threads"}
 
 
 def main():
@@ -314,7 +411,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="c2", choices=sorted(WORKLOAD_TEXT))
-    ap.add_argument("--cpu-rows", type=int, default=4096, help="loss-mask tokens in the oracle sample")
+    ap.add_argument("--cpu-rows", type=int, default=0,
+                    help="loss-mask tokens in the oracle sample (default 0: a quarter of them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (counter calibration)")
@@ -444,12 +542,14 @@ def main():
         a.record()
     torch.cuda.synchronize()
     log(f"timing {args.steps} steps")
+    clock = ClockSampler(dev.index or 0)
     torch.cuda.synchronize()
-    step_ev[0].record()
-    for i in range(args.steps):
-        step(fwd_ev[i])
-        step_ev[i + 1].record()
-    torch.cuda.synchronize()
+    with clock:
+        step_ev[0].record()
+        for i in range(args.steps):
+            step(fwd_ev[i])
+            step_ev[i + 1].record()
+        torch.cuda.synchronize()
     B.time_kernel(B.KERNEL_NONE, None, None)
     per_step = [step_ev[i].elapsed_time(step_ev[i + 1]) for i in range(args.steps)]
     ms = step_ev[0].elapsed_time(step_ev[-1]) / args.steps
@@ -484,14 +584,16 @@ def main():
                     "max": float(np.max(per_step))},
         "device": {"name": torch.cuda.get_device_properties(dev).name,
                    "arch": getattr(torch.cuda.get_device_properties(dev), "gcnArchName", ""),
-                   "compute_units": torch.cuda.get_device_properties(dev).multi_processor_count},
+                   "compute_units": torch.cuda.get_device_properties(dev).multi_processor_count,
+                   **clock.summary()},
     }
     out["breakdown"] = breakdown(step, T, H, V, esz, t_act, t_grad, torch)
     if args.vendor_gemm:
         log("vendor GEMM (context)")
-        out["vendor_gemm_context"] = vendor_gemm(db, t_act, torch)
+        vc = backward_vocab_block(chunk, V) if cfg.backward else V
+        out["vendor_gemm_context"] = vendor_gemm(db, t_act, max(t_grad // len(chunks), 1), vc, torch)
     if not args.no_cpu_baseline:
-        log(f"cpu baseline over {args.cpu_rows} rows")
+        log("cpu baseline over " + (f"{args.cpu_rows} rows" if args.cpu_rows > 0 else "a quarter of the rows"))
         out["cpu_baseline"] = cpu_baseline(batch, ref_logp, args.cpu_rows)
     print(json.dumps(out), flush=True)
 

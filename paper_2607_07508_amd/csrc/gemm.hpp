@@ -336,6 +336,16 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// One accumulator element, read out of its AGPR at this point of the program.
+// Left to itself the compiler moves all 256 accumulators to VGPRs as soon as the
+// K loop ends, which leaves no room for anything else in an epilogue and spills;
+// reading each element where it is used keeps the epilogue's VGPRs few.
+__device__ __forceinline__ float acc_read(float x) {
+  float r;
+  asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(r) : "a"(x));
+  return r;
+}
+
 // Row index inside the 256-row tile of accumulator (mi, register r) for this lane.
 __device__ __forceinline__ int acc_row(int wm, int mi, int r, int lane) {
   return wm * (kBM / 2) + mi * 32 + (r & 3) + 8 * (r >> 2) + 4 * (lane >> 5);

@@ -143,10 +143,17 @@ __global__ __launch_bounds__(256) void k_gather_rows(const typename E::storage* 
 // ------------------------------------------------------------------------- //
 // Forward: online log-sum-exp epilogue
 // ------------------------------------------------------------------------- //
+// kMasked: the launch covers the last, partial vocabulary tile (rows at or past
+// M read as -inf); otherwise every tile of the launch has 256 valid rows. The
+// two cases are separate launches, so that each kernel holds a single epilogue
+// body: with both in one kernel the compiler moves the accumulators to VGPRs
+// ahead of the branch between them and spills.
+template <bool kMasked>
 struct EpiLse {
-  float2* part;   // [m_tiles][ldp] (max, sum exp) per token and vocabulary tile
+  float2* part;   // [vocabulary tile][ldp] (max, sum exp) per token
   int64_t ldp;
-  int64_t M;      // vocabulary size
+  int64_t M;      // valid vocabulary rows of this launch
+  int64_t tile0;  // vocabulary tile of this launch's first tile
   float rm[kNI], rs[kNI];
 
   __device__ __forceinline__ void begin(int64_t, int, int, int) {
@@ -158,45 +165,47 @@ struct EpiLse {
   }
 
   // Running (max, sum exp) per token column over this wave's 128 vocabulary
-  // rows; with kMasked, rows at or past the vocabulary end (last tile only)
-  // read as -inf. The accumulators themselves are left untouched so they can
-  // stay in AGPRs.
-  template <bool kMasked>
+  // rows; with kMasked, rows at or past the vocabulary end read as -inf. The
+  // accumulators themselves are left untouched so they can stay in AGPRs.
   __device__ __forceinline__ void update(const f32x16_t (&acc)[kMI][kNI], int lim) {
-    auto z_at = [&](int mi, int ni, int r) -> float {
-      const int off = mi * 32 + (r & 3) + 8 * (r >> 2);
-      return !kMasked || off < lim ? acc[mi][ni][r] : -__builtin_inff();
-    };
+    // One token column at a time: its 64 accumulators are read out of their
+    // AGPRs into VGPRs, reduced to a max, then to a sum of exponentials.
 #pragma unroll
     for (int ni = 0; ni < kNI; ++ni) {
+      float z[kMI * 16];
+#pragma unroll
+      for (int mi = 0; mi < kMI; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int off = mi * 32 + (r & 3) + 8 * (r >> 2);
+          const float x = acc_read(acc[mi][ni][r]);
+          z[mi * 16 + r] = !kMasked || off < lim ? x : -__builtin_inff();
+        }
       float tmax = -__builtin_inff();
 #pragma unroll
-      for (int mi = 0; mi < kMI; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, z_at(mi, ni, r));
+      for (int i = 0; i < kMI * 16; ++i) tmax = fmaxf(tmax, z[i]);
       const float mn = fmaxf(rm[ni], tmax);
-      if (mn == -__builtin_inff()) continue;
-      const float sc = mn * kLog2e;
-      float s = rs[ni] * fast_exp2(fmaf(rm[ni], kLog2e, -sc));
+      if (mn != -__builtin_inff()) {
+        const float sc = mn * kLog2e;
+        float s = rs[ni] * fast_exp2(fmaf(rm[ni], kLog2e, -sc));
 #pragma unroll
-      for (int mi = 0; mi < kMI; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s += fast_exp2(fmaf(z_at(mi, ni, r), kLog2e, -sc));
-      rm[ni] = mn;
-      rs[ni] = s;
+        for (int i = 0; i < kMI * 16; ++i) s += fast_exp2(fmaf(z[i], kLog2e, -sc));
+        rm[ni] = mn;
+        rs[ni] = s;
+      }
     }
   }
 
   __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t, int wm, int,
                                        int lane, void*) {
-    // Vocabulary rows from this wave's first row; the lane's rows sit at offsets
-    // up to 123 past it plus 4 (lane >> 5), so 128 rows leave nothing to mask.
-    const int64_t rows = M - m0 - wm * (kBM / 2);
-    if (rows >= kBM / 2) {
-      update<false>(acc, 0);
-    } else {
+    if constexpr (kMasked) {
+      // Vocabulary rows from this wave's first row; the lane's rows sit at offsets
+      // up to 123 past it plus 4 (lane >> 5).
+      const int64_t rows = M - m0 - wm * (kBM / 2);
       const int64_t lim64 = rows - 4 * (lane >> 5);
-      update<true>(acc, lim64 > kBM ? kBM : static_cast<int>(lim64));
+      update(acc, lim64 > kBM ? kBM : static_cast<int>(lim64));
+    } else {
+      update(acc, kBM);
     }
   }
 
@@ -218,20 +227,21 @@ struct EpiLse {
       for (int ni = 0; ni < kNI; ++ni) {
         const float2 o = sh[acc_col(wn, ni, lane)];
         lse_merge(rm[ni], rs[ni], o.x, o.y);
-        part[static_cast<int64_t>(mg) * ldp + n0 + acc_col(wn, ni, lane)] = make_float2(rm[ni], rs[ni]);
+        part[(tile0 + mg) * ldp + n0 + acc_col(wn, ni, lane)] = make_float2(rm[ni], rs[ni]);
       }
     }
   }
 };
 
-template <class E>
+template <class E, bool kMasked>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t V) {
+void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t tile0) {
   __shared__ v4u lds[kStages][kStageChunks];
-  EpiLse epi;
+  EpiLse<kMasked> epi;
   epi.part = part;
   epi.ldp = ldp;
-  epi.M = V;
+  epi.M = s.m;
+  epi.tile0 = tile0;
   gemm_body<E, false, false>(s, epi, lds);
 }
 
@@ -326,8 +336,9 @@ __device__ __forceinline__ void store4<F32>(float* p, const float (&d)[4]) {
 // dz_{t,v} = g_t (1[v = y_t] - exp(z_{t,v} - lse_t)) for one vocabulary block, stored
 // token-major dz[c][v - v0] (row stride ldz). The dH product reads it K-major, the
 // dW product MN-major, so no transposed copy is written. Columns past the block's
-// valid vocabulary rows hold zeros.
-template <class E>
+// valid vocabulary rows hold zeros. kMasked: the launch covers the block's last,
+// partial vocabulary tile (a launch of its own, like the forward's).
+template <class E, bool kMasked>
 struct EpiDz {
   typename E::storage* dz;
   int64_t ldz;
@@ -355,13 +366,12 @@ struct EpiDz {
   // row of a token lies in a given tile rarely, so the one-hot term is a branch
   // on yt (the target's tile row, or far outside), and rows at or past the end
   // of the block (last tile only, kMasked) are zero.
-  template <bool kMasked>
   __device__ __forceinline__ void dz4(const f32x16_t (&acc)[kMI][kNI], int mi, int ni, int j, int vt,
                                       int rows, float (&d)[4]) const {
     float p[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      p[e] = fast_exp2(fmaf(acc[mi][ni][4 * j + e], kLog2e, -ll[ni]));
+      p[e] = fast_exp2(fmaf(acc_read(acc[mi][ni][4 * j + e]), kLog2e, -ll[ni]));
       d[e] = gl[ni] * -p[e];
     }
     const unsigned k = static_cast<unsigned>(yt[ni] - vt);
@@ -384,10 +394,9 @@ struct EpiDz {
 
   __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t n0, int wm, int wn,
                                        int lane, void* smem) {
-    // Valid rows of this tile, and whether all of this wave's 128 rows are.
+    // Valid rows of this tile (all 256 unless kMasked).
     const int64_t rows64 = m_valid - m0;
     const int rows = rows64 > kBM ? kBM : static_cast<int>(rows64);
-    const bool full = rows >= (wm + 1) * (kBM / 2);
 #pragma unroll
     for (int ni = 0; ni < kNI; ++ni) {
       const int64_t y = yl[ni] - m0;
@@ -397,29 +406,23 @@ struct EpiDz {
       // Stage the 256 x 256 bf16 tile in LDS as [t][v] (128 KB), then write it
       // with 16-byte stores.
       v4u* tile16 = static_cast<v4u*>(smem);       // [256 rows][32 chunks]
-      auto stage = [&](auto masked) {
 #pragma unroll
-        for (int ni = 0; ni < kNI; ++ni) {
-          const int t = acc_col(wn, ni, lane);
+      for (int ni = 0; ni < kNI; ++ni) {
+        const int t = acc_col(wn, ni, lane);
 #pragma unroll
-          for (int mi = 0; mi < kMI; ++mi) {
+        for (int mi = 0; mi < kMI; ++mi) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int vl = acc_row(wm, mi, 4 * j, lane);   // multiple of 4
-              float d[4];
-              dz4<decltype(masked)::value>(acc, mi, ni, j, vl, rows, d);
-              const uint32_t lo = pack_bf16x2(d[0], d[1]);
-              const uint32_t hi = pack_bf16x2(d[2], d[3]);
-              uint2* p = reinterpret_cast<uint2*>(tile16 + t * 32 + tswz(t, vl >> 3)) + ((vl >> 2) & 1);
-              *p = make_uint2(lo, hi);
-            }
+          for (int j = 0; j < 4; ++j) {
+            const int vl = acc_row(wm, mi, 4 * j, lane);   // multiple of 4
+            float d[4];
+            dz4(acc, mi, ni, j, vl, rows, d);
+            const uint32_t lo = pack_bf16x2(d[0], d[1]);
+            const uint32_t hi = pack_bf16x2(d[2], d[3]);
+            uint2* p = reinterpret_cast<uint2*>(tile16 + t * 32 + tswz(t, vl >> 3)) + ((vl >> 2) & 1);
+            *p = make_uint2(lo, hi);
           }
         }
-      };
-      if (full)
-        stage(std::false_type{});
-      else
-        stage(std::true_type{});
+      }
       __syncthreads();
       const int tid = threadIdx.x;
       // [t][v]: thread takes chunk c of row t for 32 (t, c) pairs.
@@ -441,7 +444,7 @@ struct EpiDz {
           for (int j = 0; j < 4; ++j) {
             const int vl = acc_row(wm, mi, 4 * j, lane);
             float d[4];
-            dz4<true>(acc, mi, ni, j, vl, rows, d);
+            dz4(acc, mi, ni, j, vl, rows, d);
             store4<E>(row + m0 + vl, d);
           }
         }
@@ -484,9 +487,9 @@ struct EpiAcc {
   __device__ __forceinline__ void finish(int, int64_t, int, int, int, void*) {}
 };
 
-template <class E>
+template <class E, bool kMasked>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void k_bwd_dz(GemmShape s, EpiDz<E> epi) {
+void k_bwd_dz(GemmShape s, EpiDz<E, kMasked> epi) {
   __shared__ v4u lds[kStages][kStageChunks];
   gemm_body<E, false, false>(s, epi, lds);
 }
@@ -575,12 +578,25 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
   const int rows4 = static_cast<int>(L.t_pad / 4);
   hipLaunchKernelGGL(k_gather_rows<E>, dim3(rows4), dim3(256), 0, st, static_cast<const S*>(hidden),
                      ld_hidden, H, idx, count, hc, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
-  GemmShape s = make_shape(w_head, ld_w, V, hc, H, T, H);
-  s.n_dev = count;
+  // The vocabulary tiles with 256 valid rows, then (when V is not a multiple of
+  // 256) the last, partial tile in a launch of its own with the masked epilogue.
+  const int64_t full_tiles = V / kBM;
+  const int64_t rem = V - full_tiles * kBM;
   const KernelTimer& tm = kernel_timer();
   const bool timed = tm.kernel == SAO_KERNEL_HEAD_FORWARD && tm.start && tm.stop;
   if (timed) (void)hipEventRecord(tm.start, st);
-  hipLaunchKernelGGL(k_head_fwd<E>, dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad, V);
+  if (full_tiles > 0) {
+    GemmShape s = make_shape(w_head, ld_w, full_tiles * kBM, hc, H, T, H);
+    s.n_dev = count;
+    hipLaunchKernelGGL((k_head_fwd<E, false>), dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad,
+                       int64_t{0});
+  }
+  if (rem > 0) {
+    GemmShape s = make_shape(static_cast<const S*>(w_head) + full_tiles * kBM * ld_w, ld_w, rem, hc, H, T, H);
+    s.n_dev = count;
+    hipLaunchKernelGGL((k_head_fwd<E, true>), dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad,
+                       full_tiles);
+  }
   if (timed) (void)hipEventRecord(tm.stop, st);
   hipLaunchKernelGGL(k_fwd_finalize<E>, dim3(rows4), dim3(256), 0, st, part, L.t_pad,
                      static_cast<int>(L.m_tiles), hc, H, static_cast<const S*>(w_head), ld_w, V, idx,
@@ -621,11 +637,21 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
   for (int64_t vb = 0; vb < L.n_vblocks; ++vb) {
     const int64_t v0 = vb * L.vc;
     const int64_t vlen = (V - v0) < L.vc ? (V - v0) : L.vc;
-    // (A) z^T[v][t] = W[v0 + v] . Hg[t] -> dz[t][v]
-    GemmShape sa = make_shape(w + v0 * ld_w, ld_w, vlen, hg, H, T, H);
-    sa.n_dev = count;
-    EpiDz<E> ez{dz, L.vc, vlen, v0, g_c, lse_c, y_c, {}, {}, {}};
-    hipLaunchKernelGGL(k_bwd_dz<E>, dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez);
+    // (A) z^T[v][t] = W[v0 + v] . Hg[t] -> dz[t][v]: the block's tiles with 256 valid
+    // vocabulary rows, then its partial last tile (if any) with the masked epilogue.
+    const int64_t full_v = vlen / kBM * kBM;
+    if (full_v > 0) {
+      GemmShape sa = make_shape(w + v0 * ld_w, ld_w, full_v, hg, H, T, H);
+      sa.n_dev = count;
+      EpiDz<E, false> ez{dz, L.vc, full_v, v0, g_c, lse_c, y_c, {}, {}, {}, {}};
+      hipLaunchKernelGGL((k_bwd_dz<E, false>), dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez);
+    }
+    if (vlen > full_v) {
+      GemmShape sa = make_shape(w + (v0 + full_v) * ld_w, ld_w, vlen - full_v, hg, H, T, H);
+      sa.n_dev = count;
+      EpiDz<E, true> ez{dz + full_v, L.vc, vlen - full_v, v0 + full_v, g_c, lse_c, y_c, {}, {}, {}, {}};
+      hipLaunchKernelGGL((k_bwd_dz<E, true>), dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez);
+    }
     // (B) dH[t][h] += sum_v dz[t][v] W[v0 + v][h]: A = dz K-major, B = W MN-major
     // With few token rows the dH tiles cannot fill the GPU: K (the vocabulary)
     // is cut into dh_pieces pieces, each adding into its own accumulator.

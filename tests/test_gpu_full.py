@@ -3,8 +3,8 @@
 Log-probs and lse are compared on every loss-mask row against the oracle values
 stored by tests/golden/make_full_logprobs.py; advantages, flags, counts, loss
 and g on every token (the oracle scan and loss are cheap); dhidden and dW_head
-on sampled rows that the oracle computes one by one, plus exact zeros on every
-row with g = 0.
+on every element at c2 (the bench's workload), on sampled rows that the oracle
+computes one by one at c3 and c4, plus exact zeros on every row with g = 0.
 """
 import numpy as np
 import pytest
@@ -25,7 +25,26 @@ def _gpu():
         pytest.skip("no HIP device")
 
 
-def _full(name, backward, n_rows=24, seed=0):
+def _oracle_backward_every_row(b, ref_lse, g, w64, chunk=4096):
+    """The oracle's dH and dW over every token and vocabulary row, computed over
+    chunks of the rows with g != 0 (both are sums over tokens, so the chunks'
+    dW add up to the whole), with a progress line per chunk."""
+    live = np.nonzero(g)[0]
+    dH = np.zeros((b.T, b.cfg.H), dtype=np.float64)
+    dW = np.zeros((b.cfg.V, b.cfg.H), dtype=np.float64)
+    for s in range(0, live.size, chunk):
+        r = live[s:s + chunk]
+        gc = np.zeros_like(g)
+        gc[r] = g[r]
+        dh_c, dw_c = oracle.loss_backward(b.hidden, None, b.target, ref_lse, gc, w64=w64)
+        dH[r] = dh_c[r]
+        dW += dw_c
+        del dh_c, dw_c
+        say(f"{b.cfg.name}: oracle backward rows {s + r.size} of {live.size}")
+    return dH, dW
+
+
+def _full(name, backward, n_rows=24, seed=0, every_row=False):
     cfg = CONFIGS[name]
     say(f"{name}: generating T={cfg.T} H={cfg.H} V={cfg.V}")
     b = generate(cfg)
@@ -62,12 +81,19 @@ def _full(name, backward, n_rows=24, seed=0):
     rows = np.sort(rng.choice(live, size=n_rows, replace=False))
     vrows = np.unique(np.concatenate([b.target[rows[:n_rows // 2]], rng.choice(cfg.V, n_rows, replace=False),
                                       [0, cfg.V - 1]]))
-    say(f"{name}: oracle backward on {rows.size} token rows and {vrows.size} vocabulary rows")
     w64 = b.w_head.astype(np.float64)
-    dH, dW = oracle.loss_backward(b.hidden, None, b.target, ref_lse, g, dh_rows=rows, dw_rows=vrows, w64=w64)
-    check_grad(got["dh"][rows], dH[rows], None, "dhidden rows")
+    if every_row:
+        say(f"{name}: oracle backward on all {live.size} token rows with g != 0 and all {cfg.V} vocabulary rows")
+        dH, dW = _oracle_backward_every_row(b, ref_lse, g, w64)
+        check_grad(got["dh"], dH, np.nonzero(g == 0)[0], "dhidden (every row)")
+        check_grad(got["dw"], dW, None, "dw_head (every row)")
+        del dH, dW
+    else:
+        say(f"{name}: oracle backward on {rows.size} token rows and {vrows.size} vocabulary rows")
+        dH, dW = oracle.loss_backward(b.hidden, None, b.target, ref_lse, g, dh_rows=rows, dw_rows=vrows, w64=w64)
+        check_grad(got["dh"][rows], dH[rows], None, "dhidden rows")
+        check_grad(got["dw"][vrows], dW[vrows], None, "dw_head rows")
     assert (got["dh"][g == 0] == 0).all()
-    check_grad(got["dw"][vrows], dW[vrows], None, "dw_head rows")
     # the vocabulary sum of dz is 0 for every token, so sum_v dW_v = 0 up to rounding
     col = got["dw"].astype(np.float64).sum(axis=0)
     assert np.abs(col).max() <= 1e-2 * np.abs(got["dw"]).sum(axis=0).max()
@@ -114,7 +140,8 @@ def test_loss_kernel_alone_on_oracle_logprobs(name):
 
 @pytest.mark.skipif(not __import__("os").path.exists(path_for("c2")), reason="stored oracle values missing")
 def test_c2_full_forward_backward():
-    _full("c2", backward=True)
+    # every dH and dW element against the oracle (a few minutes of fp64 BLAS on the host)
+    _full("c2", backward=True, every_row=True)
 
 
 @pytest.mark.skipif(not __import__("os").path.exists(path_for("c1")), reason="stored oracle values missing")
