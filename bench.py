@@ -86,10 +86,10 @@ def copy_calibration(nbytes: int = 1 << 30):
 
 def backward_vocab_block(T: int, V: int) -> int:
     """Vocabulary rows per block of sao_loss_backward for T token rows (the rule of
-    csrc/layout.hpp: a 16,384-row target, doubled up to 65,536 while the dz product
+    csrc/layout.hpp: a 32,768-row target, doubled up to 65,536 while the dz product
     has fewer than 8192 tiles, then V cut into that many equal 256-row multiples)."""
     tiles_t = -(-T // 256)
-    vc = 16384
+    vc = 32768
     while vc < 65536 and tiles_t * (vc // 256) < 8192:
         vc *= 2
     blocks = -(-V // vc)

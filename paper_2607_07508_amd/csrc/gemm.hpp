@@ -455,16 +455,24 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   const int64_t slab_b = static_cast<int64_t>(G::kRows) * s.ldb * esz;
   const uint32_t lds0 = uniform_u32(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0])));
   v4u* lds_flat = &lds[0][0];
-  auto copy_one = [&](int q, int kt, int stage) {
+  // Scalar base address of slab kt of operand A or B (the slab's offset is
+  // uniform and goes into the base; the lanes' offsets stay fixed).
+  auto slab_ptr = [&](bool is_a, int kt) -> const char* {
+    const bool mn = is_a ? AMn : BMn;
+    const int64_t k_off = mn ? static_cast<int64_t>(kt) * (is_a ? slab_a : slab_b)
+                             : static_cast<int64_t>(kt) * kRowChunks * P * esz;
+    return static_cast<const char*>(uniform_ptr((is_a ? a_base : b_base) + k_off));
+  };
+  // Copy q of a slab whose A and B bases are ga and gb, into `stage`.
+  auto copy_at = [&](int q, const char* ga, const char* gb, int stage) {
     const bool is_a = q < QA;
     const int qq = is_a ? q : q - QA;
     const int slot = (is_a ? 0 : kAChunks) + (wave * (is_a ? QA : QB) + qq) * 64;
-    const bool mn = is_a ? AMn : BMn;
-    // The slab's offset is uniform and goes into the scalar base address.
-    const int64_t k_off = mn ? static_cast<int64_t>(kt) * (is_a ? slab_a : slab_b)
-                             : static_cast<int64_t>(kt) * kRowChunks * P * esz;
-    dma16(uniform_ptr((is_a ? a_base : b_base) + k_off), is_a ? offa[qq] : offb[qq],
+    dma16(is_a ? ga : gb, is_a ? offa[qq] : offb[qq],
           uniform_u32(lds0 + static_cast<uint32_t>(stage * kStageChunks + slot) * 16));
+  };
+  auto copy_one = [&](int q, int kt, int stage) {
+    copy_at(q, q < QA ? slab_ptr(true, kt) : nullptr, q < QA ? nullptr : slab_ptr(false, kt), stage);
   };
   auto inside_k = [&](int q, int kt) -> bool {
     const bool is_a = q < QA;
@@ -514,27 +522,35 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   constexpr int kCopyNext = kCopiesPerSlab - kCopyNow;
   static_assert(kCopyNow > 0 && kCopyNext > 0 && (kMI * kNI) % kCopyNow == 0 && (kMI * kNI) % kCopyNext == 0,
                 "copies spread evenly over a step's MFMAs");
-  bool carry = false;  // the previous iteration left copies of slab kt + 1 to step 0
-  for (int kt = 0; kt < nk; ++kt) {
+  // Whether the previous iteration left copies of slab kt + 1 to step 0 (a
+  // wave-uniform scalar, so that the copies' guards are scalar branches).
+  uint32_t carry = 0;
+  // One slab. In the steady state (kSteady: 1 <= kt <= nk - 4) every copy is
+  // issued, so those iterations carry no guards at all.
+  auto slab = [&](int kt, auto steady) {
+    constexpr bool kSteady = decltype(steady)::value;
     const int stage = kt % kStages;
     const int cstage = (kt + 1) % kStages;
     // K steps 0 .. kSteps-2 multiply f0 / f1 (even / odd steps) while reading
     // the next step's fragments from this stage. Step 0 also issues the copies
-    // of slab kt + 1 that the previous iteration left over.
+    // of slab kt + 1 that the previous iteration left over. The slab's scalar
+    // bases are formed once, not per copy.
     constexpr int kEveryNext = kMI * kNI / kCopyNext;
+    const char* ga1 = slab_ptr(true, kt + 1);
+    const char* gb1 = slab_ptr(false, kt + 1);
 #pragma unroll
     for (int st = 0; st + 1 < kSteps; ++st) {
       Frags& cur = st % 2 == 0 ? f0 : f1;
       Frags& nxt = st % 2 == 0 ? f1 : f0;
       mma_step_mix<E, AMn, BMn>(acc, cur, nxt, lds[stage], lds[stage] + kAChunks, st + 1, wm, wn, lane,
                                 [&](int t) {
-                                  if (st == 0 && t % kEveryNext == kEveryNext - 1 && carry)
-                                    copy_one(kCopyNow + t / kEveryNext, kt + 1, cstage);
+                                  if (st == 0 && t % kEveryNext == kEveryNext - 1 && (kSteady || carry))
+                                    copy_at(kCopyNow + t / kEveryNext, ga1, gb1, cstage);
                                 });
     }
     Frags& last = kSteps % 2 == 0 ? f1 : f0;
     const int kn = kt + kStages;  // the slab that refills this stage
-    if (kt + 1 < nk) {
+    if (kSteady || kt + 1 < nk) {
       const int rest = nk - kt - 2;
       wait_slabs_barrier<kCopiesPerSlab>(rest < kStages - 2 ? rest : kStages - 2);
     }
@@ -544,14 +560,21 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
     // stage: kCopyNow copies spread over this step's MFMAs, the rest over step 0
     // of the next slab; the last slab, when K ends inside it, is copied after
     // them with its zero fill.
-    const bool refill = kn < nk - 1 || (kn == nk - 1 && !tail);
+    const uint32_t refill = kSteady ? 1u : uniform_u32(kn < nk - 1 || (kn == nk - 1 && !tail) ? 1u : 0u);
+    const char* ga2 = slab_ptr(true, kn);
+    const char* gb2 = slab_ptr(false, kn);
     constexpr int kEveryNow = kMI * kNI / kCopyNow;
     mma_step_mix<E, AMn, BMn>(acc, last, f0, lds[cstage], lds[cstage] + kAChunks, 0, wm, wn, lane, [&](int t) {
-      if (t % kEveryNow == kEveryNow - 1 && refill) copy_one(t / kEveryNow, kn, stage);
+      if (t % kEveryNow == kEveryNow - 1 && (kSteady || refill)) copy_at(t / kEveryNow, ga2, gb2, stage);
     });
-    if (kn == nk - 1 && tail) copy_slab(kn, stage);
+    if (!kSteady && kn == nk - 1 && tail) copy_slab(kn, stage);
     carry = refill;
-  }
+  };
+  // kt = 0 (nothing carried), the steady iterations, then the last three.
+  int kt = 0;
+  if (nk > 0) slab(kt++, std::false_type{});
+  for (; kt <= nk - 4; ++kt) slab(kt, std::true_type{});
+  for (; kt < nk; ++kt) slab(kt, std::false_type{});
   // Every copy has landed (the last wait drained them); once every wave's LDS
   // reads have returned, the epilogue may use LDS as scratch.
   lds_barrier();

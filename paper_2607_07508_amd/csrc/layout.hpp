@@ -8,7 +8,7 @@ namespace sao {
 
 constexpr int64_t kTile = 256;
 constexpr int64_t kRowsPerCountBlock = 1024;  // rows per block of the compaction count
-constexpr int64_t kVocabBlock = 16384;        // vocabulary rows per backward dZ block (at least)
+constexpr int64_t kVocabBlock = 32768;        // vocabulary rows per backward dZ block (at least)
 constexpr int64_t kVocabBlockMax = 65536;     // ... and at most
 constexpr int kLossThreads = 256;
 constexpr int kLossPerThread = 8;
