@@ -26,6 +26,7 @@ import sys
 import time
 
 import numpy as np
+from typing import Optional
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -96,63 +97,41 @@ def backward_vocab_block(T: int, V: int) -> int:
     return -(-(-(-V // blocks)) // 256) * 256
 
 
-class ClockSampler:
-    """The GPU's graphics clock (mean over its XCDs) and socket power, sampled every
-    ~10 ms in a thread while the timed steps run (amdsmi; None where it is not
-    available)."""
+def wall_clock_khz() -> Optional[int]:
+    """The device's constant wall-clock rate (hipDeviceAttributeWallClockRate), in kHz."""
+    import ctypes
+    try:
+        hip = ctypes.CDLL("libamdhip64.so")
+        v = ctypes.c_int(0)
+        if hip.hipDeviceGetAttribute(ctypes.byref(v), 10017, 0) != 0:  # hipDeviceAttributeWallClockRate
+            return None
+        return int(v.value) or None
+    except OSError:
+        return None
 
-    def __init__(self, index: int = 0, period: float = 0.01):
-        import threading
-        self.samples, self.period, self.err = [], period, None
-        self._stop = threading.Event()
-        self._thread = None
-        try:
-            import amdsmi
-            amdsmi.amdsmi_init()
-            self._smi = amdsmi
-            self._h = amdsmi.amdsmi_get_processor_handles()[index]
-            self._read()
-        except Exception as e:  # noqa: BLE001 - the clock is a reported extra, never required
-            self._smi, self.err = None, repr(e)[:200]
 
-    def _read(self):
-        m = self._smi.amdsmi_get_gpu_metrics_info(self._h)
-        clks = [float(c) for c in m["current_gfxclks"] if isinstance(c, (int, float))]
-        power = m.get("current_socket_power")
-        return (sum(clks) / len(clks), float(power) if isinstance(power, (int, float)) else float("nan"))
-
-    def _run(self):
-        while not self._stop.is_set():
-            try:
-                self.samples.append(self._read())
-            except Exception as e:  # noqa: BLE001
-                self.err = repr(e)[:200]
-                return
-            self._stop.wait(self.period)
-
-    def __enter__(self):
-        import threading
-        if self._smi is not None:
-            self._thread = threading.Thread(target=self._run, daemon=True)
-            self._thread.start()
-        return self
-
-    def __exit__(self, *exc):
-        self._stop.set()
-        if self._thread is not None:
-            self._thread.join()
-        return False
-
-    def summary(self):
-        if not self.samples:
-            return {"gfx_clock_mhz": None, "note": self.err or "no samples"}
-        a = np.asarray(self.samples)
-        clk, pw = a[:, 0], a[:, 1]
-        return {"gfx_clock_mhz": {"median": float(np.median(clk)), "min": float(clk.min()), "max": float(clk.max()),
-                                  "samples": int(clk.size)},
-                "socket_power_w": {"median": float(np.nanmedian(pw)) if np.isfinite(pw).any() else None},
-                "note": "amdsmi GPU metrics, sampled every 10 ms over the timed steps: current graphics clock "
-                        "(mean over the 8 XCDs) and socket power"}
+def forward_clock(step, torch, dev, B) -> dict:
+    """The shader clock the head-forward kernel runs at: one more step (after the
+    timed ones) with the kernel's own per-workgroup records on, cycles
+    (s_memtime) over wall-clock time (s_memrealtime at the rate the runtime
+    reports). Weighted by workgroup time, over the step's forward launches."""
+    khz = wall_clock_khz()
+    slots = 1 << 18
+    rec = torch.zeros((slots, 3), dtype=torch.int64, device=dev)
+    try:
+        B.clock_samples(rec)          # each forward launch overwrites the records: the step's last one stays
+        step()
+        torch.cuda.synchronize()
+    finally:
+        B.clock_samples(None)
+    r = rec.cpu().numpy()
+    live = r[:, 2] > r[:, 1]
+    cycles, ticks = int(r[live, 0].sum()), int((r[live, 2] - r[live, 1]).sum())
+    if not khz or ticks == 0:
+        return {"forward_clock_mhz": None, "clock_note": "wall-clock rate or records unavailable"}
+    return {"forward_clock_mhz": cycles / (ticks / (khz * 1e3)) / 1e6,
+            "clock_note": "shader clock of k_head_fwd's workgroups over one step (s_memtime cycles over "
+                          "s_memrealtime time, last forward launch of the step)"}
 
 
 def vendor_gemm(db, t_act: int, t_grad: int, vc: int, torch, reps: int = 3):
@@ -196,6 +175,47 @@ def vendor_gemm(db, t_act: int, t_grad: int, vc: int, torch, reps: int = 3):
     del hg, dz
     torch.cuda.empty_cache()
     return out
+
+
+def mfma_ceiling(blocks: int = 2048, iters: int = 20000, reps: int = 3):
+    """What the bf16 MFMA pipe delivers with nothing else to issue: the probe library's
+    loop of 16 v_mfma_f32_32x32x16_bf16 per round on 256 accumulators, one wave per
+    SIMD (the head kernels' arrangement), for random, constant and refreshed-random
+    operands, with the clock the workgroups ran at. One JSON line per mode."""
+    import ctypes
+    import torch
+    from paper_2607_07508_amd import build as bld
+    if not torch.cuda.is_available():
+        print("the probe needs a HIP device", file=sys.stderr)
+        sys.exit(1)
+    lib = ctypes.CDLL(bld.PROBE_LIB)
+    fn = lib.sao_probe_mfma
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    clk = torch.zeros((blocks, 3), dtype=torch.int64, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+    khz = wall_clock_khz()
+    flops = 2.0 * 32 * 32 * 16 * 16 * 4 * blocks * iters
+    for mode, name in ((0, "random operands"), (1, "constant operands"), (2, "random operands refreshed per round")):
+        if fn(blocks, iters, mode, out.data_ptr(), clk.data_ptr(), st) != 0:
+            raise RuntimeError("probe launch failed")
+        torch.cuda.synchronize()
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn(blocks, iters, mode, out.data_ptr(), clk.data_ptr(), st)
+        z.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(z) / reps
+        r = clk.cpu().numpy()
+        cyc, ticks = float(r[:, 0].sum()), float((r[:, 2] - r[:, 1]).sum())
+        mhz = cyc / (ticks / (khz * 1e3)) / 1e6 if khz and ticks else None
+        tf = flops / ms / 1e9
+        print(json.dumps({"mode": "mfma_ceiling", "operands": name, "ms": ms, "TFLOP/s": tf,
+                          "frac": tf / PEAK_BF16_TFLOPS, "clock_mhz": mhz,
+                          "frac_at_clock": (tf / (PEAK_BF16_TFLOPS * mhz / 2400.0)) if mhz else None,
+                          "blocks": blocks, "iters": iters}), flush=True)
 
 
 def epilogue_sweep(exps=(20, 22, 24, 26), reps=20):
@@ -418,6 +438,8 @@ def main():
                     help="run only a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--vendor-gemm", action="store_true",
                     help="also time torch.matmul (bf16) at the forward's shape, as context (allocates the T_act x V output)")
+    ap.add_argument("--mfma-ceiling", action="store_true",
+                    help="run only the MFMA-only probe loop (random and constant operands), one line per mode")
     ap.add_argument("--epilogue-sweep", action="store_true",
                     help="HBM bandwidth of the scan and loss epilogue at T = 2^20 .. 2^26 (one line per size)")
     args = ap.parse_args()
@@ -426,6 +448,9 @@ def main():
         return
     if args.epilogue_sweep:
         epilogue_sweep()
+        return
+    if args.mfma_ceiling:
+        mfma_ceiling()
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -542,14 +567,12 @@ def main():
         a.record()
     torch.cuda.synchronize()
     log(f"timing {args.steps} steps")
-    clock = ClockSampler(dev.index or 0)
     torch.cuda.synchronize()
-    with clock:
-        step_ev[0].record()
-        for i in range(args.steps):
-            step(fwd_ev[i])
-            step_ev[i + 1].record()
-        torch.cuda.synchronize()
+    step_ev[0].record()
+    for i in range(args.steps):
+        step(fwd_ev[i])
+        step_ev[i + 1].record()
+    torch.cuda.synchronize()
     B.time_kernel(B.KERNEL_NONE, None, None)
     per_step = [step_ev[i].elapsed_time(step_ev[i + 1]) for i in range(args.steps)]
     ms = step_ev[0].elapsed_time(step_ev[-1]) / args.steps
@@ -585,7 +608,7 @@ def main():
         "device": {"name": torch.cuda.get_device_properties(dev).name,
                    "arch": getattr(torch.cuda.get_device_properties(dev), "gcnArchName", ""),
                    "compute_units": torch.cuda.get_device_properties(dev).multi_processor_count,
-                   **clock.summary()},
+                   **forward_clock(step, torch, dev, B)},
     }
     out["breakdown"] = breakdown(step, T, H, V, esz, t_act, t_grad, torch)
     if args.vendor_gemm:

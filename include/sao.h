@@ -15,7 +15,8 @@
  * Memory.   Every array argument is a DEVICE pointer owned by the caller. The
  *           library never allocates or frees caller-visible memory. Its only
  *           mutable host state is per calling thread (the last error message and
- *           the measurement hook of sao_debug_time_kernel), plus, per device, the
+ *           the measurement hooks sao_debug_time_kernel and
+ *           sao_debug_clock_samples), plus, per device, the
  *           address of sao_clipped_loss_noalloc's static scratch. Scratch space is the caller's `ws` buffer of
  *           `ws_bytes` bytes (device memory, 256-byte aligned), at least
  *           sao_workspace_size(...) bytes; its contents on entry are ignored.
@@ -380,6 +381,17 @@ sao_status_t sao_value_loss(const void* hidden, int64_t ld_hidden, const void* w
 #define SAO_KERNEL_NONE         0
 #define SAO_KERNEL_HEAD_FORWARD 1  /* the MFMA head-forward kernel of sao_token_logprob */
 void sao_debug_time_kernel(int kernel, void* start_event, void* stop_event);
+
+/*
+ * Measurement hook, not part of the pass. For the calling thread, makes the next
+ * launches of the head-forward kernel record, for each workgroup b < slots, three
+ * int64 values in the caller's device buffer `records` (3 * slots int64): the
+ * shader-clock cycles the workgroup ran (s_memtime difference) and its start and
+ * end on the device's constant-rate wall clock (s_memrealtime). Summed cycles
+ * over summed wall-clock time give the clock the kernel ran at. NULL or
+ * slots <= 0 disables it. Each launch overwrites the records of the previous one.
+ */
+void sao_debug_clock_samples(void* records, int64_t slots);
 
 #ifdef __cplusplus
 }

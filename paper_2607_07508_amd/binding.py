@@ -26,7 +26,7 @@ EXPORTS = ("sao_status_string", "sao_last_error_message", "sao_version", "sao_wo
            "sao_token_logprob", "sao_advantage", "sao_clipped_loss", "sao_loss_backward",
            "sao_value_forward", "sao_value_loss", "sao_ppo_loss", "sao_explained_variance", "sao_step_advantage",
            "sao_group_advantage", "sao_running_mean_advantage", "sao_clipped_loss_noalloc",
-           "sao_debug_time_kernel")
+           "sao_debug_time_kernel", "sao_debug_clock_samples")
 KERNEL_NONE, KERNEL_HEAD_FORWARD = 0, 1
 
 
@@ -69,6 +69,7 @@ _SIGS = {
                                                   ctypes.c_int32, _p, _p, _p, _p, _p, _p, _p, _p, ctypes.c_size_t,
                                                   _p]),
     "sao_debug_time_kernel": (None, [ctypes.c_int, _p, _p]),
+    "sao_debug_clock_samples": (None, [_p, _i64]),
 }
 
 _lib = None
@@ -475,3 +476,15 @@ def time_kernel(kernel: int, start: Optional[torch.cuda.Event], stop: Optional[t
         lib().sao_debug_time_kernel(KERNEL_NONE, None, None)
         return
     lib().sao_debug_time_kernel(kernel, start.cuda_event, stop.cuda_event)
+
+
+def clock_samples(records: Optional[torch.Tensor]) -> None:
+    """Make the next head-forward launches record per-workgroup (cycles, wall-clock
+    start, wall-clock end) into `records` (int64 [slots, 3] on the device); None
+    disables."""
+    if records is None:
+        lib().sao_debug_clock_samples(None, 0)
+        return
+    if records.dtype != torch.int64 or records.dim() != 2 or records.shape[1] != 3 or not records.is_contiguous():
+        raise ValueError("records must be a contiguous int64 [slots, 3] tensor")
+    lib().sao_debug_clock_samples(records.data_ptr(), records.shape[0])

@@ -15,6 +15,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsao.so")
+PROBE_LIB = os.path.join(PKG, "libsao_probe.so")   # bench.py --mfma-ceiling only
 ARCH = os.environ.get("SAO_OFFLOAD_ARCH", "gfx950")
 
 SOURCES = ["api.cpp", "runtime.cpp", "head.hip", "scan.hip", "step.hip", "baseline.hip", "loss.hip", "ev.hip", "value.hip"]
@@ -55,8 +56,16 @@ def build(extra=(), verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, LIB)
+    # the measurement probe of bench.py --mfma-ceiling, a library of its own
+    pobj = _compile("probe.hip", list(extra))
+    ptmp = PROBE_LIB + ".tmp"
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", ptmp, pobj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    os.replace(ptmp, PROBE_LIB)
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {PROBE_LIB}")
     return LIB
 
 

@@ -171,12 +171,14 @@ __device__ __forceinline__ const void* uniform_ptr(const void* p) {
 
 // Direct copy of 16 bytes per lane from global memory (uniform base `g` plus the
 // lane's byte offset `off`) into LDS: lane l writes LDS bytes [m0 + 16 l, +16),
-// m0 being the wave-uniform LDS byte address `lds_addr`. Issued as inline
-// assembly so that the compiler does not insert its conservative full waits
-// before every LDS read; completion is tracked with explicit vmcnt waits.
-__device__ __forceinline__ void dma16(const void* g, uint32_t off, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(g), "s"(lds_addr)
-               : "memory", "m0");
+// m0 being the wave-uniform LDS byte address lds_base + lds_off (summed straight
+// into m0). Issued as inline assembly so that the compiler does not insert its
+// conservative full waits before every LDS read; completion is tracked with
+// explicit vmcnt waits.
+__device__ __forceinline__ void dma16(const void* g, uint32_t off, uint32_t lds_base, uint32_t lds_off) {
+  asm volatile("s_add_u32 m0, %2, %3\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(g), "s"(lds_base),
+               "s"(lds_off)
+               : "memory", "m0", "scc");
 }
 
 // This wave's copies except the N most recent have landed in LDS, its LDS
@@ -469,7 +471,8 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
     const int qq = is_a ? q : q - QA;
     const int slot = (is_a ? 0 : kAChunks) + (wave * (is_a ? QA : QB) + qq) * 64;
     dma16(is_a ? ga : gb, is_a ? offa[qq] : offb[qq],
-          uniform_u32(lds0 + static_cast<uint32_t>(stage * kStageChunks + slot) * 16));
+          uniform_u32(lds0 + static_cast<uint32_t>(stage * kStageChunks) * 16),
+          uniform_u32(static_cast<uint32_t>(slot) * 16));
   };
   auto copy_one = [&](int q, int kt, int stage) {
     copy_at(q, q < QA ? slab_ptr(true, kt) : nullptr, q < QA ? nullptr : slab_ptr(false, kt), stage);

@@ -233,16 +233,29 @@ struct EpiLse {
   }
 };
 
+// With `clk` (a measurement hook, normally null), workgroup b records the
+// shader-clock cycles it ran (s_memtime) and its start and end on the constant
+// wall clock (s_memrealtime) in clk[3b .. 3b+2], for b < clk_slots.
 template <class E, bool kMasked>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t tile0) {
+void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t tile0, int64_t* clk, int64_t clk_slots) {
   __shared__ v4u lds[kStages][kStageChunks];
+  const uint64_t c0 = clk ? __builtin_amdgcn_s_memtime() : 0;
+  const uint64_t r0 = clk ? __builtin_amdgcn_s_memrealtime() : 0;
   EpiLse<kMasked> epi;
   epi.part = part;
   epi.ldp = ldp;
   epi.M = s.m;
   epi.tile0 = tile0;
   gemm_body<E, false, false>(s, epi, lds);
+  if (clk && threadIdx.x == 0 && static_cast<int64_t>(blockIdx.x) < clk_slots) {
+    const uint64_t c1 = __builtin_amdgcn_s_memtime();
+    const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
+    int64_t* rec = clk + 3 * static_cast<int64_t>(blockIdx.x);
+    rec[0] = static_cast<int64_t>(c1 - c0);
+    rec[1] = static_cast<int64_t>(r0);
+    rec[2] = static_cast<int64_t>(r1);
+  }
 }
 
 template <class E>
@@ -589,13 +602,13 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
     GemmShape s = make_shape(w_head, ld_w, full_tiles * kBM, hc, H, T, H);
     s.n_dev = count;
     hipLaunchKernelGGL((k_head_fwd<E, false>), dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad,
-                       int64_t{0});
+                       int64_t{0}, tm.clocks, tm.clock_slots);
   }
   if (rem > 0) {
     GemmShape s = make_shape(static_cast<const S*>(w_head) + full_tiles * kBM * ld_w, ld_w, rem, hc, H, T, H);
     s.n_dev = count;
     hipLaunchKernelGGL((k_head_fwd<E, true>), dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad,
-                       full_tiles);
+                       full_tiles, static_cast<int64_t*>(nullptr), int64_t{0});
   }
   if (timed) (void)hipEventRecord(tm.stop, st);
   hipLaunchKernelGGL(k_fwd_finalize<E>, dim3(rows4), dim3(256), 0, st, part, L.t_pad,

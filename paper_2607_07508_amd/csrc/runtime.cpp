@@ -17,6 +17,12 @@ KernelTimer& kernel_timer() {
 
 }  // namespace sao
 
+extern "C" void sao_debug_clock_samples(void* records, int64_t slots) {
+  sao::KernelTimer& t = sao::kernel_timer();
+  t.clocks = (records && slots > 0) ? static_cast<int64_t*>(records) : nullptr;
+  t.clock_slots = t.clocks ? slots : 0;
+}
+
 extern "C" void sao_debug_time_kernel(int kernel, void* start_event, void* stop_event) {
   sao::KernelTimer& t = sao::kernel_timer();
   t.kernel = (start_event && stop_event) ? kernel : SAO_KERNEL_NONE;
