@@ -110,71 +110,59 @@ def wall_clock_khz() -> Optional[int]:
         return None
 
 
-def forward_clock(step, torch, dev, B) -> dict:
-    """The shader clock the head-forward kernel runs at: one more step (after the
-    timed ones) with the kernel's own per-workgroup records on, cycles
-    (s_memtime) over wall-clock time (s_memrealtime at the rate the runtime
-    reports). Weighted by workgroup time, over the step's forward launches."""
-    khz = wall_clock_khz()
-    slots = 1 << 18
-    rec = torch.zeros((slots, 3), dtype=torch.int64, device=dev)
+def forward_timeline(step, torch, dev, B):
+    """One more step (after the timed ones) with the head-forward kernel's own
+    per-workgroup records on (the step's last forward launch stays recorded).
+    Returns the records as a numpy int64 [n, 8] array of the workgroups that ran a
+    tile, and the wall-clock rate in kHz."""
+    rec = torch.zeros((1 << 18, 8), dtype=torch.int64, device=dev)
     try:
-        B.clock_samples(rec)          # each forward launch overwrites the records: the step's last one stays
+        B.clock_samples(rec)
         step()
         torch.cuda.synchronize()
     finally:
         B.clock_samples(None)
     r = rec.cpu().numpy()
-    live = r[:, 2] > r[:, 1]
-    cycles, ticks = int(r[live, 0].sum()), int((r[live, 2] - r[live, 1]).sum())
-    if not khz or ticks == 0:
+    return r[(r[:, 2] > r[:, 1]) & (r[:, 7] >= 0)], wall_clock_khz()
+
+
+def forward_clock(step, torch, dev, B) -> dict:
+    """The shader clock the head-forward kernel ran at: s_memtime cycles over
+    s_memrealtime time, summed over its workgroups."""
+    r, khz = forward_timeline(step, torch, dev, B)
+    if not khz or r.shape[0] == 0:
         return {"forward_clock_mhz": None, "clock_note": "wall-clock rate or records unavailable"}
+    cycles, ticks = float((r[:, 6] - r[:, 3]).sum()), float((r[:, 2] - r[:, 1]).sum())
     return {"forward_clock_mhz": cycles / (ticks / (khz * 1e3)) / 1e6,
             "clock_note": "shader clock of k_head_fwd's workgroups over one step (s_memtime cycles over "
                           "s_memrealtime time, last forward launch of the step)"}
 
 
-def vendor_gemm(db, t_act: int, t_grad: int, vc: int, torch, reps: int = 3):
-    """torch.matmul (hipBLASLt) in bf16 at the four head-contraction shapes the
-    library runs on MFMA, for context only (run, never inspected):
-      forward       (T_act x H) . (H x V)       on the batch's hidden rows and W_head
-      dz recompute  (T_grad x H) . (H x Vb)     one backward vocabulary block of W_head
-      dH            (T_grad x Vb) . (Vb x H)
-      dW            (Vb x T_grad) . (T_grad x H)
-    Vb is the library's full backward block. Every operand is contiguous (no
-    transposed views); the dz operands are random, scaled like small gradients.
-    The library kernels' own times come from the kernel trace of the same run."""
-    H = db.hidden.shape[1]
-    w = db.w_head
-    gen = torch.Generator(device=db.hidden.device).manual_seed(7)
-    hg = db.hidden[:t_grad].contiguous()
-    dz = (torch.randn(t_grad, vc, generator=gen, device=db.hidden.device) * 1e-4).to(torch.bfloat16)
-    shapes = {
-        "forward": (lambda: db.hidden[:t_act].contiguous(), lambda: w.t().contiguous(), t_act, w.shape[0], H),
-        "dz_recompute": (lambda: hg, lambda: w[:vc].t().contiguous(), t_grad, vc, H),
-        "dH": (lambda: dz, lambda: w[:vc].contiguous(), t_grad, H, vc),
-        "dW": (lambda: dz.t().contiguous(), lambda: hg, vc, H, t_grad),
-    }
-    out = {}
-    for name, (fa, fb, M, N, K) in shapes.items():
-        a, b = fa(), fb()
-        c = torch.matmul(a, b)
-        torch.cuda.synchronize()
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ev0.record()
-        for _ in range(reps):
-            torch.matmul(a, b, out=c)
-        ev1.record()
-        torch.cuda.synchronize()
-        ms = ev0.elapsed_time(ev1) / reps
-        flops = 2.0 * M * N * K
-        out[name] = {"op": f"torch.matmul bf16 ({M} x {K}) . ({K} x {N})", "M": M, "N": N, "K": K, "ms": ms,
-                     "TFLOP/s": flops / ms / 1e9, "frac": flops / ms / 1e9 / PEAK_BF16_TFLOPS}
-        del a, b, c
-        torch.cuda.empty_cache()
-    del hg, dz
-    torch.cuda.empty_cache()
-    return out
+def timeline_summary(r, khz) -> dict:
+    """Where a head-forward tile's time goes: per-tile prologue, K loop and epilogue
+    cycles, and per CU the wall-clock gaps between one workgroup's end and the next
+    one's start, in cycles at the measured clock."""
+    clk = (r[:, 6] - r[:, 3]).sum() / ((r[:, 2] - r[:, 1]).sum() / (khz * 1e3))
+    pro, loop, epi = r[:, 4] - r[:, 3], r[:, 5] - r[:, 4], r[:, 6] - r[:, 5]
+    hw = r[:, 0]
+    cu = ((hw >> 32) << 16) | (((hw >> 13) & 7) << 8) | (((hw >> 12) & 1) << 4) | ((hw >> 8) & 15)
+    gaps, per_cu = [], {}
+    for c in np.unique(cu):
+        sel = np.nonzero(cu == c)[0]
+        o = sel[np.argsort(r[sel, 1])]
+        g = (r[o[1:], 1] - r[o[:-1], 2]) / (khz * 1e3) * clk
+        gaps.append(g)
+        per_cu[int(c)] = int(o.size)
+    g = np.concatenate(gaps) if gaps else np.zeros(0)
+    span = (r[:, 2].max() - r[:, 1].min()) / (khz * 1e3)
+    busy = ((r[:, 2] - r[:, 1]).sum() / (khz * 1e3)) / (len(per_cu) * span)
+    return {"clock_mhz": clk / 1e6, "tiles": int(r.shape[0]), "cus": len(per_cu),
+            "tiles_per_cu": [int(min(per_cu.values())), int(max(per_cu.values()))],
+            "cycles_per_tile": {"prologue": float(pro.mean()), "k_loop": float(loop.mean()),
+                                "epilogue": float(epi.mean()), "total": float((pro + loop + epi).mean())},
+            "gap_cycles_between_tiles": {"median": float(np.median(g)) if g.size else None,
+                                         "mean": float(g.mean()) if g.size else None},
+            "cu_busy_fraction": float(busy), "launch_span_ms": float(span * 1e3)}
 
 
 def mfma_ceiling(blocks: int = 2048, iters: int = 20000, reps: int = 3):
@@ -438,6 +426,8 @@ def main():
                     help="run only a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--vendor-gemm", action="store_true",
                     help="also time torch.matmul (bf16) at the forward's shape, as context (allocates the T_act x V output)")
+    ap.add_argument("--timeline", action="store_true",
+                    help="also record the head-forward kernel's per-workgroup timeline over one extra step")
     ap.add_argument("--mfma-ceiling", action="store_true",
                     help="run only the MFMA-only probe loop (random and constant operands), one line per mode")
     ap.add_argument("--epilogue-sweep", action="store_true",
@@ -611,6 +601,9 @@ def main():
                    **forward_clock(step, torch, dev, B)},
     }
     out["breakdown"] = breakdown(step, T, H, V, esz, t_act, t_grad, torch)
+    if args.timeline:
+        r, khz = forward_timeline(step, torch, dev, B)
+        out["forward_timeline"] = timeline_summary(r, khz) if khz and r.shape[0] else None
     if args.vendor_gemm:
         log("vendor GEMM (context)")
         vc = backward_vocab_block(chunk, V) if cfg.backward else V

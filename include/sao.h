@@ -384,12 +384,14 @@ void sao_debug_time_kernel(int kernel, void* start_event, void* stop_event);
 
 /*
  * Measurement hook, not part of the pass. For the calling thread, makes the next
- * launches of the head-forward kernel record, for each workgroup b < slots, three
- * int64 values in the caller's device buffer `records` (3 * slots int64): the
- * shader-clock cycles the workgroup ran (s_memtime difference) and its start and
- * end on the device's constant-rate wall clock (s_memrealtime). Summed cycles
- * over summed wall-clock time give the clock the kernel ran at. NULL or
- * slots <= 0 disables it. Each launch overwrites the records of the previous one.
+ * launches of the head-forward kernel record, for each workgroup b < slots, eight
+ * int64 values in the caller's device buffer `records` (8 * slots int64): the
+ * hardware ids of its first wave (XCC_ID << 32 | HW_ID), its start and end on the
+ * device's constant-rate wall clock (s_memrealtime), the shader clock (s_memtime)
+ * at its start, after its prologue, after its K loop and at its end, and its
+ * tile (vocabulary tile << 32 | token tile, -1 for none). Summed cycles over
+ * summed wall-clock time give the clock the kernel ran at. NULL or slots <= 0
+ * disables it. Each launch overwrites the records of the previous one.
  */
 void sao_debug_clock_samples(void* records, int64_t slots);
 

@@ -478,13 +478,16 @@ def time_kernel(kernel: int, start: Optional[torch.cuda.Event], stop: Optional[t
     lib().sao_debug_time_kernel(kernel, start.cuda_event, stop.cuda_event)
 
 
+CLOCK_RECORD = ("hw_id", "wall_start", "wall_end", "clk_start", "clk_prologue", "clk_loop", "clk_end", "tile")
+
+
 def clock_samples(records: Optional[torch.Tensor]) -> None:
-    """Make the next head-forward launches record per-workgroup (cycles, wall-clock
-    start, wall-clock end) into `records` (int64 [slots, 3] on the device); None
+    """Make the next head-forward launches record each workgroup's timeline
+    (fields CLOCK_RECORD) into `records` (int64 [slots, 8] on the device); None
     disables."""
     if records is None:
         lib().sao_debug_clock_samples(None, 0)
         return
-    if records.dtype != torch.int64 or records.dim() != 2 or records.shape[1] != 3 or not records.is_contiguous():
-        raise ValueError("records must be a contiguous int64 [slots, 3] tensor")
+    if records.dtype != torch.int64 or records.dim() != 2 or records.shape[1] != 8 or not records.is_contiguous():
+        raise ValueError("records must be a contiguous int64 [slots, 8] tensor")
     lib().sao_debug_clock_samples(records.data_ptr(), records.shape[0])

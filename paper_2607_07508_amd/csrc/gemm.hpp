@@ -58,6 +58,7 @@
 #pragma once
 
 #include <type_traits>
+#include <utility>
 
 #include "common.hpp"
 
@@ -356,6 +357,17 @@ __device__ __forceinline__ int acc_col(int wn, int ni, int lane) {
   return wn * (kBN / kWavesN) + ni * 32 + (lane & 31);
 }
 
+// Optional timeline marks of an epilogue (a measurement hook): mark(0) after the
+// prologue (the first slab has landed), mark(1) after the K loop.
+template <class Epi, class = void>
+struct HasMark : std::false_type {};
+template <class Epi>
+struct HasMark<Epi, std::void_t<decltype(std::declval<Epi&>().mark(0))>> : std::true_type {};
+template <class Epi>
+__device__ __forceinline__ void epi_mark(Epi& epi, int phase) {
+  if constexpr (HasMark<Epi>::value) epi.mark(phase);
+}
+
 // The generic kernel body: one 256 x 256 tile per workgroup. Epi provides:
 //   begin(n0, wm, wn, lane)                 before the K loop
 //   tile(acc, m0, n0, wm, wn, lane, lds)    after it (LDS is free)
@@ -520,6 +532,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
     if (tail && nk <= kStages) pending = 0;  // the partial slab is among these copies
     wait_slabs_barrier<kCopiesPerSlab>(pending);
   }
+  epi_mark(epi, 0);
   Frags f0, f1;
   read_frags<E, AMn, BMn>(f0, lds[0], lds[0] + kAChunks, 0, wm, wn, lane);
   constexpr int kCopyNext = kCopiesPerSlab - kCopyNow;
@@ -581,6 +594,7 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
   // Every copy has landed (the last wait drained them); once every wave's LDS
   // reads have returned, the epilogue may use LDS as scratch.
   lds_barrier();
+  epi_mark(epi, 1);
   epi.tile(acc, m0, n0, wm, wn, lane, reinterpret_cast<void*>(&lds[0][0]));
   epi.finish(mt, n0, wm, wn, lane, reinterpret_cast<void*>(&lds[0][0]));
 }

@@ -154,7 +154,14 @@ struct EpiLse {
   int64_t ldp;
   int64_t M;      // valid vocabulary rows of this launch
   int64_t tile0;  // vocabulary tile of this launch's first tile
+  bool timeline;  // record the marks below (measurement hook)
+  uint64_t t_mark[2];
+  int64_t tile_id;
   float rm[kNI], rs[kNI];
+
+  __device__ __forceinline__ void mark(int phase) {
+    if (timeline) t_mark[phase] = __builtin_amdgcn_s_memtime();
+  }
 
   __device__ __forceinline__ void begin(int64_t, int, int, int) {
 #pragma unroll
@@ -210,6 +217,7 @@ struct EpiLse {
   }
 
   __device__ __forceinline__ void finish(int mg, int64_t n0, int wm, int wn, int lane, void* smem) {
+    tile_id = ((tile0 + mg) << 32) | (n0 / kBN);
 #pragma unroll
     for (int ni = 0; ni < kNI; ++ni) {
       const float m2 = __shfl_xor(rm[ni], 32, 64);
@@ -233,9 +241,12 @@ struct EpiLse {
   }
 };
 
-// With `clk` (a measurement hook, normally null), workgroup b records the
-// shader-clock cycles it ran (s_memtime) and its start and end on the constant
-// wall clock (s_memrealtime) in clk[3b .. 3b+2], for b < clk_slots.
+// With `clk` (a measurement hook, normally null), workgroup b < clk_slots records
+// its timeline in clk[8b .. 8b+7]: the hardware ids of its wave 0
+// (HW_REG_XCC_ID << 32 | HW_REG_HW_ID), its start and end on the constant wall
+// clock (s_memrealtime), the shader clock (s_memtime) at its start, after the
+// prologue, after the K loop and at its end, and its tile (vocabulary tile << 32
+// | token tile; -1 if it had none).
 template <class E, bool kMasked>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t tile0, int64_t* clk, int64_t clk_slots) {
@@ -247,14 +258,25 @@ void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t tile0, int64_t* 
   epi.ldp = ldp;
   epi.M = s.m;
   epi.tile0 = tile0;
+  epi.timeline = clk != nullptr;
+  epi.t_mark[0] = epi.t_mark[1] = 0;
+  epi.tile_id = -1;
   gemm_body<E, false, false>(s, epi, lds);
   if (clk && threadIdx.x == 0 && static_cast<int64_t>(blockIdx.x) < clk_slots) {
     const uint64_t c1 = __builtin_amdgcn_s_memtime();
     const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
-    int64_t* rec = clk + 3 * static_cast<int64_t>(blockIdx.x);
-    rec[0] = static_cast<int64_t>(c1 - c0);
+    // s_getreg_b32 of the whole HW_ID (register 4) and XCC_ID (register 20)
+    const uint32_t hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);
+    const uint32_t xcc = __builtin_amdgcn_s_getreg((31 << 11) | 20);
+    int64_t* rec = clk + 8 * static_cast<int64_t>(blockIdx.x);
+    rec[0] = (static_cast<int64_t>(xcc) << 32) | hw;
     rec[1] = static_cast<int64_t>(r0);
     rec[2] = static_cast<int64_t>(r1);
+    rec[3] = static_cast<int64_t>(c0);
+    rec[4] = static_cast<int64_t>(epi.t_mark[0]);
+    rec[5] = static_cast<int64_t>(epi.t_mark[1]);
+    rec[6] = static_cast<int64_t>(c1);
+    rec[7] = epi.tile_id;
   }
 }
 
