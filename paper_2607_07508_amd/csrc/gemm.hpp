@@ -113,8 +113,11 @@ inline int gemm_grid(const GemmShape& s) {
   return nw * mw * 256;
 }
 
-// N-split: SN so that 8 SN N-tiles fill the N range with little waste.
+// N-split: SN so that 8 SN N-tiles fill the N range with little waste. (For
+// the backward's logit recompute at 256 token tiles, SN 8 measured 0.8 % faster
+// than 4 and SN 2 1.7 % slower; at 128 token tiles SN 8 was 1.8 % slower.)
 inline int pick_sn(int n_tiles) {
+  if (n_tiles > 128) return 8;
   if (n_tiles % 32 == 0 || n_tiles > 96) return 4;
   if (n_tiles % 16 == 0) return 2;
   return 1;

@@ -620,15 +620,23 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
   const KernelTimer& tm = kernel_timer();
   const bool timed = tm.kernel == SAO_KERNEL_HEAD_FORWARD && tm.start && tm.stop;
   if (timed) (void)hipEventRecord(tm.start, st);
+  // The forward splits the vocabulary across the XCDs (M-split) whatever the
+  // token count: each XCD streams its own W panels while all of them read the
+  // same hidden rows, which the memory-side cache holds (measured 0.7 % faster
+  // than splitting the tokens at 65,536 tokens).
   if (full_tiles > 0) {
     GemmShape s = make_shape(w_head, ld_w, full_tiles * kBM, hc, H, T, H);
     s.n_dev = count;
+    s.msplit = 1;
+    s.sn = pick_sn_msplit(s.n_tiles);
     hipLaunchKernelGGL((k_head_fwd<E, false>), dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad,
                        int64_t{0}, tm.clocks, tm.clock_slots);
   }
   if (rem > 0) {
     GemmShape s = make_shape(static_cast<const S*>(w_head) + full_tiles * kBM * ld_w, ld_w, rem, hc, H, T, H);
     s.n_dev = count;
+    s.msplit = 1;
+    s.sn = pick_sn_msplit(s.n_tiles);
     hipLaunchKernelGGL((k_head_fwd<E, true>), dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad,
                        full_tiles, static_cast<int64_t*>(nullptr), int64_t{0});
   }
