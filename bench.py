@@ -165,6 +165,49 @@ def timeline_summary(r, khz) -> dict:
             "cu_busy_fraction": float(busy), "launch_span_ms": float(span * 1e3)}
 
 
+def vendor_gemm(db, t_act: int, t_grad: int, vc: int, torch, reps: int = 3):
+    """torch.matmul (hipBLASLt) in bf16 at the four head-contraction shapes the
+    library runs on MFMA, for context only (run, never inspected):
+      forward       (T_act x H) . (H x V)       on the batch's hidden rows and W_head
+      dz recompute  (T_grad x H) . (H x Vb)     one backward vocabulary block of W_head
+      dH            (T_grad x Vb) . (Vb x H)
+      dW            (Vb x T_grad) . (T_grad x H)
+    Vb is the library's full backward block. Every operand is contiguous (no
+    transposed views); the dz operands are random, scaled like small gradients.
+    The library kernels' own times come from the kernel trace of the same run."""
+    H = db.hidden.shape[1]
+    w = db.w_head
+    gen = torch.Generator(device=db.hidden.device).manual_seed(7)
+    hg = db.hidden[:t_grad].contiguous()
+    dz = (torch.randn(t_grad, vc, generator=gen, device=db.hidden.device) * 1e-4).to(torch.bfloat16)
+    shapes = {
+        "forward": (lambda: db.hidden[:t_act].contiguous(), lambda: w.t().contiguous(), t_act, w.shape[0], H),
+        "dz_recompute": (lambda: hg, lambda: w[:vc].t().contiguous(), t_grad, vc, H),
+        "dH": (lambda: dz, lambda: w[:vc].contiguous(), t_grad, H, vc),
+        "dW": (lambda: dz.t().contiguous(), lambda: hg, vc, H, t_grad),
+    }
+    out = {}
+    for name, (fa, fb, M, N, K) in shapes.items():
+        a, b = fa(), fb()
+        c = torch.matmul(a, b)
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(reps):
+            torch.matmul(a, b, out=c)
+        ev1.record()
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / reps
+        flops = 2.0 * M * N * K
+        out[name] = {"op": f"torch.matmul bf16 ({M} x {K}) . ({K} x {N})", "M": M, "N": N, "K": K, "ms": ms,
+                     "TFLOP/s": flops / ms / 1e9, "frac": flops / ms / 1e9 / PEAK_BF16_TFLOPS}
+        del a, b, c
+        torch.cuda.empty_cache()
+    del hg, dz
+    torch.cuda.empty_cache()
+    return out
+
+
 def mfma_ceiling(blocks: int = 2048, iters: int = 20000, reps: int = 3):
     """What the bf16 MFMA pipe delivers with nothing else to issue: the probe library's
     loop of 16 v_mfma_f32_32x32x16_bf16 per round on 256 accumulators, one wave per
