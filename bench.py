@@ -110,14 +110,15 @@ def wall_clock_khz() -> Optional[int]:
         return None
 
 
-def forward_timeline(step, torch, dev, B):
-    """One more step (after the timed ones) with the head-forward kernel's own
-    per-workgroup records on (the step's last forward launch stays recorded).
-    Returns the records as a numpy int64 [n, 8] array of the workgroups that ran a
-    tile, and the wall-clock rate in kHz."""
+def kernel_timeline(step, torch, dev, B, kernel=None):
+    """One more step (after the timed ones) with a head kernel's own per-workgroup
+    records on (default the head forward; the step's last launch of it stays
+    recorded, for the backward kernels the first vocabulary block's). Returns the
+    records as a numpy int64 [n, 8] array of the workgroups that ran a tile, and
+    the wall-clock rate in kHz."""
     rec = torch.zeros((1 << 18, 8), dtype=torch.int64, device=dev)
     try:
-        B.clock_samples(rec)
+        B.clock_samples(rec, B.KERNEL_HEAD_FORWARD if kernel is None else kernel)
         step()
         torch.cuda.synchronize()
     finally:
@@ -129,7 +130,7 @@ def forward_timeline(step, torch, dev, B):
 def forward_clock(step, torch, dev, B) -> dict:
     """The shader clock the head-forward kernel ran at: s_memtime cycles over
     s_memrealtime time, summed over its workgroups."""
-    r, khz = forward_timeline(step, torch, dev, B)
+    r, khz = kernel_timeline(step, torch, dev, B)
     if not khz or r.shape[0] == 0:
         return {"forward_clock_mhz": None, "clock_note": "wall-clock rate or records unavailable"}
     cycles, ticks = float((r[:, 6] - r[:, 3]).sum()), float((r[:, 2] - r[:, 1]).sum())
@@ -138,10 +139,12 @@ def forward_clock(step, torch, dev, B) -> dict:
                           "s_memrealtime time, last forward launch of the step)"}
 
 
-def timeline_summary(r, khz) -> dict:
-    """Where a head-forward tile's time goes: per-tile prologue, K loop and epilogue
+def timeline_summary(r, khz, k=None) -> dict:
+    """Where a head kernel's tile time goes: per-tile prologue, K loop and epilogue
     cycles, and per CU the wall-clock gaps between one workgroup's end and the next
-    one's start, in cycles at the measured clock."""
+    one's start, in cycles at the measured clock. With the contraction length k,
+    also the MFMA cycles a tile needs (256 x 256 x k x 2 flop at 4 SIMDs x 1024
+    bf16 flop per cycle) and the K loop's MFMA efficiency."""
     clk = (r[:, 6] - r[:, 3]).sum() / ((r[:, 2] - r[:, 1]).sum() / (khz * 1e3))
     pro, loop, epi = r[:, 4] - r[:, 3], r[:, 5] - r[:, 4], r[:, 6] - r[:, 5]
     hw = r[:, 0]
@@ -156,7 +159,10 @@ def timeline_summary(r, khz) -> dict:
     g = np.concatenate(gaps) if gaps else np.zeros(0)
     span = (r[:, 2].max() - r[:, 1].min()) / (khz * 1e3)
     busy = ((r[:, 2] - r[:, 1]).sum() / (khz * 1e3)) / (len(per_cu) * span)
+    mfma = 256 * 256 * 2 * k / 4096 if k else None
     return {"clock_mhz": clk / 1e6, "tiles": int(r.shape[0]), "cus": len(per_cu),
+            "k": k, "mfma_cycles_per_tile": mfma,
+            "k_loop_mfma_efficiency": float(mfma / loop.mean()) if mfma else None,
             "tiles_per_cu": [int(min(per_cu.values())), int(max(per_cu.values()))],
             "cycles_per_tile": {"prologue": float(pro.mean()), "k_loop": float(loop.mean()),
                                 "epilogue": float(epi.mean()), "total": float((pro + loop + epi).mean())},
@@ -470,7 +476,8 @@ def main():
     ap.add_argument("--vendor-gemm", action="store_true",
                     help="also time torch.matmul (bf16) at the forward's shape, as context (allocates the T_act x V output)")
     ap.add_argument("--timeline", action="store_true",
-                    help="also record the head-forward kernel's per-workgroup timeline over one extra step")
+                    help="also record the per-workgroup timelines of the head forward and the backward's three "
+                         "products (first vocabulary block), one extra step each")
     ap.add_argument("--mfma-ceiling", action="store_true",
                     help="run only the MFMA-only probe loop (random and constant operands), one line per mode")
     ap.add_argument("--epilogue-sweep", action="store_true",
@@ -645,8 +652,18 @@ def main():
     }
     out["breakdown"] = breakdown(step, T, H, V, esz, t_act, t_grad, torch)
     if args.timeline:
-        r, khz = forward_timeline(step, torch, dev, B)
-        out["forward_timeline"] = timeline_summary(r, khz) if khz and r.shape[0] else None
+        vc0 = min(backward_vocab_block(chunk, V), V)
+        # dH cuts K into pieces when a chunk's token tiles are few (the rule of csrc/layout.hpp)
+        pieces = min(max(-(-1024 // (-(-chunk // 256) * -(-H // 256))), 1), 8)
+        k_dh = vc0 if pieces == 1 else -(-(-(-vc0 // pieces)) // 64) * 64
+        kernels = [("forward", B.KERNEL_HEAD_FORWARD, H)]
+        if cfg.backward:
+            kernels += [("dz", B.KERNEL_BACKWARD_DZ, H), ("dH", B.KERNEL_BACKWARD_DH, k_dh),
+                        ("dW", B.KERNEL_BACKWARD_DW, t_grad if len(chunks) == 1 else None)]
+        out["timelines"] = {}
+        for name, kid, k in kernels:
+            r, khz = kernel_timeline(step, torch, dev, B, kid)
+            out["timelines"][name] = timeline_summary(r, khz, k) if khz and r.shape[0] else None
     if args.vendor_gemm:
         log("vendor GEMM (context)")
         vc = backward_vocab_block(chunk, V) if cfg.backward else V

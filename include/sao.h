@@ -380,20 +380,26 @@ sao_status_t sao_value_loss(const void* hidden, int64_t ld_hidden, const void* w
  */
 #define SAO_KERNEL_NONE         0
 #define SAO_KERNEL_HEAD_FORWARD 1  /* the MFMA head-forward kernel of sao_token_logprob */
+#define SAO_KERNEL_BACKWARD_DZ  2  /* sao_loss_backward's logit recompute (dz), first vocabulary block */
+#define SAO_KERNEL_BACKWARD_DH  3  /* its dH += dz . W product, first vocabulary block */
+#define SAO_KERNEL_BACKWARD_DW  4  /* its dW += dz^T . H product, first vocabulary block */
 void sao_debug_time_kernel(int kernel, void* start_event, void* stop_event);
 
 /*
  * Measurement hook, not part of the pass. For the calling thread, makes the next
- * launches of the head-forward kernel record, for each workgroup b < slots, eight
+ * launches of kernel `kernel` (one of the SAO_KERNEL_* above; the backward ones
+ * on their first vocabulary block) record, for each workgroup b < slots, eight
  * int64 values in the caller's device buffer `records` (8 * slots int64): the
  * hardware ids of its first wave (XCC_ID << 32 | HW_ID), its start and end on the
  * device's constant-rate wall clock (s_memrealtime), the shader clock (s_memtime)
  * at its start, after its prologue, after its K loop and at its end, and its
- * tile (vocabulary tile << 32 | token tile, -1 for none). Summed cycles over
- * summed wall-clock time give the clock the kernel ran at. NULL or slots <= 0
- * disables it. Each launch overwrites the records of the previous one.
+ * tile (M tile << 32 | N tile of the product, -1 for none; for the head forward
+ * the vocabulary tile and the token tile). Workgroup b is blockIdx.x plus
+ * blockIdx.y times the grid's x size. Summed cycles over summed wall-clock time
+ * give the clock the kernel ran at. SAO_KERNEL_NONE, NULL or slots <= 0 disables
+ * it. Each launch overwrites the records of the previous one.
  */
-void sao_debug_clock_samples(void* records, int64_t slots);
+void sao_debug_clock_samples(int kernel, void* records, int64_t slots);
 
 #ifdef __cplusplus
 }

@@ -27,7 +27,7 @@ EXPORTS = ("sao_status_string", "sao_last_error_message", "sao_version", "sao_wo
            "sao_value_forward", "sao_value_loss", "sao_ppo_loss", "sao_explained_variance", "sao_step_advantage",
            "sao_group_advantage", "sao_running_mean_advantage", "sao_clipped_loss_noalloc",
            "sao_debug_time_kernel", "sao_debug_clock_samples")
-KERNEL_NONE, KERNEL_HEAD_FORWARD = 0, 1
+KERNEL_NONE, KERNEL_HEAD_FORWARD, KERNEL_BACKWARD_DZ, KERNEL_BACKWARD_DH, KERNEL_BACKWARD_DW = 0, 1, 2, 3, 4
 
 
 class SaoError(RuntimeError):
@@ -69,7 +69,7 @@ _SIGS = {
                                                   ctypes.c_int32, _p, _p, _p, _p, _p, _p, _p, _p, ctypes.c_size_t,
                                                   _p]),
     "sao_debug_time_kernel": (None, [ctypes.c_int, _p, _p]),
-    "sao_debug_clock_samples": (None, [_p, _i64]),
+    "sao_debug_clock_samples": (None, [ctypes.c_int, _p, _i64]),
 }
 
 _lib = None
@@ -481,13 +481,13 @@ def time_kernel(kernel: int, start: Optional[torch.cuda.Event], stop: Optional[t
 CLOCK_RECORD = ("hw_id", "wall_start", "wall_end", "clk_start", "clk_prologue", "clk_loop", "clk_end", "tile")
 
 
-def clock_samples(records: Optional[torch.Tensor]) -> None:
-    """Make the next head-forward launches record each workgroup's timeline
-    (fields CLOCK_RECORD) into `records` (int64 [slots, 8] on the device); None
-    disables."""
+def clock_samples(records: Optional[torch.Tensor], kernel: int = KERNEL_HEAD_FORWARD) -> None:
+    """Make the next launches of `kernel` (KERNEL_*; the backward ones on their
+    first vocabulary block) record each workgroup's timeline (fields CLOCK_RECORD)
+    into `records` (int64 [slots, 8] on the device); None disables."""
     if records is None:
-        lib().sao_debug_clock_samples(None, 0)
+        lib().sao_debug_clock_samples(KERNEL_NONE, None, 0)
         return
     if records.dtype != torch.int64 or records.dim() != 2 or records.shape[1] != 8 or not records.is_contiguous():
         raise ValueError("records must be a contiguous int64 [slots, 8] tensor")
-    lib().sao_debug_clock_samples(records.data_ptr(), records.shape[0])
+    lib().sao_debug_clock_samples(kernel, records.data_ptr(), records.shape[0])

@@ -324,7 +324,9 @@ __device__ __forceinline__ void mma_step_mix(f32x16_t (&acc)[kMI][kNI], const Fr
                                              int lane, Hook&& hook) {
 #pragma unroll
   for (int t = 0; t < kMI * kNI; ++t) {
-    Mma<E>::run(acc[t / kNI][t % kNI], cur.a[t / kNI], cur.b[t % kNI]);
+    const int mi = t / kNI;
+    const int ni = mi % 2 == 0 ? t % kNI : kNI - 1 - t % kNI;
+    Mma<E>::run(acc[mi][ni], cur.a[mi], cur.b[ni]);
     pin_order();
     if (t % kReadEvery == kReadEvery - 1 && t / kReadEvery < kMI + kNI)
       read_one<E, AMn, BMn>(nxt, t / kReadEvery, la, lb, s_next, wm, wn, lane);

@@ -140,6 +140,24 @@ __global__ __launch_bounds__(256) void k_gather_rows(const typename E::storage* 
   }
 }
 
+// Timeline marks of an epilogue (a measurement hook, off unless `timeline`):
+// s_memtime after the prologue and after the K loop, and the tile (M tile << 32
+// | N tile, -1 for none).
+struct TileClock {
+  bool timeline;
+  uint64_t t_mark[2];
+  int64_t tile_id;
+
+  __device__ __forceinline__ void mark(int phase) {
+    if (timeline) t_mark[phase] = __builtin_amdgcn_s_memtime();
+  }
+  __device__ __forceinline__ void start(bool on) {
+    timeline = on;
+    t_mark[0] = t_mark[1] = 0;
+    tile_id = -1;
+  }
+};
+
 // ------------------------------------------------------------------------- //
 // Forward: online log-sum-exp epilogue
 // ------------------------------------------------------------------------- //
@@ -154,14 +172,10 @@ struct EpiLse {
   int64_t ldp;
   int64_t M;      // valid vocabulary rows of this launch
   int64_t tile0;  // vocabulary tile of this launch's first tile
-  bool timeline;  // record the marks below (measurement hook)
-  uint64_t t_mark[2];
-  int64_t tile_id;
+  TileClock clock;  // measurement hook
   float rm[kNI], rs[kNI];
 
-  __device__ __forceinline__ void mark(int phase) {
-    if (timeline) t_mark[phase] = __builtin_amdgcn_s_memtime();
-  }
+  __device__ __forceinline__ void mark(int phase) { clock.mark(phase); }
 
   __device__ __forceinline__ void begin(int64_t, int, int, int) {
 #pragma unroll
@@ -217,7 +231,7 @@ struct EpiLse {
   }
 
   __device__ __forceinline__ void finish(int mg, int64_t n0, int wm, int wn, int lane, void* smem) {
-    tile_id = ((tile0 + mg) << 32) | (n0 / kBN);
+    clock.tile_id = ((tile0 + mg) << 32) | (n0 / kBN);
 #pragma unroll
     for (int ni = 0; ni < kNI; ++ni) {
       const float m2 = __shfl_xor(rm[ni], 32, 64);
@@ -241,12 +255,34 @@ struct EpiLse {
   }
 };
 
-// With `clk` (a measurement hook, normally null), workgroup b < clk_slots records
-// its timeline in clk[8b .. 8b+7]: the hardware ids of its wave 0
-// (HW_REG_XCC_ID << 32 | HW_REG_HW_ID), its start and end on the constant wall
-// clock (s_memrealtime), the shader clock (s_memtime) at its start, after the
-// prologue, after the K loop and at its end, and its tile (vocabulary tile << 32
-// | token tile; -1 if it had none).
+// With `clk` (a measurement hook, normally null), workgroup b (blockIdx.x plus
+// blockIdx.y times gridDim.x) < clk_slots records its timeline in clk[8b .. 8b+7]:
+// the hardware ids of its wave 0 (HW_REG_XCC_ID << 32 | HW_REG_HW_ID), its start
+// and end on the constant wall clock (s_memrealtime), the shader clock
+// (s_memtime) at its start, after the prologue, after the K loop and at its end,
+// and its tile. c0 and r0 are the start readings.
+__device__ __forceinline__ void write_clock_record(int64_t* clk, int64_t clk_slots, uint64_t c0, uint64_t r0,
+                                                   const TileClock& tc) {
+  const int64_t b = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
+  if (!clk || threadIdx.x != 0 || b >= clk_slots) return;
+  const uint64_t c1 = __builtin_amdgcn_s_memtime();
+  const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
+  // s_getreg_b32 of the whole HW_ID (register 4) and XCC_ID (register 20)
+  const uint32_t hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);
+  const uint32_t xcc = __builtin_amdgcn_s_getreg((31 << 11) | 20);
+  int64_t* rec = clk + 8 * b;
+  rec[0] = (static_cast<int64_t>(xcc) << 32) | hw;
+  rec[1] = static_cast<int64_t>(r0);
+  rec[2] = static_cast<int64_t>(r1);
+  rec[3] = static_cast<int64_t>(c0);
+  rec[4] = static_cast<int64_t>(tc.t_mark[0]);
+  rec[5] = static_cast<int64_t>(tc.t_mark[1]);
+  rec[6] = static_cast<int64_t>(c1);
+  rec[7] = tc.tile_id;
+}
+
+// The head forward, with the timeline hook above (the tile is vocabulary tile
+// << 32 | token tile).
 template <class E, bool kMasked>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t tile0, int64_t* clk, int64_t clk_slots) {
@@ -258,26 +294,9 @@ void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t tile0, int64_t* 
   epi.ldp = ldp;
   epi.M = s.m;
   epi.tile0 = tile0;
-  epi.timeline = clk != nullptr;
-  epi.t_mark[0] = epi.t_mark[1] = 0;
-  epi.tile_id = -1;
+  epi.clock.start(clk != nullptr);
   gemm_body<E, false, false>(s, epi, lds);
-  if (clk && threadIdx.x == 0 && static_cast<int64_t>(blockIdx.x) < clk_slots) {
-    const uint64_t c1 = __builtin_amdgcn_s_memtime();
-    const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
-    // s_getreg_b32 of the whole HW_ID (register 4) and XCC_ID (register 20)
-    const uint32_t hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);
-    const uint32_t xcc = __builtin_amdgcn_s_getreg((31 << 11) | 20);
-    int64_t* rec = clk + 8 * static_cast<int64_t>(blockIdx.x);
-    rec[0] = (static_cast<int64_t>(xcc) << 32) | hw;
-    rec[1] = static_cast<int64_t>(r0);
-    rec[2] = static_cast<int64_t>(r1);
-    rec[3] = static_cast<int64_t>(c0);
-    rec[4] = static_cast<int64_t>(epi.t_mark[0]);
-    rec[5] = static_cast<int64_t>(epi.t_mark[1]);
-    rec[6] = static_cast<int64_t>(c1);
-    rec[7] = epi.tile_id;
-  }
+  write_clock_record(clk, clk_slots, c0, r0, epi.clock);
 }
 
 template <class E>
@@ -385,6 +404,9 @@ struct EpiDz {
   float gl[kNI], ll[kNI];
   int64_t yl[kNI];
   int yt[kNI];  // target row of the column's token inside the current tile, or -8 when outside
+  TileClock clock;  // measurement hook
+
+  __device__ __forceinline__ void mark(int phase) { clock.mark(phase); }
 
   __device__ __forceinline__ void begin(int64_t n0, int, int wn, int lane) {
 #pragma unroll
@@ -422,13 +444,9 @@ struct EpiDz {
     }
   }
 
-  // LDS chunk position of 16-byte chunk c (8 vocabulary entries) of token row t
-  // in the staged bf16 tile: conflict-free for the accumulator writes (32
-  // consecutive rows, one chunk), the row reads and the 8-row block reads.
-  static __device__ __forceinline__ int tswz(int t, int c) { return c ^ ((t ^ (t >> 3)) & 15); }
-
   __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t n0, int wm, int wn,
-                                       int lane, void* smem) {
+                                       int lane, void*) {
+    clock.tile_id = ((m0 / kBM) << 32) | (n0 / kBN);
     // Valid rows of this tile (all 256 unless kMasked).
     const int64_t rows64 = m_valid - m0;
     const int rows = rows64 > kBM ? kBM : static_cast<int>(rows64);
@@ -438,35 +456,29 @@ struct EpiDz {
       yt[ni] = y >= 0 && y < kBM ? static_cast<int>(y) : -8;
     }
     if constexpr (sizeof(typename E::storage) == 2) {
-      // Stage the 256 x 256 bf16 tile in LDS as [t][v] (128 KB), then write it
-      // with 16-byte stores.
-      v4u* tile16 = static_cast<v4u*>(smem);       // [256 rows][32 chunks]
+      // Straight from the accumulators with 16-byte stores. Of the register
+      // groups j = 2p and 2p + 1 (vocabulary rows 16p + 4h .. +3 and 16p + 8 + 4h
+      // .. +3 of lane half h), v_permlane32_swap trades group 2p of the upper
+      // half for group 2p + 1 of the lower half, so that each lane holds 8
+      // consecutive rows (16p + 8h ..) of its token: one 16-byte chunk.
 #pragma unroll
       for (int ni = 0; ni < kNI; ++ni) {
-        const int t = acc_col(wn, ni, lane);
+        typename E::storage* row = dz + (n0 + acc_col(wn, ni, lane)) * ldz + m0;
 #pragma unroll
         for (int mi = 0; mi < kMI; ++mi) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int vl = acc_row(wm, mi, 4 * j, lane);   // multiple of 4
-            float d[4];
-            dz4(acc, mi, ni, j, vl, rows, d);
-            const uint32_t lo = pack_bf16x2(d[0], d[1]);
-            const uint32_t hi = pack_bf16x2(d[2], d[3]);
-            uint2* p = reinterpret_cast<uint2*>(tile16 + t * 32 + tswz(t, vl >> 3)) + ((vl >> 2) & 1);
-            *p = make_uint2(lo, hi);
+          for (int p = 0; p < 2; ++p) {
+            float d0[4], d1[4];
+            dz4(acc, mi, ni, 2 * p, acc_row(wm, mi, 8 * p, lane), rows, d0);
+            dz4(acc, mi, ni, 2 * p + 1, acc_row(wm, mi, 8 * p + 4, lane), rows, d1);
+            const auto lo = __builtin_amdgcn_permlane32_swap(pack_bf16x2(d0[0], d0[1]), pack_bf16x2(d1[0], d1[1]),
+                                                             false, false);
+            const auto hi = __builtin_amdgcn_permlane32_swap(pack_bf16x2(d0[2], d0[3]), pack_bf16x2(d1[2], d1[3]),
+                                                             false, false);
+            const int v = wm * (kBM / 2) + mi * 32 + 16 * p + 8 * (lane >> 5);
+            *reinterpret_cast<v4u*>(row + v) = v4u{lo[0], hi[0], lo[1], hi[1]};
           }
         }
-      }
-      __syncthreads();
-      const int tid = threadIdx.x;
-      // [t][v]: thread takes chunk c of row t for 32 (t, c) pairs.
-#pragma unroll 4
-      for (int k = 0; k < 32; ++k) {
-        const int id = k * kThreads + tid;
-        const int t = id >> 5, c = id & 31;
-        const v4u x = tile16[t * 32 + tswz(t, c)];
-        *reinterpret_cast<v4u*>(dz + (n0 + t) * ldz + m0 + c * 8) = x;
       }
     } else {
 #pragma unroll
@@ -500,11 +512,15 @@ struct EpiAcc {
   int64_t m_valid;
   int64_t n_valid;
   int64_t split_stride;  // elements between the outputs of successive K pieces
+  TileClock clock;       // measurement hook
+
+  __device__ __forceinline__ void mark(int phase) { clock.mark(phase); }
 
   __device__ __forceinline__ void begin(int64_t, int, int, int) {}
 
   __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t n0, int wm, int wn,
                                        int lane, void*) {
+    clock.tile_id = ((m0 / kBM) << 32) | (n0 / kBN);
 #pragma unroll
     for (int ni = 0; ni < kNI; ++ni) {
       const int64_t n = n0 + acc_col(wn, ni, lane);
@@ -524,18 +540,26 @@ struct EpiAcc {
 
 template <class E, bool kMasked>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void k_bwd_dz(GemmShape s, EpiDz<E, kMasked> epi) {
+void k_bwd_dz(GemmShape s, EpiDz<E, kMasked> epi, int64_t* clk, int64_t clk_slots) {
   __shared__ v4u lds[kStages][kStageChunks];
+  const uint64_t c0 = clk ? __builtin_amdgcn_s_memtime() : 0;
+  const uint64_t r0 = clk ? __builtin_amdgcn_s_memrealtime() : 0;
+  epi.clock.start(clk != nullptr);
   gemm_body<E, false, false>(s, epi, lds);
+  write_clock_record(clk, clk_slots, c0, r0, epi.clock);
 }
 
 // dH += dz . W (dz K-major, W MN-major) and dW += dz^T . Hg (both MN-major).
 template <class E, bool AMn, bool BMn>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void k_bwd_acc(GemmShape s, EpiAcc epi) {
+void k_bwd_acc(GemmShape s, EpiAcc epi, int64_t* clk, int64_t clk_slots) {
   __shared__ v4u lds[kStages][kStageChunks];
+  const uint64_t c0 = clk ? __builtin_amdgcn_s_memtime() : 0;
+  const uint64_t r0 = clk ? __builtin_amdgcn_s_memrealtime() : 0;
+  epi.clock.start(clk != nullptr);
   epi.out += static_cast<int64_t>(blockIdx.y) * epi.split_stride;  // this K piece's own output
   gemm_body<E, AMn, BMn>(s, epi, lds);
+  write_clock_record(clk, clk_slots, c0, r0, epi.clock);
 }
 
 
@@ -618,7 +642,7 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
   const int64_t full_tiles = V / kBM;
   const int64_t rem = V - full_tiles * kBM;
   const KernelTimer& tm = kernel_timer();
-  const bool timed = tm.kernel == SAO_KERNEL_HEAD_FORWARD && tm.start && tm.stop;
+  const bool timed = tm.timed(SAO_KERNEL_HEAD_FORWARD);
   if (timed) (void)hipEventRecord(tm.start, st);
   // The forward splits the vocabulary across the XCDs (M-split) whatever the
   // token count: each XCD streams its own W panels while all of them read the
@@ -630,7 +654,7 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
     s.msplit = 1;
     s.sn = pick_sn_msplit(s.n_tiles);
     hipLaunchKernelGGL((k_head_fwd<E, false>), dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad,
-                       int64_t{0}, tm.clocks, tm.clock_slots);
+                       int64_t{0}, tm.clocks_for(SAO_KERNEL_HEAD_FORWARD), tm.clock_slots);
   }
   if (rem > 0) {
     GemmShape s = make_shape(static_cast<const S*>(w_head) + full_tiles * kBM * ld_w, ld_w, rem, hc, H, T, H);
@@ -677,6 +701,12 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
   const int64_t dh_stride = L.t_pad * H;
   hipLaunchKernelGGL(k_zero_rows, dim3(rows4), dim3(256), 0, st, dh, H, count, L.dh_pieces, dh_stride);
 
+  // The measurement hooks apply to the first vocabulary block's launches.
+  const KernelTimer& tm = kernel_timer();
+  auto hook = [&](int64_t vb, int kernel, bool stop_event) {
+    if (vb == 0 && tm.timed(kernel)) (void)hipEventRecord(stop_event ? tm.stop : tm.start, st);
+  };
+  auto clocks = [&](int64_t vb, int kernel) { return vb == 0 ? tm.clocks_for(kernel) : nullptr; };
   for (int64_t vb = 0; vb < L.n_vblocks; ++vb) {
     const int64_t v0 = vb * L.vc;
     const int64_t vlen = (V - v0) < L.vc ? (V - v0) : L.vc;
@@ -686,14 +716,18 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
     if (full_v > 0) {
       GemmShape sa = make_shape(w + v0 * ld_w, ld_w, full_v, hg, H, T, H);
       sa.n_dev = count;
-      EpiDz<E, false> ez{dz, L.vc, full_v, v0, g_c, lse_c, y_c, {}, {}, {}, {}};
-      hipLaunchKernelGGL((k_bwd_dz<E, false>), dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez);
+      EpiDz<E, false> ez{dz, L.vc, full_v, v0, g_c, lse_c, y_c, {}, {}, {}, {}, {}};
+      hook(vb, SAO_KERNEL_BACKWARD_DZ, false);
+      hipLaunchKernelGGL((k_bwd_dz<E, false>), dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez,
+                         clocks(vb, SAO_KERNEL_BACKWARD_DZ), tm.clock_slots);
+      hook(vb, SAO_KERNEL_BACKWARD_DZ, true);
     }
     if (vlen > full_v) {
       GemmShape sa = make_shape(w + (v0 + full_v) * ld_w, ld_w, vlen - full_v, hg, H, T, H);
       sa.n_dev = count;
-      EpiDz<E, true> ez{dz + full_v, L.vc, vlen - full_v, v0 + full_v, g_c, lse_c, y_c, {}, {}, {}, {}};
-      hipLaunchKernelGGL((k_bwd_dz<E, true>), dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez);
+      EpiDz<E, true> ez{dz + full_v, L.vc, vlen - full_v, v0 + full_v, g_c, lse_c, y_c, {}, {}, {}, {}, {}};
+      hipLaunchKernelGGL((k_bwd_dz<E, true>), dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez,
+                         static_cast<int64_t*>(nullptr), int64_t{0});
     }
     // (B) dH[t][h] += sum_v dz[t][v] W[v0 + v][h]: A = dz K-major, B = W MN-major
     // With few token rows the dH tiles cannot fill the GPU: K (the vocabulary)
@@ -704,16 +738,21 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
     sb.sn = pick_sn_msplit(sb.n_tiles);
     sb.k_split = L.dh_pieces > 1 ? round_up(ceil_div(vlen, L.dh_pieces), 64) : 0;
     const int pieces_b = L.dh_pieces > 1 ? static_cast<int>(ceil_div(vlen, sb.k_split)) : 1;
-    EpiAcc eb{dh, H, L.t_pad, H, dh_stride};
+    EpiAcc eb{dh, H, L.t_pad, H, dh_stride, {}};
+    hook(vb, SAO_KERNEL_BACKWARD_DH, false);
     hipLaunchKernelGGL((k_bwd_acc<E, false, true>), dim3(gemm_grid(sb), pieces_b), dim3(kThreads), 0, st, sb,
-                       eb);
+                       eb, clocks(vb, SAO_KERNEL_BACKWARD_DH), tm.clock_slots);
+    hook(vb, SAO_KERNEL_BACKWARD_DH, true);
     // (C) dW[v0 + v][h] += sum_t dz[t][v] Hg[t][h]: both MN-major
     GemmShape sc = make_shape(dz, L.vc, vlen, hg, H, H, T);
     sc.k_dev = count;
     sc.msplit = 1;
     sc.sn = pick_sn_msplit(sc.n_tiles);
-    EpiAcc ec{dw + v0 * H, H, vlen, H, 0};
-    hipLaunchKernelGGL((k_bwd_acc<E, true, true>), dim3(gemm_grid(sc)), dim3(kThreads), 0, st, sc, ec);
+    EpiAcc ec{dw + v0 * H, H, vlen, H, 0, {}};
+    hook(vb, SAO_KERNEL_BACKWARD_DW, false);
+    hipLaunchKernelGGL((k_bwd_acc<E, true, true>), dim3(gemm_grid(sc)), dim3(kThreads), 0, st, sc, ec,
+                       clocks(vb, SAO_KERNEL_BACKWARD_DW), tm.clock_slots);
+    hook(vb, SAO_KERNEL_BACKWARD_DW, true);
   }
   const int t4 = static_cast<int>(ceil_div(T, 4));
   hipLaunchKernelGGL(k_dh_scatter<E>, dim3(t4), dim3(256), 0, st, dh, H, pos, T, L.dh_pieces, dh_stride,

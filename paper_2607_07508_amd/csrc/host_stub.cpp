@@ -67,4 +67,4 @@ int launch_value_loss(const void*, int64_t, const void*, const float*, const flo
 }  // namespace sao
 
 extern "C" void sao_debug_time_kernel(int, void*, void*) {}
-extern "C" void sao_debug_clock_samples(void*, int64_t) {}
+extern "C" void sao_debug_clock_samples(int, void*, int64_t) {}

@@ -17,10 +17,11 @@ KernelTimer& kernel_timer() {
 
 }  // namespace sao
 
-extern "C" void sao_debug_clock_samples(void* records, int64_t slots) {
+extern "C" void sao_debug_clock_samples(int kernel, void* records, int64_t slots) {
   sao::KernelTimer& t = sao::kernel_timer();
-  t.clocks = (records && slots > 0) ? static_cast<int64_t*>(records) : nullptr;
+  t.clocks = (kernel != SAO_KERNEL_NONE && records && slots > 0) ? static_cast<int64_t*>(records) : nullptr;
   t.clock_slots = t.clocks ? slots : 0;
+  t.clock_kernel = t.clocks ? kernel : SAO_KERNEL_NONE;
 }
 
 extern "C" void sao_debug_time_kernel(int kernel, void* start_event, void* stop_event) {
