@@ -503,9 +503,11 @@ struct EpiDz {
 };
 
 // out[m][n] += acc (fp32), rows < m_valid and columns < n_valid. Each element has
-// one writer per launch and launches on a stream are ordered, so the no-return
-// atomic add below is an ordinary deterministic accumulate that needs no
-// result registers.
+// one writer per launch and launches on a stream are ordered, so a plain load,
+// add and store per element is an exact, deterministic accumulate. The loads of
+// one 32-column block (64 per lane) are issued together, so that a tile pays a
+// few load latencies instead of a stream of read-modify-write atomics in L2
+// (every tile of a round reaches its epilogue at about the same time).
 struct EpiAcc {
   float* out;
   int64_t ldo;
@@ -521,6 +523,38 @@ struct EpiAcc {
   __device__ __forceinline__ void tile(f32x16_t (&acc)[kMI][kNI], int64_t m0, int64_t n0, int wm, int wn,
                                        int lane, void*) {
     clock.tile_id = ((m0 / kBM) << 32) | (n0 / kBN);
+    const bool whole = m0 + kBM <= m_valid && n0 + kBN <= n_valid;  // uniform
+    if (whole) {
+      // Element (mi, ni, r) sits at a uniform base (the wave's 32-row block of
+      // mi and its 32 columns of ni) plus a uniform row offset of r plus this
+      // lane's fixed offset, so the loads and stores take a scalar base and one
+      // address register (global address space, so that they are not flat).
+      using gchar = __attribute__((address_space(1))) char;
+      const uint32_t lane_off = static_cast<uint32_t>((4 * (lane >> 5) * ldo + (lane & 31)) * 4);
+#pragma unroll
+      for (int ni = 0; ni < kNI; ++ni) {
+        float v[kMI][16];
+#pragma unroll
+        for (int mi = 0; mi < kMI; ++mi) {
+          gchar* b = (gchar*)uniform_ptr(out + (m0 + wm * (kBM / 2) + mi * 32) * ldo + n0 + wn * (kBN / kWavesN) +
+                                         ni * 32);
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            v[mi][r] = *(__attribute__((address_space(1))) const float*)(b + ((r & 3) + 8 * (r >> 2)) * ldo * 4 +
+                                                                         lane_off);
+        }
+#pragma unroll
+        for (int mi = 0; mi < kMI; ++mi) {
+          gchar* b = (gchar*)uniform_ptr(out + (m0 + wm * (kBM / 2) + mi * 32) * ldo + n0 + wn * (kBN / kWavesN) +
+                                         ni * 32);
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            *(__attribute__((address_space(1))) float*)(b + ((r & 3) + 8 * (r >> 2)) * ldo * 4 + lane_off) =
+                v[mi][r] + acc_read(acc[mi][ni][r]);
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int ni = 0; ni < kNI; ++ni) {
       const int64_t n = n0 + acc_col(wn, ni, lane);
@@ -530,7 +564,7 @@ struct EpiAcc {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t m = m0 + acc_row(wm, mi, r, lane);
-          if (m < m_valid) unsafeAtomicAdd(out + m * ldo + n, acc[mi][ni][r]);
+          if (m < m_valid) out[m * ldo + n] += acc_read(acc[mi][ni][r]);
         }
     }
   }
