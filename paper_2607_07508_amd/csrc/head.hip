@@ -21,6 +21,8 @@ namespace sao {
 
 // Compacted row buffers are zero-filled up to a multiple of this many rows.
 constexpr int64_t kRowPad = 256;
+// MI355X's memory-side (Infinity) cache, shared by the XCDs.
+constexpr int64_t kMemorySideCacheBytes = int64_t{256} << 20;
 
 // ------------------------------------------------------------------------- //
 // Row compaction
@@ -750,6 +752,13 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
     if (full_v > 0) {
       GemmShape sa = make_shape(w + v0 * ld_w, ld_w, full_v, hg, H, T, H);
       sa.n_dev = count;
+      // A block of W larger than the memory-side cache is streamed once per XCD
+      // (M-split) rather than read by all XCDs together (measured at H = 6144:
+      // 1.5 ms faster per step; at H = 2048, where the block fits, 0.7 ms slower).
+      if (full_v * H * static_cast<int64_t>(sizeof(S)) > kMemorySideCacheBytes) {
+        sa.msplit = 1;
+        sa.sn = pick_sn_msplit(sa.n_tiles);
+      }
       EpiDz<E, false> ez{dz, L.vc, full_v, v0, g_c, lse_c, y_c, {}, {}, {}, {}, {}};
       hook(vb, SAO_KERNEL_BACKWARD_DZ, false);
       hipLaunchKernelGGL((k_bwd_dz<E, false>), dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez,
