@@ -218,7 +218,9 @@ def mfma_ceiling(blocks: int = 2048, iters: int = 20000, reps: int = 3):
     """What the bf16 MFMA pipe delivers with nothing else to issue: the probe library's
     loop of 16 v_mfma_f32_32x32x16_bf16 per round on 256 accumulators, one wave per
     SIMD (the head kernels' arrangement), for random, constant and refreshed-random
-    operands, with the clock the workgroups ran at. One JSON line per mode."""
+    operands; then the same MFMAs fed from LDS the way the tile engine feeds them,
+    without and with its global->LDS copies and per-slab barrier. With the clock
+    the workgroups ran at. One JSON line per mode."""
     import ctypes
     import torch
     from paper_2607_07508_amd import build as bld
@@ -228,20 +230,27 @@ def mfma_ceiling(blocks: int = 2048, iters: int = 20000, reps: int = 3):
     lib = ctypes.CDLL(bld.PROBE_LIB)
     fn = lib.sao_probe_mfma
     fn.restype = ctypes.c_int
-    fn.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    fn.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                   ctypes.c_void_p]
+    # 2 MB of random bf16 bit patterns for mode 4's copies to read
+    gen = torch.Generator(device="cuda").manual_seed(3)
+    src = (torch.randn((1 << 20,), generator=gen, device="cuda")).to(torch.bfloat16)
     out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
     clk = torch.zeros((blocks, 3), dtype=torch.int64, device="cuda")
     st = torch.cuda.current_stream().cuda_stream
     khz = wall_clock_khz()
     flops = 2.0 * 32 * 32 * 16 * 16 * 4 * blocks * iters
-    for mode, name in ((0, "random operands"), (1, "constant operands"), (2, "random operands refreshed per round")):
-        if fn(blocks, iters, mode, out.data_ptr(), clk.data_ptr(), st) != 0:
+    modes = ((0, "random operands"), (1, "constant operands"), (2, "random operands refreshed per round"),
+             (3, "random operands read from LDS as the tile engine reads them"),
+             (4, "LDS reads plus the engine's global->LDS copies and a barrier per slab"))
+    for mode, name in modes:
+        if fn(blocks, iters, mode, src.data_ptr(), out.data_ptr(), clk.data_ptr(), st) != 0:
             raise RuntimeError("probe launch failed")
         torch.cuda.synchronize()
         a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
         for _ in range(reps):
-            fn(blocks, iters, mode, out.data_ptr(), clk.data_ptr(), st)
+            fn(blocks, iters, mode, src.data_ptr(), out.data_ptr(), clk.data_ptr(), st)
         z.record()
         torch.cuda.synchronize()
         ms = a.elapsed_time(z) / reps
@@ -479,7 +488,8 @@ def main():
                     help="also record the per-workgroup timelines of the head forward and the backward's three "
                          "products (first vocabulary block), one extra step each")
     ap.add_argument("--mfma-ceiling", action="store_true",
-                    help="run only the MFMA-only probe loop (random and constant operands), one line per mode")
+                    help="run only the MFMA probe loops (register operands: random, constant, refreshed; LDS-fed "
+                         "without and with the engine's copies), one line per mode")
     ap.add_argument("--epilogue-sweep", action="store_true",
                     help="HBM bandwidth of the scan and loss epilogue at T = 2^20 .. 2^26 (one line per size)")
     args = ap.parse_args()

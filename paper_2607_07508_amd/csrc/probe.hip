@@ -11,6 +11,12 @@
 // mode 2: random operands whose A fragments get new bits every iteration (a few
 //         VALU operations per dword, issued between the MFMAs), so that the
 //         MFMAs keep seeing fresh operand bits as in a real K loop
+// mode 3: random operands read from LDS as the tile engine reads them: the
+//         fragments of the next K step, one 16-byte read after each of the
+//         first 8 MFMAs of a step, from a 2 x 64 KB ring of random bf16
+// mode 4: mode 3 plus the engine's global -> LDS copies (16 global_load_lds_dwordx4
+//         per wave per 4-step slab into the other stage, from an L2-resident 2 MB
+//         buffer) and one copy wait and workgroup barrier per slab
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -105,16 +111,138 @@ void k_mfma_probe(int64_t iters, int mode, float* out, int64_t* clk) {
   }
 }
 
+__device__ __forceinline__ void pin() { __builtin_amdgcn_sched_barrier(0); }
+__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r / 2) % 8); }
+
+struct Frags {
+  v4u a[4];
+  v4u b[4];
+};
+
+// Fragment idx of K step s (first-use order A0, B0 .. B3, A1 .. A3) from a
+// 64 KB stage holding 256 A rows then 256 B rows of 8 16-byte chunks.
+__device__ __forceinline__ void read_one(Frags& f, int idx, const v4u* l, int s, int wm, int wn, int lane) {
+  const bool is_a = idx == 0 || idx > 4;
+  const int i = idx == 0 ? 0 : (is_a ? idx - 4 : idx - 1);
+  const int r32 = lane & 31;
+  const int c = 2 * s + (lane >> 5);
+  const int row0 = is_a ? wm * 128 : 256 + wn * 128;
+  const v4u x = l[(row0 + r32) * 8 + swz(r32, c) + i * 32 * 8];
+  if (is_a)
+    f.a[i] = x;
+  else
+    f.b[i] = x;
+}
+
+__device__ __forceinline__ void dma16(const void* g, uint32_t off, uint32_t lds_base, uint32_t lds_off) {
+  asm volatile("s_add_u32 m0, %2, %3\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(g), "s"(lds_base),
+               "s"(lds_off)
+               : "memory", "m0", "scc");
+}
+
+// Modes 3 and 4 (kCopies): iters K steps of 16 MFMAs each, in slabs of 4 steps.
+template <bool kCopies>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_lds_probe(int64_t iters, const v4u* src, float* out, int64_t* clk) {
+  __shared__ v4u lds[2][4096];
+  const uint64_t c0 = __builtin_amdgcn_s_memtime();
+  const uint64_t r0 = __builtin_amdgcn_s_memrealtime();
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / 2, wn = wave % 2;
+  const uint32_t seed = (blockIdx.x * 256u + tid) * 64u;
+  for (int i = tid; i < 2 * 4096; i += 256) lds[i / 4096][i % 4096] = rnd_frag(seed + 4 * i);
+  __syncthreads();
+  f32x16_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
+  Frags f0, f1;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f0.a[i] = rnd_frag(seed + 8 * i);
+    f0.b[i] = rnd_frag(seed + 8 * i + 36);
+  }
+  f1 = f0;
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(&lds[0][0]));
+  const uint32_t src_off = static_cast<uint32_t>(tid) * 16u;
+  for (int64_t it = 0; it < iters / 4; ++it) {
+    const int stage = static_cast<int>(it & 1);
+    const v4u* l = lds[stage];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      Frags& cur = s % 2 == 0 ? f0 : f1;
+      Frags& nxt = s % 2 == 0 ? f1 : f0;
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        acc[t / 4][t % 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, cur.a[t / 4]),
+                                                                    __builtin_bit_cast(bf16x8_t, cur.b[t % 4]),
+                                                                    acc[t / 4][t % 4], 0, 0, 0);
+        pin();
+        if (t < 8) read_one(nxt, t, l, (s + 1) & 3, wm, wn, lane);
+        if constexpr (kCopies) {
+          if ((s == 3 || s == 0) && (t & 1)) {
+            // copy q of this wave: 1 KB of a 64 KB source window (32 windows in 2 MB)
+            const int q = (s == 3 ? 0 : 8) + (t >> 1);
+            const char* g = reinterpret_cast<const char*>(src) + (static_cast<int64_t>(it & 31) << 16) + q * 4096;
+            dma16(g, src_off, lds0 + static_cast<uint32_t>((stage ^ 1) * 4096 * 16),
+                  static_cast<uint32_t>((wave * 16 + q) * 1024));
+          }
+        }
+        pin();
+      }
+      if constexpr (kCopies) {
+        if (s == 2) {
+          asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+          __builtin_amdgcn_s_barrier();
+        }
+      }
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+  float sum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float x;
+        asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(x) : "a"(acc[i][j][r]));
+        sum += x;
+      }
+  out[blockIdx.x * 256 + tid] = sum;
+  if (tid == 0) {
+    const uint64_t c1 = __builtin_amdgcn_s_memtime();
+    const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
+    clk[3 * blockIdx.x] = static_cast<int64_t>(c1 - c0);
+    clk[3 * blockIdx.x + 1] = static_cast<int64_t>(r0);
+    clk[3 * blockIdx.x + 2] = static_cast<int64_t>(r1);
+  }
+}
+
 }  // namespace
 
 // Launches `blocks` workgroups of 4 waves, each wave running `iters` rounds of
-// 16 MFMAs (16 x 32 x 32 x 16 x 2 flops per round). out: blocks * 256 floats;
-// clk: blocks * 3 int64 (per-workgroup s_memtime cycles, s_memrealtime start and
-// end). Returns the HIP status of the launch.
-extern "C" int sao_probe_mfma(int64_t blocks, int64_t iters, int mode, float* out, int64_t* clk,
+// 16 MFMAs (16 x 32 x 32 x 16 x 2 flops per round; modes 3 and 4 need iters a
+// multiple of 4). src: for mode 4, a device buffer of at least 2 MB that the
+// copies read (ignored otherwise). out: blocks * 256 floats; clk: blocks * 3
+// int64 (per-workgroup s_memtime cycles, s_memrealtime start and end). Returns
+// the HIP status of the launch.
+extern "C" int sao_probe_mfma(int64_t blocks, int64_t iters, int mode, const void* src, float* out, int64_t* clk,
                               hipStream_t stream) {
-  if (blocks < 1 || blocks > (int64_t{1} << 20) || iters < 1 || mode < 0 || mode > 2 || !out || !clk)
+  if (blocks < 1 || blocks > (int64_t{1} << 20) || iters < 1 || mode < 0 || mode > 4 || !out || !clk)
     return static_cast<int>(hipErrorInvalidValue);
-  hipLaunchKernelGGL(k_mfma_probe, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, iters, mode, out, clk);
+  if (mode >= 3 && (iters % 4 != 0 || (mode == 4 && !src))) return static_cast<int>(hipErrorInvalidValue);
+  const unsigned g = static_cast<unsigned>(blocks);
+  if (mode <= 2)
+    hipLaunchKernelGGL(k_mfma_probe, dim3(g), dim3(256), 0, stream, iters, mode, out, clk);
+  else if (mode == 3)
+    hipLaunchKernelGGL(k_lds_probe<false>, dim3(g), dim3(256), 0, stream, iters, static_cast<const v4u*>(src), out,
+                       clk);
+  else
+    hipLaunchKernelGGL(k_lds_probe<true>, dim3(g), dim3(256), 0, stream, iters, static_cast<const v4u*>(src), out,
+                       clk);
   return static_cast<int>(hipGetLastError());
 }
