@@ -122,8 +122,10 @@ const char* sao_version(void);
 /* Bytes of `ws` that `op` needs for T tokens, hidden size H and vocabulary V
  * (0 if none). Returns 0 for invalid arguments as well. The backward's share is
  * dominated by one vocabulary block of the logit gradient, round_up(T, 256) x Vb
- * elements of the hidden dtype, with Vb between 32768 and 65536 rows (larger for
- * small T, at most V rounded up to 256). */
+ * elements of the hidden dtype. Vb comes from a target Vt = 32768 rows, doubled
+ * (up to 65536) while (round_up(T, 256) / 256) x (Vt / 256) < 8192: V is cut into
+ * ceil(V / Vt) equal blocks, Vb = round_up(ceil(V / blocks), 256) (30464 rows for
+ * V = 151936 at T = 65536). */
 size_t sao_workspace_size(sao_op_t op, int64_t T, int64_t H, int64_t V, sao_dtype_t dtype);
 
 /*
