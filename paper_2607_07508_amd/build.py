@@ -29,7 +29,7 @@ def hipcc() -> str:
 
 
 def _flags():
-    return ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-munsafe-fp-atomics",
+    return ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
             # packed fp32 VALU ops are kept out of generated code
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
             "-Wno-unused-command-line-argument", "-I", os.path.join(ROOT, "include"), "-I", CSRC]
