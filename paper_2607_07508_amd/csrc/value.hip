@@ -129,13 +129,20 @@ __global__ __launch_bounds__(kValueThreads) void k_value_rows(
   for (int e = 0; e < P; ++e) out[e] = acc[e];
 }
 
-// dw_v[col] += sum over row blocks (in order); block 0 also adds the loss.
+// dw_v[col] += sum over row blocks; block 0 also adds the loss. A block takes
+// 64 columns: wave w sums row blocks w, w + 4, w + 8, ... into 8 partial sums
+// per lane (so that 8 loads are in flight), which it combines in a fixed order;
+// then the 4 waves' sums are added in wave order. Every run adds in the same
+// order, so the result is deterministic.
 __global__ __launch_bounds__(kValueThreads) void k_value_final(const float* part_dw, const double* part_loss,
                                                                int64_t row_blocks, int64_t H,
                                                                const int64_t* n_ptr, double* loss_v,
                                                                float* dw_v) {
-  __shared__ double s_red[kValueThreads / 64];
-  const int64_t col = static_cast<int64_t>(blockIdx.x) * kValueThreads + threadIdx.x;
+  constexpr int kWaves = kValueThreads / 64;
+  constexpr int kLanes = 8;
+  __shared__ double s_red[kWaves];
+  __shared__ float s_col[kWaves][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (blockIdx.x == 0) {  // uniform over the block
     double l = 0.0;
     for (int64_t i = threadIdx.x; i < row_blocks; i += kValueThreads) l += part_loss[i];
@@ -143,10 +150,29 @@ __global__ __launch_bounds__(kValueThreads) void k_value_final(const float* part
     const int64_t N = *n_ptr;
     if (threadIdx.x == 0 && N > 0) loss_v[0] += l / static_cast<double>(N);
   }
-  if (col >= H) return;
-  float s = 0.0f;
-  for (int64_t rb = 0; rb < row_blocks; ++rb) s += part_dw[rb * H + col];
-  dw_v[col] += s;
+  const int64_t col = static_cast<int64_t>(blockIdx.x) * 64 + lane;
+  float acc[kLanes];
+#pragma unroll
+  for (int u = 0; u < kLanes; ++u) acc[u] = 0.0f;
+  if (col < H) {
+    int64_t rb = wave;
+    for (; rb + (kLanes - 1) * kWaves < row_blocks; rb += kLanes * kWaves) {
+#pragma unroll
+      for (int u = 0; u < kLanes; ++u) acc[u] += part_dw[(rb + u * kWaves) * H + col];
+    }
+    // fewer than kLanes row blocks of this wave remain
+#pragma unroll
+    for (int u = 0; u < kLanes; ++u)
+      if (rb + u * kWaves < row_blocks) acc[u] += part_dw[(rb + u * kWaves) * H + col];
+  }
+  s_col[wave][lane] = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
+  __syncthreads();
+  if (wave == 0 && col < H) {
+    float t = s_col[0][lane];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) t += s_col[w][lane];
+    dw_v[col] += t;
+  }
 }
 
 int launch_value_forward(const void* hidden, int64_t ld_hidden, const void* w_v, int64_t T, int64_t H,
@@ -187,7 +213,7 @@ int launch_value_loss(const void* hidden, int64_t ld_hidden, const void* w_v, co
     hipLaunchKernelGGL(k_value_rows<F32>, grid, dim3(kValueThreads), 0, st, static_cast<const float*>(hidden),
                        ld_hidden, static_cast<const float*>(w_v), v, ret, mask, T, H, n_ptr,
                        static_cast<float*>(dhidden_v), part_loss, part_dw);
-  hipLaunchKernelGGL(k_value_final, dim3(static_cast<unsigned>(ceil_div(H, kValueThreads))), dim3(kValueThreads), 0,
+  hipLaunchKernelGGL(k_value_final, dim3(static_cast<unsigned>(ceil_div(H, 64))), dim3(kValueThreads), 0,
                      st, part_dw, part_loss, L.row_blocks, H, n_ptr, loss_v, dw_v);
   return hipGetLastError();
 }
