@@ -52,11 +52,17 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "head_fwd_c2_traffic.json")
 
 
 def kernel_source_sha() -> str:
+    """Hash of the head kernels' code: their sources with comments and whitespace
+    removed, so that an edit of a comment does not mark the counters stale."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, f)) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

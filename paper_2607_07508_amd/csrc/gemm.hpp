@@ -322,6 +322,10 @@ template <class E, bool AMn, bool BMn, class Hook>
 __device__ __forceinline__ void mma_step_mix(f32x16_t (&acc)[kMI][kNI], const Frags& cur, Frags& nxt,
                                              const v4u* la, const v4u* lb, int s_next, int wm, int wn,
                                              int lane, Hook&& hook) {
+  // The MFMAs run in snake order (even rows of blocks left to right, odd rows
+  // right to left), so the B fragment stays the same across each row change:
+  // fewer operand bits switch between consecutive MFMAs, which costs less power.
+  // The fragments' first uses keep the read order above.
 #pragma unroll
   for (int t = 0; t < kMI * kNI; ++t) {
     const int mi = t / kNI;
