@@ -693,10 +693,11 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
                        int64_t{0}, tm.clocks_for(SAO_KERNEL_HEAD_FORWARD), tm.clock_slots);
   }
   if (rem > 0) {
+    // A single row of tiles: the M-split raster would deal its one M tile to one
+    // XCD, so the tiles are dealt out along N (make_shape's choice for many token
+    // tiles) and spread over all 8 XCDs.
     GemmShape s = make_shape(static_cast<const S*>(w_head) + full_tiles * kBM * ld_w, ld_w, rem, hc, H, T, H);
     s.n_dev = count;
-    s.msplit = 1;
-    s.sn = pick_sn_msplit(s.n_tiles);
     hipLaunchKernelGGL((k_head_fwd<E, true>), dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad,
                        full_tiles, static_cast<int64_t*>(nullptr), int64_t{0});
   }
