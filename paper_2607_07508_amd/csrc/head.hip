@@ -326,8 +326,14 @@ __device__ __forceinline__ float dot_chunk<F32>(const v4u& a, const v4u& b) {
   return s;
 }
 
-// One wave per compacted row: merge the vocabulary-group partials into lse, take
-// the target logit as a dot product, and write logp = z_y - lse at the row's position.
+// 64 compacted rows per block, lane l of every wave on row l. Phase 1: wave w
+// merges the row's partials of vocabulary tiles w, w + 4, w + 8, ... in that
+// order (8 loads in flight; the 64 lanes read 256 contiguous bytes of a tile's
+// partials, [tile][row]), then the four waves' results are merged in wave order.
+// Phase 2: the target logits as dot products, 8 lanes per row and 8 rows per
+// wave at a time (each lane takes every 8th 16-byte chunk of the row), then
+// logp = z_y - lse at the row's position.
+constexpr int kFinRows = 64;
 template <class E>
 __global__ __launch_bounds__(256) void k_fwd_finalize(const float2* part, int64_t ldp, int m_groups,
                                                       const typename E::storage* hc, int64_t H,
@@ -335,38 +341,70 @@ __global__ __launch_bounds__(256) void k_fwd_finalize(const float2* part, int64_
                                                       int64_t V, const int32_t* idx,
                                                       const int32_t* target, const int32_t* count,
                                                       float* logp, float* lse, int32_t* status) {
-  const int lane = threadIdx.x & 63;
-  const int64_t c = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (c >= *count) return;
-  float m = -__builtin_inff(), s = 0.0f;
-  for (int gi = lane; gi < m_groups; gi += 64) {
-    const float2 p = part[static_cast<int64_t>(gi) * ldp + c];
-    lse_merge(m, s, p.x, p.y);
-  }
+  constexpr int kWaves = 4;
+  constexpr int kInFlight = 8;
+  __shared__ float2 s_ms[kWaves][kFinRows];
+  __shared__ float s_lse[kFinRows];
+  const int64_t n = *count;
+  const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kFinRows;
+  if (c0 >= n) return;  // uniform over the block
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  {
+    const int64_t c = c0 + lane;
+    float m = -__builtin_inff(), s = 0.0f;
+    if (c < n) {
+      int gi = wave;
+      for (; gi + (kInFlight - 1) * kWaves < m_groups; gi += kInFlight * kWaves) {
+        float2 p[kInFlight];
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float m2 = __shfl_xor(m, o, 64);
-    const float s2 = __shfl_xor(s, o, 64);
-    lse_merge(m, s, m2, s2);
+        for (int u = 0; u < kInFlight; ++u) p[u] = part[static_cast<int64_t>(gi + u * kWaves) * ldp + c];
+#pragma unroll
+        for (int u = 0; u < kInFlight; ++u) lse_merge(m, s, p[u].x, p[u].y);
+      }
+      for (; gi < m_groups; gi += kWaves) {
+        const float2 p = part[static_cast<int64_t>(gi) * ldp + c];
+        lse_merge(m, s, p.x, p.y);
+      }
+    }
+    s_ms[wave][lane] = make_float2(m, s);
   }
-  const int64_t t = idx[c];
-  const int32_t y = target[t];
-  const bool yok = y >= 0 && static_cast<int64_t>(y) < V;
-  float z = 0.0f;
-  if (yok) {
-    const v4u* hr = reinterpret_cast<const v4u*>(hc + c * H);
-    const v4u* wr = reinterpret_cast<const v4u*>(w + static_cast<int64_t>(y) * ld_w);
-    const int64_t chunks = H / E::kPerChunk;
-    for (int64_t k = lane; k < chunks; k += 64) z += dot_chunk<E>(hr[k], wr[k]);
+  __syncthreads();
+  if (wave == 0) {
+    float m = s_ms[0][lane].x, s = s_ms[0][lane].y;
+#pragma unroll
+    for (int q = 1; q < kWaves; ++q) lse_merge(m, s, s_ms[q][lane].x, s_ms[q][lane].y);
+    s_lse[lane] = m + logf(s);
   }
-  z = wave_sum(z);
-  if (lane == 0) {
-    const float l = m + logf(s);
-    const bool finite = __builtin_isfinite(l);
-    if (status && !yok) atomicOr(status, SAO_STATUS_TARGET_RANGE);
-    if (status && !finite) atomicOr(status, SAO_STATUS_NONFINITE);
-    lse[t] = l;
-    logp[t] = yok ? z - l : __builtin_nanf("");
+  __syncthreads();
+  const int sub = lane & 7;                 // lane within the row's group of 8
+  const int64_t chunks = H / E::kPerChunk;  // 16-byte chunks per row
+  for (int j = 0; j < kFinRows / kWaves; j += 8) {
+    const int r = wave * (kFinRows / kWaves) + j + (lane >> 3);  // row of this block
+    const int64_t c = c0 + r;
+    float z = 0.0f;
+    int64_t t = 0;
+    bool yok = false;
+    if (c < n) {
+      t = idx[c];
+      const int32_t y = target[t];
+      yok = y >= 0 && static_cast<int64_t>(y) < V;
+      if (yok) {
+        const v4u* hr = reinterpret_cast<const v4u*>(hc + c * H);
+        const v4u* wr = reinterpret_cast<const v4u*>(w + static_cast<int64_t>(y) * ld_w);
+        for (int64_t k = sub; k < chunks; k += 8) z += dot_chunk<E>(hr[k], wr[k]);
+      }
+    }
+    z += __shfl_xor(z, 4, 64);
+    z += __shfl_xor(z, 2, 64);
+    z += __shfl_xor(z, 1, 64);
+    if (sub == 0 && c < n) {
+      const float l = s_lse[r];
+      const bool finite = __builtin_isfinite(l);
+      if (status && !yok) atomicOr(status, SAO_STATUS_TARGET_RANGE);
+      if (status && !finite) atomicOr(status, SAO_STATUS_NONFINITE);
+      lse[t] = l;
+      logp[t] = yok ? z - l : __builtin_nanf("");
+    }
   }
 }
 
@@ -702,7 +740,8 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
                        full_tiles, static_cast<int64_t*>(nullptr), int64_t{0});
   }
   if (timed) (void)hipEventRecord(tm.stop, st);
-  hipLaunchKernelGGL(k_fwd_finalize<E>, dim3(rows4), dim3(256), 0, st, part, L.t_pad,
+  hipLaunchKernelGGL(k_fwd_finalize<E>, dim3(static_cast<unsigned>(L.t_pad / kFinRows)), dim3(256), 0, st, part,
+                     L.t_pad,
                      static_cast<int>(L.m_tiles), hc, H, static_cast<const S*>(w_head), ld_w, V, idx,
                      target, count, logp, lse, status);
   return hipGetLastError();
