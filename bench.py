@@ -477,6 +477,86 @@ def cpu_baseline(batch, ref_logp, rows: int, seed: int = 0):
                       f"{cores} host cores visible, BLAS on {blas} threads"}
 
 
+
+def cpu_baseline_full(names=("c0", "c1", "c2", "c4", "c3"), chunk_rows: int = 8192):
+    """The oracle on whole workloads, on the host's cores: the forward over every
+    loss-mask row, the scan and loss over the batch, the backward over every row
+    with g != 0 where the workload has a backward (not c1), and the critic for c4,
+    each timed; the head work goes in chunks
+    of rows so that a progress line appears every few tens of seconds. c3 runs
+    the head on the rows of its first 8 of 32 token chunks and is scaled by 4
+    (labelled as extrapolated). One JSON line per workload."""
+    import oracle
+    from synth import CONFIGS, generate, rollout_logprobs
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas = None
+    cores = len(os.sched_getaffinity(0))
+    for name in names:
+        cfg = CONFIGS[name]
+        log(f"oracle in full: generating {name}")
+        b = generate(cfg)
+        T = b.T
+        act = np.nonzero(b.mask)[0]
+        scale = 1.0
+        if name == "c3":
+            limit = 8 * cfg.chunk
+            head_rows = act[act < limit]
+            scale = act.size / head_rows.size
+        else:
+            head_rows = act
+        parts = {}
+        w64 = b.w_head.astype(np.float64)
+        t = time.perf_counter()
+        if cfg.value_head:
+            values = oracle.value_forward(b.hidden, b.w_value)
+        else:
+            values = b.values
+        parts["critic_forward"] = time.perf_counter() - t
+        t = time.perf_counter()
+        adv, ret, N = oracle.advantage(values, b.rewards, b.mask, b.cu_seqlens, cfg.gamma, cfg.lam, cfg.alpha)
+        parts["scan"] = time.perf_counter() - t
+        t = time.perf_counter()
+        lp = np.zeros(T)
+        lse = np.zeros(T)
+        for s0 in range(0, head_rows.size, chunk_rows):
+            r = head_rows[s0:s0 + chunk_rows]
+            lp_c, lse_c = oracle.token_logprob(b.hidden, None, b.target, rows=r, w64=w64)
+            lp[r], lse[r] = lp_c[r], lse_c[r]
+            log(f"oracle in full: {name} forward rows {s0 + r.size} of {head_rows.size}")
+        parts["head_forward"] = time.perf_counter() - t
+        t = time.perf_counter()
+        lro = rollout_logprobs(lp, b.xi)
+        sub = np.zeros_like(b.mask)
+        sub[head_rows] = 1
+        _, g, _, _ = oracle.dis_loss(lp, lro, adv, sub, cfg.eps_low, cfg.eps_high, N)
+        parts["loss"] = time.perf_counter() - t
+        t = time.perf_counter()
+        if cfg.value_head:
+            oracle.value_loss(b.hidden, b.w_value, values, ret, b.mask, N)
+        parts["critic_loss"] = time.perf_counter() - t
+        t = time.perf_counter()
+        live = np.nonzero(g)[0] if cfg.backward else np.zeros(0, dtype=np.int64)  # c1 is forward only
+        for s0 in range(0, live.size, chunk_rows):
+            r = live[s0:s0 + chunk_rows]
+            gc = np.zeros_like(g)
+            gc[r] = g[r]
+            oracle.loss_backward(b.hidden, None, b.target, lse, gc, w64=w64)
+            log(f"oracle in full: {name} backward rows {s0 + r.size} of {live.size}")
+        parts["head_backward"] = time.perf_counter() - t
+        total = (parts["critic_forward"] + parts["scan"] + parts["loss"] + parts["critic_loss"]
+                 + (parts["head_forward"] + parts["head_backward"]) * scale)
+        print(json.dumps({"mode": "cpu_baseline_full", "workload": name, "T": T, "T_act": int(act.size),
+                          "T_grad": int(round(live.size * scale)), "seconds": total, "tokens_per_s": T / total,
+                          "parts_seconds": parts, "head_scale": scale, "extrapolated": scale != 1.0,
+                          "cores": cores, "blas_threads": blas, "kind": "oracle",
+                          "note": ("head forward and backward on the rows of 8 of the 32 token chunks, scaled by "
+                                   f"{scale:.2f}; scan, loss and critic on the whole batch") if scale != 1.0
+                          else "every loss-mask row; W_head widening to fp64 excluded"}), flush=True)
+        del b, w64, lp, lse, g
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -486,6 +566,9 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="loss-mask tokens in the oracle sample (default 0: a quarter of them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-baseline-full", action="store_true",
+                    help="run only the oracle on whole workloads (c0, c1, c2, c4; c3 on 8 of its 32 chunks) on the "
+                         "host, one line per workload (minutes)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--vendor-gemm", action="store_true",
@@ -499,6 +582,9 @@ def main():
     ap.add_argument("--epilogue-sweep", action="store_true",
                     help="HBM bandwidth of the scan and loss epilogue at T = 2^20 .. 2^26 (one line per size)")
     args = ap.parse_args()
+    if args.cpu_baseline_full:
+        cpu_baseline_full()
+        return
     if args.copy_calibration:
         copy_calibration()
         return
