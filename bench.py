@@ -225,8 +225,10 @@ def mfma_ceiling(blocks: int = 2048, iters: int = 20000, reps: int = 3):
     loop of 16 v_mfma_f32_32x32x16_bf16 per round on 256 accumulators, one wave per
     SIMD (the head kernels' arrangement), for random, constant and refreshed-random
     operands; then the same MFMAs fed from LDS the way the tile engine feeds them,
-    without and with its global->LDS copies and per-slab barrier. With the clock
-    the workgroups ran at. One JSON line per mode."""
+    without and with its global->LDS copies and per-slab barrier, and with both
+    operands MN-major through the transposing LDS read (as the backward's dW
+    product reads them), without and with the copies. With the clock the
+    workgroups ran at. One JSON line per mode."""
     import ctypes
     import torch
     from paper_2607_07508_amd import build as bld
@@ -248,7 +250,9 @@ def mfma_ceiling(blocks: int = 2048, iters: int = 20000, reps: int = 3):
     flops = 2.0 * 32 * 32 * 16 * 16 * 4 * blocks * iters
     modes = ((0, "random operands"), (1, "constant operands"), (2, "random operands refreshed per round"),
              (3, "random operands read from LDS as the tile engine reads them"),
-             (4, "LDS reads plus the engine's global->LDS copies and a barrier per slab"))
+             (4, "LDS reads plus the engine's global->LDS copies and a barrier per slab"),
+             (5, "MN-major operands read from LDS through the transposing read, as dW reads them"),
+             (6, "transposing LDS reads plus the engine's copies and a barrier per slab"))
     for mode, name in modes:
         if fn(blocks, iters, mode, src.data_ptr(), out.data_ptr(), clk.data_ptr(), st) != 0:
             raise RuntimeError("probe launch failed")

@@ -17,6 +17,10 @@
 // mode 4: mode 3 plus the engine's global -> LDS copies (16 global_load_lds_dwordx4
 //         per wave per 4-step slab into the other stage, from an L2-resident 2 MB
 //         buffer) and one copy wait and workgroup barrier per slab
+// mode 5: mode 3 with both operands stored MN-major ([k][256 elements]) and read
+//         through the transposing LDS read (ds_read_b64_tr_b16), two reads per
+//         fragment, as the backward's dW product reads them
+// mode 6: mode 5 plus the copies, copy wait and barrier of mode 4
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -134,14 +138,41 @@ __device__ __forceinline__ void read_one(Frags& f, int idx, const v4u* l, int s,
     f.b[i] = x;
 }
 
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+
+// The same fragment from a stage holding an MN-major A slab (64 rows of K, 256
+// elements each, 16-byte chunk c of row k at c ^ 4 (k & 3)) and then the B slab
+// in the same form: within each 16 lanes, lane j names 4 elements of row
+// k0 + (j >> 2) and receives column j of that 4 x 16 block; two reads give the
+// 8 k values of the lane's half.
+__device__ __forceinline__ void read_one_mn(Frags& f, int idx, const v4u* l, int s, int wm, int wn, int lane) {
+  const bool is_a = idx == 0 || idx > 4;
+  const int i = idx == 0 ? 0 : (is_a ? idx - 4 : idx - 1);
+  const char* base = reinterpret_cast<const char*>(l) + (is_a ? 0 : 32768);
+  const int j = lane & 15;
+  const int k = 8 * (2 * s + (lane >> 5)) + (j >> 2);
+  const int m = (is_a ? wm : wn) * 128 + 32 * i + 16 * ((lane >> 4) & 1) + 4 * (j & 3);
+  const int off = k * 512 + (((m >> 3) ^ (4 * (k & 3))) * 16) + (m & 7) * 2;
+  const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(base + off));
+  const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(base + off + 4 * 512));
+  const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+  const v4u x = v4u{a.x, a.y, b.x, b.y};
+  if (is_a)
+    f.a[i] = x;
+  else
+    f.b[i] = x;
+}
+
 __device__ __forceinline__ void dma16(const void* g, uint32_t off, uint32_t lds_base, uint32_t lds_off) {
   asm volatile("s_add_u32 m0, %2, %3\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(g), "s"(lds_base),
                "s"(lds_off)
                : "memory", "m0", "scc");
 }
 
-// Modes 3 and 4 (kCopies): iters K steps of 16 MFMAs each, in slabs of 4 steps.
-template <bool kCopies>
+// Modes 3 and 4 (kCopies), 5 and 6 (kMn and kCopies): iters K steps of 16
+// MFMAs each, in slabs of 4 steps.
+template <bool kCopies, bool kMn>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_lds_probe(int64_t iters, const v4u* src, float* out, int64_t* clk) {
   __shared__ v4u lds[2][4096];
@@ -180,7 +211,12 @@ void k_lds_probe(int64_t iters, const v4u* src, float* out, int64_t* clk) {
                                                                     __builtin_bit_cast(bf16x8_t, cur.b[t % 4]),
                                                                     acc[t / 4][t % 4], 0, 0, 0);
         pin();
-        if (t < 8) read_one(nxt, t, l, (s + 1) & 3, wm, wn, lane);
+        if (t < 8) {
+          if constexpr (kMn)
+            read_one_mn(nxt, t, l, (s + 1) & 3, wm, wn, lane);
+          else
+            read_one(nxt, t, l, (s + 1) & 3, wm, wn, lane);
+        }
         if constexpr (kCopies) {
           if ((s == 3 || s == 0) && (t & 1)) {
             // copy q of this wave: 1 KB of a 64 KB source window (32 windows in 2 MB)
@@ -225,24 +261,31 @@ void k_lds_probe(int64_t iters, const v4u* src, float* out, int64_t* clk) {
 }  // namespace
 
 // Launches `blocks` workgroups of 4 waves, each wave running `iters` rounds of
-// 16 MFMAs (16 x 32 x 32 x 16 x 2 flops per round; modes 3 and 4 need iters a
-// multiple of 4). src: for mode 4, a device buffer of at least 2 MB that the
+// 16 MFMAs (16 x 32 x 32 x 16 x 2 flops per round; modes 3 to 6 need iters a
+// multiple of 4). src: for modes 4 and 6, a device buffer of at least 2 MB that the
 // copies read (ignored otherwise). out: blocks * 256 floats; clk: blocks * 3
 // int64 (per-workgroup s_memtime cycles, s_memrealtime start and end). Returns
 // the HIP status of the launch.
 extern "C" int sao_probe_mfma(int64_t blocks, int64_t iters, int mode, const void* src, float* out, int64_t* clk,
                               hipStream_t stream) {
-  if (blocks < 1 || blocks > (int64_t{1} << 20) || iters < 1 || mode < 0 || mode > 4 || !out || !clk)
+  if (blocks < 1 || blocks > (int64_t{1} << 20) || iters < 1 || mode < 0 || mode > 6 || !out || !clk)
     return static_cast<int>(hipErrorInvalidValue);
-  if (mode >= 3 && (iters % 4 != 0 || (mode == 4 && !src))) return static_cast<int>(hipErrorInvalidValue);
+  if (mode >= 3 && (iters % 4 != 0 || ((mode == 4 || mode == 6) && !src)))
+    return static_cast<int>(hipErrorInvalidValue);
   const unsigned g = static_cast<unsigned>(blocks);
   if (mode <= 2)
     hipLaunchKernelGGL(k_mfma_probe, dim3(g), dim3(256), 0, stream, iters, mode, out, clk);
   else if (mode == 3)
-    hipLaunchKernelGGL(k_lds_probe<false>, dim3(g), dim3(256), 0, stream, iters, static_cast<const v4u*>(src), out,
-                       clk);
+    hipLaunchKernelGGL((k_lds_probe<false, false>), dim3(g), dim3(256), 0, stream, iters,
+                       static_cast<const v4u*>(src), out, clk);
+  else if (mode == 4)
+    hipLaunchKernelGGL((k_lds_probe<true, false>), dim3(g), dim3(256), 0, stream, iters,
+                       static_cast<const v4u*>(src), out, clk);
+  else if (mode == 5)
+    hipLaunchKernelGGL((k_lds_probe<false, true>), dim3(g), dim3(256), 0, stream, iters,
+                       static_cast<const v4u*>(src), out, clk);
   else
-    hipLaunchKernelGGL(k_lds_probe<true>, dim3(g), dim3(256), 0, stream, iters, static_cast<const v4u*>(src), out,
-                       clk);
+    hipLaunchKernelGGL((k_lds_probe<true, true>), dim3(g), dim3(256), 0, stream, iters,
+                       static_cast<const v4u*>(src), out, clk);
   return static_cast<int>(hipGetLastError());
 }
