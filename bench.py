@@ -91,16 +91,24 @@ def copy_calibration(nbytes: int = 1 << 30):
     print(json.dumps({"copy_bytes": nbytes, "launches": 3}), flush=True)
 
 
-def backward_vocab_block(T: int, V: int) -> int:
+def backward_vocab_block(T: int, V: int, H: int, esize: int = 2) -> int:
     """Vocabulary rows per block of sao_loss_backward for T token rows (the rule of
     csrc/layout.hpp: a 32,768-row target, doubled up to 65,536 while the dz product
-    has fewer than 8192 tiles, then V cut into that many equal 256-row multiples)."""
+    has fewer than 8192 tiles, then V cut into that many near-equal blocks; where
+    the block's rows of W fit the 256 MB memory-side cache, each is rounded up to
+    a whole number of rounds of its dW tiles on 256 CUs)."""
+    import math
     tiles_t = -(-T // 256)
     vc = 32768
     while vc < 65536 and tiles_t * (vc // 256) < 8192:
         vc *= 2
     blocks = -(-V // vc)
-    return -(-(-(-V // blocks)) // 256) * 256
+    tiles = -(-(-(-V // blocks)) // 256)
+    align = 256 // math.gcd(256, -(-H // 256))
+    rounded = -(-tiles // align) * align
+    if blocks > 1 and rounded <= vc // 256 and rounded * 256 * H * esize <= 256 << 20:
+        tiles = rounded
+    return tiles * 256
 
 
 def wall_clock_khz() -> Optional[int]:
@@ -758,7 +766,7 @@ def main():
     }
     out["breakdown"] = breakdown(step, T, H, V, esz, t_act, t_grad, torch)
     if args.timeline:
-        vc0 = min(backward_vocab_block(chunk, V), V)
+        vc0 = min(backward_vocab_block(chunk, V, H, esz), V)
         # dH cuts K into pieces when a chunk's token tiles are few (the rule of csrc/layout.hpp)
         pieces = min(max(-(-1024 // (-(-chunk // 256) * -(-H // 256))), 1), 8)
         k_dh = vc0 if pieces == 1 else -(-(-(-vc0 // pieces)) // 64) * 64
@@ -772,7 +780,7 @@ def main():
             out["timelines"][name] = timeline_summary(r, khz, k) if khz and r.shape[0] else None
     if args.vendor_gemm:
         log("vendor GEMM (context)")
-        vc = backward_vocab_block(chunk, V) if cfg.backward else V
+        vc = backward_vocab_block(chunk, V, H, esz) if cfg.backward else V
         out["vendor_gemm_context"] = vendor_gemm(db, t_act, max(t_grad // len(chunks), 1), vc, torch)
     if not args.no_cpu_baseline:
         log("cpu baseline over " + (f"{args.cpu_rows} rows" if args.cpu_rows > 0 else "a quarter of the rows"))

@@ -21,8 +21,6 @@ namespace sao {
 
 // Compacted row buffers are zero-filled up to a multiple of this many rows.
 constexpr int64_t kRowPad = 256;
-// MI355X's memory-side (Infinity) cache, shared by the XCDs.
-constexpr int64_t kMemorySideCacheBytes = int64_t{256} << 20;
 
 // ------------------------------------------------------------------------- //
 // Row compaction
