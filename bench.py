@@ -94,9 +94,9 @@ def copy_calibration(nbytes: int = 1 << 30):
 def backward_vocab_block(T: int, V: int, H: int, esize: int = 2) -> int:
     """Vocabulary rows per block of sao_loss_backward for T token rows (the rule of
     csrc/layout.hpp: a 32,768-row target, doubled up to 65,536 while the dz product
-    has fewer than 8192 tiles, then V cut into that many near-equal blocks; where
-    the block's rows of W fit the 256 MB memory-side cache, each is rounded up to
-    a whole number of rounds of its dW tiles on 256 CUs)."""
+    has fewer than 8192 tiles, then V cut into that many near-equal blocks, each
+    rounded to a whole number of rounds of its dW tiles on 256 CUs: up where the
+    block's rows of W then fit the 256 MB memory-side cache, else down)."""
     import math
     tiles_t = -(-T // 256)
     vc = 32768
@@ -108,6 +108,8 @@ def backward_vocab_block(T: int, V: int, H: int, esize: int = 2) -> int:
     rounded = -(-tiles // align) * align
     if blocks > 1 and rounded <= vc // 256 and rounded * 256 * H * esize <= 256 << 20:
         tiles = rounded
+    elif blocks > 1 and tiles >= align:
+        tiles = tiles // align * align
     return tiles * 256
 
 

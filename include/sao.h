@@ -125,10 +125,11 @@ const char* sao_version(void);
  * elements of the hidden dtype. Vb comes from a target Vt = 32768 rows, doubled
  * (up to 65536) while (round_up(T, 256) / 256) x (Vt / 256) < 8192: V is cut into
  * n = ceil(V / Vt) blocks of b = ceil(ceil(V / n) / 256) tiles of 256 rows. When
- * n > 1, b is then rounded up to a multiple of 256 / gcd(256, ceil(H / 256)) if
- * that stays within Vt / 256 tiles and 256 x b x H elements fit in 256 MiB.
- * Vb = 256 b (32768 rows for V = 151936, H = 2048 bf16 at T = 65536; 30464 for
- * H = 6144). */
+ * n > 1, b is then rounded up to a multiple m of 256 / gcd(256, ceil(H / 256)) if
+ * that stays within Vt / 256 tiles and 256 x b x H elements fit in 256 MiB, and
+ * otherwise rounded down to a multiple of m if b >= m. Vb = 256 b (32768 rows for
+ * V = 151936, H = 2048 bf16 at T = 65536; 24576 for V = 151552, H = 6144 at
+ * T = 32768). */
 size_t sao_workspace_size(sao_op_t op, int64_t T, int64_t H, int64_t V, sao_dtype_t dtype);
 
 /*
