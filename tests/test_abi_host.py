@@ -239,6 +239,48 @@ def test_workspace_sizes(L):
     assert 0 < ws(binding.OP_VALUE, 32768, 6144, 1, 0) < 32768 * 6144 * 2 // 16
 
 
+def _block_rule(T, H, V, esize):
+    """The backward's vocabulary block as include/sao.h states it for
+    sao_workspace_size."""
+    from math import gcd
+    tiles_t = -(-T // 256)
+    vt = 32768
+    while vt < 65536 and tiles_t * (vt // 256) < 8192:
+        vt *= 2
+    n = -(-V // vt)
+    b = -(-(-(-V // n)) // 256)
+    m = 256 // gcd(256, -(-H // 256))
+    if n > 1:
+        up = -(-b // m) * m
+        if up <= vt // 256 and 256 * up * H * esize <= 256 << 20:
+            b = up
+        elif b >= m:
+            b = b // m * m
+    return 256 * b
+
+
+@pytest.mark.parametrize("T,H,V,dt", [
+    (65536, 2048, 151936, 0),   # rounded up to whole dW rounds: 4 x 32768 + 20864
+    (65536, 2048, 151936, 1),   # fp32: 256 x 128 x 2048 x 4 bytes is exactly 256 MiB, still rounded up
+    (65536, 4096, 151936, 1),   # fp32 at H = 4096: 32768-row blocks would not fit, rounded down to 28672
+    (32768, 6144, 151552, 0),   # W's block beyond the cache: rounded down to 24576
+    (8192, 2048, 151936, 0),    # a short chunk: 65536-row target, 2 x 57344 + 37248
+    (640, 64, 140000, 0),       # H = 64: 256-tile multiples
+    (65536, 2048, 20000, 0),    # a single block: V rounded to a whole tile
+    (3000, 768, 99999, 1),      # H = 768: a multiple of 256 tiles, the whole 65536-row target
+    (65536, 2304, 151936, 0),   # H = 2304: 256-tile multiples exceed the target, blocks left equal
+])
+def test_backward_block_rule(L, T, H, V, dt):
+    # the workspace differs between two vocabularies by the dz block alone
+    # (esize x round_up(T, 256) x Vb bytes); V = 256 gives a one-tile block
+    ws = binding.workspace_size
+    esize = 2 if dt == 0 else 4
+    t_pad = -(-T // 256) * 256
+    d = ws(binding.OP_BACKWARD, T, H, V, dt) - ws(binding.OP_BACKWARD, T, H, 256, dt)
+    assert d % (esize * t_pad) == 0
+    assert d // (esize * t_pad) + 256 == _block_rule(T, H, V, esize)
+
+
 def test_error_message_is_per_thread(L):
     # Two threads fail with different errors at the same time; each reads its own
     # message (the library keeps the last message per calling thread).
