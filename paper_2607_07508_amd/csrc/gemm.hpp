@@ -377,6 +377,10 @@ __device__ __forceinline__ void epi_mark(Epi& epi, int phase) {
   if constexpr (HasMark<Epi>::value) epi.mark(phase);
 }
 
+template <class E, bool AMn, bool BMn, class Epi>
+__device__ __forceinline__ void gemm_tile(const GemmShape& s, Epi& epi, v4u (*lds)[kStageChunks], int mt,
+                                          int n_tile);
+
 // The generic kernel body: one 256 x 256 tile per workgroup. Epi provides:
 //   begin(n0, wm, wn, lane)                 before the K loop
 //   tile(acc, m0, n0, wm, wn, lane, lds)    after it (LDS is free)
@@ -384,12 +388,6 @@ __device__ __forceinline__ void epi_mark(Epi& epi, int phase) {
 // AMn / BMn select the MN-major layout for A / B.
 template <class E, bool AMn, bool BMn, class Epi>
 __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*lds)[kStageChunks]) {
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = static_cast<int>(uniform_u32(static_cast<uint32_t>(tid >> 6)));  // keeps copy addresses scalar
-  const int wm = wave / kWavesN;
-  const int wn = wave % kWavesN;
-
   // Raster: block -> (N tile, M tile).
   const int b = blockIdx.x;
   const int sn = s.sn;
@@ -405,6 +403,19 @@ __device__ __forceinline__ void gemm_body(const GemmShape& s, Epi& epi, v4u (*ld
     n_tile = (w % nw) * 8 * sn + (slot % sn) * 8 + (xcd + w / nw) % 8;
     mt = (w / nw) * (32 / sn) + slot / sn;
   }
+  gemm_tile<E, AMn, BMn>(s, epi, lds, mt, n_tile);
+}
+
+// Tile (mt, n_tile) of the product, K piece blockIdx.y; nothing if the tile
+// lies past the valid rows.
+template <class E, bool AMn, bool BMn, class Epi>
+__device__ __forceinline__ void gemm_tile(const GemmShape& s, Epi& epi, v4u (*lds)[kStageChunks], int mt,
+                                          int n_tile) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = static_cast<int>(uniform_u32(static_cast<uint32_t>(tid >> 6)));  // keeps copy addresses scalar
+  const int wm = wave / kWavesN;
+  const int wn = wave % kWavesN;
 
   const int64_t n_valid = s.n_dev ? static_cast<int64_t>(*s.n_dev) : s.n;
   const int64_t m_valid = s.m_dev ? static_cast<int64_t>(*s.m_dev) : s.m;

@@ -42,8 +42,9 @@ __device__ __forceinline__ T block_sum_256(T v, T* sh) {
 }
 
 __global__ __launch_bounds__(256) void k_count_rows(const uint8_t* mask, const float* g, int64_t T,
-                                                    int32_t* blk_counts) {
+                                                    int32_t* blk_counts, int32_t* zero8) {
   __shared__ int32_t sh[4];
+  if (zero8 && blockIdx.x == 0 && threadIdx.x < 8) zero8[threadIdx.x] = 0;
   const int64_t base = static_cast<int64_t>(blockIdx.x) * kRowsPerCountBlock + threadIdx.x * 4;
   int32_t c = 0;
 #pragma unroll
@@ -255,16 +256,15 @@ struct EpiLse {
   }
 };
 
-// With `clk` (a measurement hook, normally null), workgroup b (blockIdx.x plus
-// blockIdx.y times gridDim.x) < clk_slots records its timeline in clk[8b .. 8b+7]:
-// the hardware ids of its wave 0 (HW_REG_XCC_ID << 32 | HW_REG_HW_ID), its start
-// and end on the constant wall clock (s_memrealtime), the shader clock
-// (s_memtime) at its start, after the prologue, after the K loop and at its end,
-// and its tile. c0 and r0 are the start readings.
+// With `clk` (a measurement hook, normally null), slot b < clk_slots (by default
+// the workgroup, blockIdx.x plus blockIdx.y times gridDim.x) records a tile's
+// timeline in clk[8b .. 8b+7]: the hardware ids of its wave 0 (HW_REG_XCC_ID << 32
+// | HW_REG_HW_ID), its start and end on the constant wall clock (s_memrealtime),
+// the shader clock (s_memtime) at its start, after the prologue, after the K loop
+// and at its end, and its tile. c0 and r0 are the start readings.
 __device__ __forceinline__ void write_clock_record(int64_t* clk, int64_t clk_slots, uint64_t c0, uint64_t r0,
-                                                   const TileClock& tc) {
-  const int64_t b = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
-  if (!clk || threadIdx.x != 0 || b >= clk_slots) return;
+                                                   const TileClock& tc, int64_t b) {
+  if (!clk || threadIdx.x != 0 || b < 0 || b >= clk_slots) return;
   const uint64_t c1 = __builtin_amdgcn_s_memtime();
   const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
   // s_getreg_b32 of the whole HW_ID (register 4) and XCC_ID (register 20)
@@ -279,6 +279,10 @@ __device__ __forceinline__ void write_clock_record(int64_t* clk, int64_t clk_slo
   rec[5] = static_cast<int64_t>(tc.t_mark[1]);
   rec[6] = static_cast<int64_t>(c1);
   rec[7] = tc.tile_id;
+}
+__device__ __forceinline__ void write_clock_record(int64_t* clk, int64_t clk_slots, uint64_t c0, uint64_t r0,
+                                                   const TileClock& tc) {
+  write_clock_record(clk, clk_slots, c0, r0, tc, static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x);
 }
 
 // The head forward, with the timeline hook above (the tile is vocabulary tile
@@ -297,6 +301,61 @@ void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t tile0, int64_t* 
   epi.clock.start(clk != nullptr);
   gemm_body<E, false, false>(s, epi, lds);
   write_clock_record(clk, clk_slots, c0, r0, epi.clock);
+}
+
+__global__ __launch_bounds__(256) void k_fill_i64(int64_t* p, int64_t n, int64_t v) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    p[i] = v;
+}
+
+// The head forward over the full vocabulary tiles, as a grid of workgroups (a
+// multiple of 8, normally one per CU) that pull tiles until none is left,
+// instead of one workgroup per tile. Workgroup b runs on XCD b % 8 and takes
+// the tiles of that XCD's vocabulary tiles (v with v % 8 == b % 8) from the
+// XCD's own counter next[b % 8] (zeroed before the launch), in groups of 4
+// vocabulary tiles x 8 token tiles, so that the 32 tiles an XCD runs at once
+// share 12 operand panels in its L2. Only valid token tiles (below the device
+// count) are enumerated, so no workgroup is dispatched for nothing, and a
+// workgroup takes its next tile as soon as it is free, whichever shader engine
+// it sits on. The timeline hook records tile (v, t) in slot v x n_tiles + t.
+template <class E>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_head_fwd_pull(GemmShape s, float2* part, int64_t ldp, int32_t* next, int64_t* clk, int64_t clk_slots) {
+  __shared__ v4u lds[kStages][kStageChunks];
+  __shared__ int32_t s_idx;
+  const int xcd = static_cast<int>(blockIdx.x & 7);
+  const int64_t n_valid = s.n_dev ? static_cast<int64_t>(*s.n_dev) : s.n;
+  const int64_t nv64 = (n_valid + kBN - 1) / kBN;
+  const int nv = static_cast<int>(nv64 < s.n_tiles ? nv64 : s.n_tiles);        // valid token tiles
+  const int mx = xcd < s.m_tiles ? (s.m_tiles - 1 - xcd) / 8 + 1 : 0;            // this XCD's vocabulary tiles
+  const int32_t total = mx * nv;
+  EpiLse<false> epi;
+  epi.part = part;
+  epi.ldp = ldp;
+  epi.M = s.m;
+  epi.tile0 = 0;
+  for (;;) {
+    if (threadIdx.x == 0) s_idx = atomicAdd(next + xcd, 1);
+    __syncthreads();  // also: the previous tile's epilogue is done with LDS
+    const int32_t idx = s_idx;
+    __syncthreads();  // every thread has read s_idx
+    if (idx >= total) break;
+    // idx -> (group of up to 4 vocabulary tiles, token tile wave of up to 8, tile within it)
+    const int g = idx / (4 * nv);
+    const int msz = mx - 4 * g < 4 ? mx - 4 * g : 4;
+    const int rem = idx - g * 4 * nv;
+    const int nwave = rem / (msz * 8);
+    const int r2 = rem - nwave * msz * 8;
+    const int nsz = nv - 8 * nwave < 8 ? nv - 8 * nwave : 8;
+    const int mt = (4 * g + r2 / nsz) * 8 + xcd;
+    const int n_tile = 8 * nwave + r2 % nsz;
+    const uint64_t c0 = clk ? __builtin_amdgcn_s_memtime() : 0;
+    const uint64_t r0 = clk ? __builtin_amdgcn_s_memrealtime() : 0;
+    epi.clock.start(clk != nullptr);
+    gemm_tile<E, false, false>(s, epi, lds, mt, n_tile);
+    write_clock_record(clk, clk_slots, c0, r0, epi.clock, static_cast<int64_t>(mt) * s.n_tiles + n_tile);
+  }
 }
 
 template <class E>
@@ -688,6 +747,25 @@ static GemmShape make_shape(const void* a, int64_t lda, int64_t m, const void* b
   return s;
 }
 
+// Host-bound token tiles up to which the forward pulls its tiles
+// (k_head_fwd_pull) rather than launching one workgroup per tile of the host
+// bound. Measured per workload against the one-workgroup-per-tile raster: an
+// 8192-token chunk (32 host-bound tiles, about 16 with loss-mask rows) 7 %
+// faster; 32,768 tokens at H = 6144 (128 tiles) 4 % slower, 65,536 tokens
+// (256) 0.7 % slower.
+constexpr int kPullMaxNTiles = 32;
+
+// Workgroups of a pulling launch: one per CU of the current device, rounded
+// down to a multiple of 8 (the XCDs), at least 8.
+static int pull_grid() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus = 256;
+  cus = cus / 8 * 8;
+  return cus < 8 ? 8 : cus;
+}
+
 template <class E>
 static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void* w_head, int64_t ld_w,
                                const int32_t* target, const uint8_t* mask, int64_t T, int64_t H,
@@ -703,7 +781,8 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
   float2* part = reinterpret_cast<float2*>(w8 + L.part);
 
   const int nb = static_cast<int>(L.n_count_blocks);
-  hipLaunchKernelGGL(k_count_rows, dim3(nb), dim3(256), 0, st, mask, nullptr, T, blk);
+  int32_t* next = reinterpret_cast<int32_t*>(w8 + L.next);
+  hipLaunchKernelGGL(k_count_rows, dim3(nb), dim3(256), 0, st, mask, nullptr, T, blk, next);
   hipLaunchKernelGGL(k_compact_rows, dim3(nb), dim3(256), 0, st, mask, nullptr, T, blk, idx,
                      nullptr, count, logp, lse);
   const int rows4 = static_cast<int>(L.t_pad / 4);
@@ -723,10 +802,20 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
   if (full_tiles > 0) {
     GemmShape s = make_shape(w_head, ld_w, full_tiles * kBM, hc, H, T, H);
     s.n_dev = count;
-    s.msplit = 1;
-    s.sn = pick_sn_msplit(s.n_tiles);
-    hipLaunchKernelGGL((k_head_fwd<E, false>), dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad,
-                       int64_t{0}, tm.clocks_for(SAO_KERNEL_HEAD_FORWARD), tm.clock_slots);
+    int64_t* clk = tm.clocks_for(SAO_KERNEL_HEAD_FORWARD);
+    if (s.n_tiles <= kPullMaxNTiles) {
+      // The pulling kernel records by tile, not by workgroup: clear the records
+      // first, so that this launch's are the only ones left.
+      if (clk)
+        hipLaunchKernelGGL(k_fill_i64, dim3(64), dim3(256), 0, st, clk, 8 * tm.clock_slots, int64_t{0});
+      hipLaunchKernelGGL(k_head_fwd_pull<E>, dim3(static_cast<unsigned>(pull_grid())), dim3(kThreads), 0, st, s,
+                         part, L.t_pad, next, clk, tm.clock_slots);
+    } else {
+      s.msplit = 1;
+      s.sn = pick_sn_msplit(s.n_tiles);
+      hipLaunchKernelGGL((k_head_fwd<E, false>), dim3(gemm_grid(s)), dim3(kThreads), 0, st, s, part, L.t_pad,
+                         int64_t{0}, clk, tm.clock_slots);
+    }
   }
   if (rem > 0) {
     // A single row of tiles: the M-split raster would deal its one M tile to one
@@ -766,7 +855,7 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
   const S* w = static_cast<const S*>(w_head);
 
   const int nb = static_cast<int>(L.n_count_blocks);
-  hipLaunchKernelGGL(k_count_rows, dim3(nb), dim3(256), 0, st, nullptr, g, T, blk);
+  hipLaunchKernelGGL(k_count_rows, dim3(nb), dim3(256), 0, st, nullptr, g, T, blk, static_cast<int32_t*>(nullptr));
   hipLaunchKernelGGL(k_compact_rows, dim3(nb), dim3(256), 0, st, nullptr, g, T, blk, idx, pos, count,
                      nullptr, nullptr);
   const int rows4 = static_cast<int>(L.t_pad / 4);

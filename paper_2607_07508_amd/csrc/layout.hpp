@@ -30,7 +30,7 @@ struct Carve {
 // sao_token_logprob
 struct LogprobLayout {
   int64_t t_pad, n_count_blocks, m_tiles;
-  size_t blk_counts, count, idx, hc, part, total;
+  size_t blk_counts, count, next, idx, hc, part, total;
 };
 
 inline LogprobLayout logprob_layout(int64_t T, int64_t H, int64_t V, size_t esize) {
@@ -41,6 +41,7 @@ inline LogprobLayout logprob_layout(int64_t T, int64_t H, int64_t V, size_t esiz
   Carve c;
   L.blk_counts = c.take(4 * static_cast<size_t>(L.n_count_blocks));
   L.count = c.take(4);
+  L.next = c.take(4 * 8);  // the forward's tile counters, one per XCD
   L.idx = c.take(4 * static_cast<size_t>(L.t_pad));
   L.hc = c.take(esize * static_cast<size_t>(L.t_pad) * static_cast<size_t>(H));
   L.part = c.take(8 * static_cast<size_t>(L.m_tiles) * static_cast<size_t>(L.t_pad));
