@@ -158,7 +158,9 @@ def forward_clock(step, torch, dev, B) -> dict:
 def timeline_summary(r, khz, k=None) -> dict:
     """Where a head kernel's tile time goes: per-tile prologue, K loop and epilogue
     cycles, and per CU the wall-clock gaps between one workgroup's end and the next
-    one's start, in cycles at the measured clock. With the contraction length k,
+    one's start, in cycles at the measured clock; the range of the CUs' busy
+    fractions and of the tiles per shader engine (XCC and SE from the hardware
+    ids). With the contraction length k,
     also the MFMA cycles a tile needs (256 x 256 x k x 2 flop at 4 SIMDs x 1024
     bf16 flop per cycle) and the K loop's MFMA efficiency."""
     clk = (r[:, 6] - r[:, 3]).sum() / ((r[:, 2] - r[:, 1]).sum() / (khz * 1e3))
@@ -175,6 +177,10 @@ def timeline_summary(r, khz, k=None) -> dict:
     g = np.concatenate(gaps) if gaps else np.zeros(0)
     span = (r[:, 2].max() - r[:, 1].min()) / (khz * 1e3)
     busy = ((r[:, 2] - r[:, 1]).sum() / (khz * 1e3)) / (len(per_cu) * span)
+    # per CU, the fraction of the span it held a tile; per shader engine (XCC, SE), its tiles
+    held = [((r[cu == c, 2] - r[cu == c, 1]).sum() / (khz * 1e3)) / span for c in per_cu]
+    se = (hw >> 32) * 8 + ((hw >> 13) & 7)
+    per_se = np.unique(se, return_counts=True)[1]
     mfma = 256 * 256 * 2 * k / 4096 if k else None
     return {"clock_mhz": clk / 1e6, "tiles": int(r.shape[0]), "cus": len(per_cu),
             "k": k, "mfma_cycles_per_tile": mfma,
@@ -184,7 +190,9 @@ def timeline_summary(r, khz, k=None) -> dict:
                                 "epilogue": float(epi.mean()), "total": float((pro + loop + epi).mean())},
             "gap_cycles_between_tiles": {"median": float(np.median(g)) if g.size else None,
                                          "mean": float(g.mean()) if g.size else None},
-            "cu_busy_fraction": float(busy), "launch_span_ms": float(span * 1e3)}
+            "cu_busy_fraction": float(busy), "cu_busy_range": [float(min(held)), float(max(held))],
+            "tiles_per_shader_engine": [int(per_se.min()), int(per_se.max())],
+            "launch_span_ms": float(span * 1e3)}
 
 
 def vendor_gemm(db, t_act: int, t_grad: int, vc: int, torch, reps: int = 3):
