@@ -109,6 +109,28 @@ def test_accumulation_and_determinism():
     check_grad(dw, 2 * ref["dw"], None, "dw x2")
 
 
+def test_forward_launch_forms_agree():
+    """Up to 8192 tokens the forward runs one workgroup per CU pulling tiles; above
+    it, one workgroup per tile. Both compute every tile's log-sum-exp partials the
+    same way and merge them in the same order, so the first 8192 rows come out
+    bit for bit the same either way; sampled rows match the oracle."""
+    T, H, V = 8193, 64, 3000
+    b = generate(small_config("launch-forms", 27, B=8, T=T, H=H, V=V))
+    hid = torch.from_numpy(bf16_bits(b.hidden)).view(torch.bfloat16).cuda()
+    w = torch.from_numpy(bf16_bits(b.w_head)).view(torch.bfloat16).cuda()
+    tgt = torch.from_numpy(b.target).cuda()
+    mask = torch.from_numpy(b.mask).cuda()
+    say(f"case launch-forms: T={T} (tiles pulled) and {T - 1} (one workgroup per tile), H={H} V={V}")
+    lp_a, lse_a = sao.token_logprob(hid, w, tgt, mask)                       # 8193 rows: one workgroup per tile
+    lp_b, lse_b = sao.token_logprob(hid[:T - 1], w, tgt[:T - 1], mask[:T - 1])  # 8192 rows: pulled
+    torch.cuda.synchronize()
+    assert torch.equal(lp_a[:T - 1], lp_b) and torch.equal(lse_a[:T - 1], lse_b)
+    rows = np.nonzero(b.mask)[0][::97]
+    ref_lp, ref_lse = oracle.token_logprob(b.hidden, b.w_head, b.target, rows=rows)
+    assert np.abs(lp_b.cpu().numpy()[rows] - ref_lp[rows]).max() <= TOL_LOGP
+    assert np.abs(lse_b.cpu().numpy()[rows] - ref_lse[rows]).max() <= TOL_LOGP
+
+
 def test_chunked_equals_whole():
     """Token chunks with the global N: losses, counts and dW sum to the whole-batch values."""
     b = generate(small_config("chunks", 26, B=3, T=1200, H=64, V=900))
