@@ -611,6 +611,7 @@ struct EpiAcc {
   int64_t m_valid;
   int64_t n_valid;
   int64_t split_stride;  // elements between the outputs of successive K pieces
+  bool overwrite;        // store the tile instead of adding it (the first contribution)
   TileClock clock;       // measurement hook
 
   __device__ __forceinline__ void mark(int phase) { clock.mark(phase); }
@@ -628,6 +629,20 @@ struct EpiAcc {
       // address register (global address space, so that they are not flat).
       using gchar = __attribute__((address_space(1))) char;
       const uint32_t lane_off = static_cast<uint32_t>((4 * (lane >> 5) * ldo + (lane & 31)) * 4);
+      if (overwrite) {
+#pragma unroll
+        for (int ni = 0; ni < kNI; ++ni)
+#pragma unroll
+          for (int mi = 0; mi < kMI; ++mi) {
+            gchar* b = (gchar*)uniform_ptr(out + (m0 + wm * (kBM / 2) + mi * 32) * ldo + n0 +
+                                           wn * (kBN / kWavesN) + ni * 32);
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              *(__attribute__((address_space(1))) float*)(b + ((r & 3) + 8 * (r >> 2)) * ldo * 4 + lane_off) =
+                  acc_read(acc[mi][ni][r]);
+          }
+        return;
+      }
 #pragma unroll
       for (int ni = 0; ni < kNI; ++ni) {
         float v[kMI][16];
@@ -661,7 +676,7 @@ struct EpiAcc {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t m = m0 + acc_row(wm, mi, r, lane);
-          if (m < m_valid) out[m * ldo + n] += acc_read(acc[mi][ni][r]);
+          if (m < m_valid) out[m * ldo + n] = acc_read(acc[mi][ni][r]) + (overwrite ? 0.0f : out[m * ldo + n]);
         }
     }
   }
@@ -694,13 +709,13 @@ void k_bwd_acc(GemmShape s, EpiAcc epi, int64_t* clk, int64_t clk_slots) {
 }
 
 
-// Zero rows [0, round_up(*count, 256)) of a [rows][H] fp32 buffer.
-// Zero rows [0, round_up(count, kRowPad)) of `pieces` accumulators `stride` floats apart.
-__global__ __launch_bounds__(256) void k_zero_rows(float* p, int64_t H, const int32_t* count, int pieces,
+// Zero rows [0, round_up(count, kRowPad)) of accumulators q0 .. pieces - 1, `stride`
+// floats apart.
+__global__ __launch_bounds__(256) void k_zero_rows(float* p, int64_t H, const int32_t* count, int q0, int pieces,
                                                    int64_t stride) {
   const int64_t c = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (c >= round_up_dev(*count, kRowPad)) return;
-  for (int q = 0; q < pieces; ++q) {
+  for (int q = q0; q < pieces; ++q) {
     float4* r = reinterpret_cast<float4*>(p + q * stride + c * H);
     for (int64_t k = threadIdx.x & 63; k < H / 4; k += 64) r[k] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
@@ -862,7 +877,18 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
   hipLaunchKernelGGL(k_gather_rows<E>, dim3(rows4), dim3(256), 0, st, static_cast<const S*>(hidden),
                      ld_hidden, H, idx, count, hg, target, y_c, g, g_c, lse, lse_c);
   const int64_t dh_stride = L.t_pad * H;
-  hipLaunchKernelGGL(k_zero_rows, dim3(rows4), dim3(256), 0, st, dh, H, count, L.dh_pieces, dh_stride);
+  // dH's K pieces for a block of vlen rows (each piece has its own accumulator).
+  auto dh_split = [&](int64_t vlen) { return L.dh_pieces > 1 ? round_up(ceil_div(vlen, L.dh_pieces), 64) : int64_t{0}; };
+  auto dh_pieces_of = [&](int64_t vlen) {
+    return L.dh_pieces > 1 ? static_cast<int>(ceil_div(vlen, dh_split(vlen))) : 1;
+  };
+  // The first vocabulary block stores its dH tiles rather than adding them, so
+  // only accumulators it has no K piece for need zeros. (Rows past the count in
+  // the last token tile are written too, with values nothing reads.)
+  const int first_pieces = dh_pieces_of(V < L.vc ? V : L.vc);
+  if (first_pieces < L.dh_pieces)
+    hipLaunchKernelGGL(k_zero_rows, dim3(rows4), dim3(256), 0, st, dh, H, count, first_pieces, L.dh_pieces,
+                       dh_stride);
 
   // The measurement hooks apply to the first vocabulary block's launches.
   const KernelTimer& tm = kernel_timer();
@@ -906,9 +932,9 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
     sb.m_dev = count;
     sb.msplit = 1;
     sb.sn = pick_sn_msplit(sb.n_tiles);
-    sb.k_split = L.dh_pieces > 1 ? round_up(ceil_div(vlen, L.dh_pieces), 64) : 0;
-    const int pieces_b = L.dh_pieces > 1 ? static_cast<int>(ceil_div(vlen, sb.k_split)) : 1;
-    EpiAcc eb{dh, H, L.t_pad, H, dh_stride, {}};
+    sb.k_split = dh_split(vlen);
+    const int pieces_b = dh_pieces_of(vlen);
+    EpiAcc eb{dh, H, L.t_pad, H, dh_stride, vb == 0, {}};
     hook(vb, SAO_KERNEL_BACKWARD_DH, false);
     hipLaunchKernelGGL((k_bwd_acc<E, false, true>), dim3(gemm_grid(sb), pieces_b), dim3(kThreads), 0, st, sb,
                        eb, clocks(vb, SAO_KERNEL_BACKWARD_DH), tm.clock_slots);
@@ -918,7 +944,7 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
     sc.k_dev = count;
     sc.msplit = 1;
     sc.sn = pick_sn_msplit(sc.n_tiles);
-    EpiAcc ec{dw + v0 * H, H, vlen, H, 0, {}};
+    EpiAcc ec{dw + v0 * H, H, vlen, H, 0, false, {}};
     hook(vb, SAO_KERNEL_BACKWARD_DW, false);
     hipLaunchKernelGGL((k_bwd_acc<E, true, true>), dim3(gemm_grid(sc)), dim3(kThreads), 0, st, sc, ec,
                        clocks(vb, SAO_KERNEL_BACKWARD_DW), tm.clock_slots);
