@@ -402,9 +402,9 @@ void sao_debug_time_kernel(int kernel, void* start_event, void* stop_event);
  * tile (M tile << 32 | N tile of the product, -1 for none; for the head forward
  * the vocabulary tile and the token tile). Workgroup b is blockIdx.x plus
  * blockIdx.y times the grid's x size. The head forward at up to 8192 tokens runs
- * a fixed grid of workgroups that each take many tiles; there the records are per
- * tile instead, tile (v, t) in slot b = v x ceil(T / 256) + t, and the launch
- * clears all slots first. Summed cycles over summed wall-clock time give the
+ * one launch of a fixed grid of workgroups that each take many tiles, the partial
+ * last vocabulary tile's included; there the records are per tile instead, tile
+ * (v, t) in slot b = v x ceil(T / 256) + t, and the launch clears all slots first. Summed cycles over summed wall-clock time give the
  * clock the kernel ran at. SAO_KERNEL_NONE, NULL or slots <= 0 disables it. Each
  * launch overwrites the records of the previous one.
  */

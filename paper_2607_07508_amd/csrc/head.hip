@@ -321,7 +321,8 @@ __global__ __launch_bounds__(256) void k_fill_i64(int64_t* p, int64_t n, int64_t
 // it sits on. The timeline hook records tile (v, t) in slot v x n_tiles + t.
 template <class E>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void k_head_fwd_pull(GemmShape s, float2* part, int64_t ldp, int32_t* next, int64_t* clk, int64_t clk_slots) {
+void k_head_fwd_pull(GemmShape s, GemmShape st, float2* part, int64_t ldp, int32_t* next, int64_t* clk,
+                     int64_t clk_slots) {
   __shared__ v4u lds[kStages][kStageChunks];
   __shared__ int32_t s_idx;
   const int xcd = static_cast<int>(blockIdx.x & 7);
@@ -330,17 +331,33 @@ void k_head_fwd_pull(GemmShape s, float2* part, int64_t ldp, int32_t* next, int6
   const int nv = static_cast<int>(nv64 < s.n_tiles ? nv64 : s.n_tiles);        // valid token tiles
   const int mx = xcd < s.m_tiles ? (s.m_tiles - 1 - xcd) / 8 + 1 : 0;            // this XCD's vocabulary tiles
   const int32_t total = mx * nv;
+  // then the partial last vocabulary tile's token tiles t with t % 8 == xcd (st.m > 0)
+  const int32_t tail = st.m > 0 && xcd < nv ? (nv - 1 - xcd) / 8 + 1 : 0;
   EpiLse<false> epi;
   epi.part = part;
   epi.ldp = ldp;
   epi.M = s.m;
   epi.tile0 = 0;
+  EpiLse<true> epi_t;
+  epi_t.part = part;
+  epi_t.ldp = ldp;
+  epi_t.M = st.m;
+  epi_t.tile0 = s.m_tiles;
   for (;;) {
     if (threadIdx.x == 0) s_idx = atomicAdd(next + xcd, 1);
     __syncthreads();  // also: the previous tile's epilogue is done with LDS
     const int32_t idx = s_idx;
     __syncthreads();  // every thread has read s_idx
-    if (idx >= total) break;
+    if (idx >= total + tail) break;
+    if (idx >= total) {
+      const int n_tile = (idx - total) * 8 + xcd;
+      const uint64_t c0 = clk ? __builtin_amdgcn_s_memtime() : 0;
+      const uint64_t r0 = clk ? __builtin_amdgcn_s_memrealtime() : 0;
+      epi_t.clock.start(clk != nullptr);
+      gemm_tile<E, false, false>(st, epi_t, lds, 0, n_tile);
+      write_clock_record(clk, clk_slots, c0, r0, epi_t.clock, static_cast<int64_t>(s.m_tiles) * s.n_tiles + n_tile);
+      continue;
+    }
     // idx -> (group of up to 4 vocabulary tiles, token tile wave of up to 8, tile within it)
     const int g = idx / (4 * nv);
     const int msz = mx - 4 * g < 4 ? mx - 4 * g : 4;
@@ -814,6 +831,7 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
   // token count: each XCD streams its own W panels while all of them read the
   // same hidden rows, which the memory-side cache holds (measured 0.7 % faster
   // than splitting the tokens at 65,536 tokens).
+  bool tail_done = false;
   if (full_tiles > 0) {
     GemmShape s = make_shape(w_head, ld_w, full_tiles * kBM, hc, H, T, H);
     s.n_dev = count;
@@ -823,8 +841,15 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
       // first, so that this launch's are the only ones left.
       if (clk)
         hipLaunchKernelGGL(k_fill_i64, dim3(64), dim3(256), 0, st, clk, 8 * tm.clock_slots, int64_t{0});
+      // It also takes the partial last vocabulary tile's tiles, at the end of each XCD's list.
+      GemmShape stail{};
+      if (rem > 0) {
+        stail = make_shape(static_cast<const S*>(w_head) + full_tiles * kBM * ld_w, ld_w, rem, hc, H, T, H);
+        stail.n_dev = count;
+      }
       hipLaunchKernelGGL(k_head_fwd_pull<E>, dim3(static_cast<unsigned>(pull_grid())), dim3(kThreads), 0, st, s,
-                         part, L.t_pad, next, clk, tm.clock_slots);
+                         stail, part, L.t_pad, next, clk, tm.clock_slots);
+      tail_done = true;
     } else {
       s.msplit = 1;
       s.sn = pick_sn_msplit(s.n_tiles);
@@ -832,7 +857,7 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
                          int64_t{0}, clk, tm.clock_slots);
     }
   }
-  if (rem > 0) {
+  if (rem > 0 && !tail_done) {
     // A single row of tiles: the M-split raster would deal its one M tile to one
     // XCD, so the tiles are dealt out along N (make_shape's choice for many token
     // tiles) and spread over all 8 XCDs.
