@@ -401,10 +401,12 @@ void sao_debug_time_kernel(int kernel, void* start_event, void* stop_event);
  * at its start, after its prologue, after its K loop and at its end, and its
  * tile (M tile << 32 | N tile of the product, -1 for none; for the head forward
  * the vocabulary tile and the token tile). Workgroup b is blockIdx.x plus
- * blockIdx.y times the grid's x size. The head forward at up to 8192 tokens runs
- * one launch of a fixed grid of workgroups that each take many tiles, the partial
- * last vocabulary tile's included; there the records are per tile instead, tile
- * (v, t) in slot b = v x ceil(T / 256) + t, and the launch clears all slots first. Summed cycles over summed wall-clock time give the
+ * blockIdx.y times the grid's x size. At up to 8192 tokens the head forward and
+ * the backward's logit recompute run one launch (per vocabulary block) of a fixed
+ * grid of workgroups that each take many tiles, the partial last vocabulary tile's
+ * included; there the records are per tile instead, tile (v, t) of the launch's
+ * vocabulary range in slot b = v x ceil(T / 256) + t, and the launch clears all
+ * slots first. Summed cycles over summed wall-clock time give the
  * clock the kernel ran at. SAO_KERNEL_NONE, NULL or slots <= 0 disables it. Each
  * launch overwrites the records of the previous one.
  */

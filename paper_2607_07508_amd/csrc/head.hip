@@ -42,9 +42,10 @@ __device__ __forceinline__ T block_sum_256(T v, T* sh) {
 }
 
 __global__ __launch_bounds__(256) void k_count_rows(const uint8_t* mask, const float* g, int64_t T,
-                                                    int32_t* blk_counts, int32_t* zero8) {
+                                                    int32_t* blk_counts, int32_t* zero, int n_zero) {
   __shared__ int32_t sh[4];
-  if (zero8 && blockIdx.x == 0 && threadIdx.x < 8) zero8[threadIdx.x] = 0;
+  if (blockIdx.x == 0)
+    for (int i = threadIdx.x; i < n_zero; i += blockDim.x) zero[i] = 0;
   const int64_t base = static_cast<int64_t>(blockIdx.x) * kRowsPerCountBlock + threadIdx.x * 4;
   int32_t c = 0;
 #pragma unroll
@@ -303,6 +304,22 @@ void k_head_fwd(GemmShape s, float2* part, int64_t ldp, int64_t tile0, int64_t* 
   write_clock_record(clk, clk_slots, c0, r0, epi.clock);
 }
 
+// Tile idx (< mx * nv) of an XCD's list in a pulling launch: its vocabulary
+// tiles v (v % 8 == xcd, mx of them) against the nv valid token tiles, in groups
+// of up to 4 vocabulary tiles, and within a group in waves of up to 8 token tiles,
+// vocabulary tile by vocabulary tile. The 32 tiles an XCD runs at once thus share
+// 12 operand panels in its L2.
+__device__ __forceinline__ void pull_tile(int idx, int mx, int nv, int xcd, int& mt, int& n_tile) {
+  const int g = idx / (4 * nv);
+  const int msz = mx - 4 * g < 4 ? mx - 4 * g : 4;
+  const int rem = idx - g * 4 * nv;
+  const int nwave = rem / (msz * 8);
+  const int r2 = rem - nwave * msz * 8;
+  const int nsz = nv - 8 * nwave < 8 ? nv - 8 * nwave : 8;
+  mt = (4 * g + r2 / nsz) * 8 + xcd;
+  n_tile = 8 * nwave + r2 % nsz;
+}
+
 __global__ __launch_bounds__(256) void k_fill_i64(int64_t* p, int64_t n, int64_t v) {
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
        i += static_cast<int64_t>(gridDim.x) * blockDim.x)
@@ -358,15 +375,8 @@ void k_head_fwd_pull(GemmShape s, GemmShape st, float2* part, int64_t ldp, int32
       write_clock_record(clk, clk_slots, c0, r0, epi_t.clock, static_cast<int64_t>(s.m_tiles) * s.n_tiles + n_tile);
       continue;
     }
-    // idx -> (group of up to 4 vocabulary tiles, token tile wave of up to 8, tile within it)
-    const int g = idx / (4 * nv);
-    const int msz = mx - 4 * g < 4 ? mx - 4 * g : 4;
-    const int rem = idx - g * 4 * nv;
-    const int nwave = rem / (msz * 8);
-    const int r2 = rem - nwave * msz * 8;
-    const int nsz = nv - 8 * nwave < 8 ? nv - 8 * nwave : 8;
-    const int mt = (4 * g + r2 / nsz) * 8 + xcd;
-    const int n_tile = 8 * nwave + r2 % nsz;
+    int mt, n_tile;
+    pull_tile(idx, mx, nv, xcd, mt, n_tile);
     const uint64_t c0 = clk ? __builtin_amdgcn_s_memtime() : 0;
     const uint64_t r0 = clk ? __builtin_amdgcn_s_memrealtime() : 0;
     epi.clock.start(clk != nullptr);
@@ -712,6 +722,48 @@ void k_bwd_dz(GemmShape s, EpiDz<E, kMasked> epi, int64_t* clk, int64_t clk_slot
   write_clock_record(clk, clk_slots, c0, r0, epi.clock);
 }
 
+// The logit recompute of one vocabulary block as a pulling launch (at up to 8192
+// tokens), with the block's partial last tile (st.m > 0) taken after each XCD's
+// full tiles: the same tile lists as the pulling head forward. Tile (v, t) of the
+// block records in slot v x n_tiles + t.
+template <class E>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_bwd_dz_pull(GemmShape s, GemmShape st, EpiDz<E, false> epi, EpiDz<E, true> epi_t, int32_t* next,
+                   int64_t* clk, int64_t clk_slots) {
+  __shared__ v4u lds[kStages][kStageChunks];
+  __shared__ int32_t s_idx;
+  const int xcd = static_cast<int>(blockIdx.x & 7);
+  const int64_t n_valid = s.n_dev ? static_cast<int64_t>(*s.n_dev) : s.n;
+  const int64_t nv64 = (n_valid + kBN - 1) / kBN;
+  const int nv = static_cast<int>(nv64 < s.n_tiles ? nv64 : s.n_tiles);
+  const int mx = xcd < s.m_tiles ? (s.m_tiles - 1 - xcd) / 8 + 1 : 0;
+  const int32_t total = mx * nv;
+  const int32_t tail = st.m > 0 && xcd < nv ? (nv - 1 - xcd) / 8 + 1 : 0;
+  for (;;) {
+    if (threadIdx.x == 0) s_idx = atomicAdd(next + xcd, 1);
+    __syncthreads();  // also: the previous tile's epilogue is done with LDS
+    const int32_t idx = s_idx;
+    __syncthreads();  // every thread has read s_idx
+    if (idx >= total + tail) break;
+    const uint64_t c0 = clk ? __builtin_amdgcn_s_memtime() : 0;
+    const uint64_t r0 = clk ? __builtin_amdgcn_s_memrealtime() : 0;
+    if (idx >= total) {
+      const int n_tile = (idx - total) * 8 + xcd;
+      epi_t.clock.start(clk != nullptr);
+      gemm_tile<E, false, false>(st, epi_t, lds, 0, n_tile);
+      // the record names the tile within the block, not within the tail's own shape
+      if (epi_t.clock.tile_id >= 0) epi_t.clock.tile_id += static_cast<int64_t>(s.m_tiles) << 32;
+      write_clock_record(clk, clk_slots, c0, r0, epi_t.clock, static_cast<int64_t>(s.m_tiles) * s.n_tiles + n_tile);
+      continue;
+    }
+    int mt, n_tile;
+    pull_tile(idx, mx, nv, xcd, mt, n_tile);
+    epi.clock.start(clk != nullptr);
+    gemm_tile<E, false, false>(s, epi, lds, mt, n_tile);
+    write_clock_record(clk, clk_slots, c0, r0, epi.clock, static_cast<int64_t>(mt) * s.n_tiles + n_tile);
+  }
+}
+
 // dH += dz . W (dz K-major, W MN-major) and dW += dz^T . Hg (both MN-major).
 template <class E, bool AMn, bool BMn>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
@@ -814,7 +866,7 @@ static hipError_t logprob_impl(const void* hidden, int64_t ld_hidden, const void
 
   const int nb = static_cast<int>(L.n_count_blocks);
   int32_t* next = reinterpret_cast<int32_t*>(w8 + L.next);
-  hipLaunchKernelGGL(k_count_rows, dim3(nb), dim3(256), 0, st, mask, nullptr, T, blk, next);
+  hipLaunchKernelGGL(k_count_rows, dim3(nb), dim3(256), 0, st, mask, nullptr, T, blk, next, 8);
   hipLaunchKernelGGL(k_compact_rows, dim3(nb), dim3(256), 0, st, mask, nullptr, T, blk, idx,
                      nullptr, count, logp, lse);
   const int rows4 = static_cast<int>(L.t_pad / 4);
@@ -895,7 +947,9 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
   const S* w = static_cast<const S*>(w_head);
 
   const int nb = static_cast<int>(L.n_count_blocks);
-  hipLaunchKernelGGL(k_count_rows, dim3(nb), dim3(256), 0, st, nullptr, g, T, blk, static_cast<int32_t*>(nullptr));
+  int32_t* next = reinterpret_cast<int32_t*>(w8 + L.next);  // 8 tile counters per vocabulary block
+  hipLaunchKernelGGL(k_count_rows, dim3(nb), dim3(256), 0, st, nullptr, g, T, blk, next,
+                     static_cast<int>(8 * L.n_vblocks));
   hipLaunchKernelGGL(k_compact_rows, dim3(nb), dim3(256), 0, st, nullptr, g, T, blk, idx, pos, count,
                      nullptr, nullptr);
   const int rows4 = static_cast<int>(L.t_pad / 4);
@@ -927,6 +981,7 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
     // (A) z^T[v][t] = W[v0 + v] . Hg[t] -> dz[t][v]: the block's tiles with 256 valid
     // vocabulary rows, then its partial last tile (if any) with the masked epilogue.
     const int64_t full_v = vlen / kBM * kBM;
+    bool tail_done = false;
     if (full_v > 0) {
       GemmShape sa = make_shape(w + v0 * ld_w, ld_w, full_v, hg, H, T, H);
       sa.n_dev = count;
@@ -938,12 +993,29 @@ static hipError_t backward_impl(const void* hidden, int64_t ld_hidden, const voi
         sa.sn = pick_sn_msplit(sa.n_tiles);
       }
       EpiDz<E, false> ez{dz, L.vc, full_v, v0, g_c, lse_c, y_c, {}, {}, {}, {}, {}};
+      int64_t* clk = clocks(vb, SAO_KERNEL_BACKWARD_DZ);
       hook(vb, SAO_KERNEL_BACKWARD_DZ, false);
-      hipLaunchKernelGGL((k_bwd_dz<E, false>), dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez,
-                         clocks(vb, SAO_KERNEL_BACKWARD_DZ), tm.clock_slots);
+      if (sa.n_tiles <= kPullMaxNTiles) {
+        // Few token tiles: tiles pulled per XCD, as in the head forward, the
+        // block's partial last tile included.
+        GemmShape stail{};
+        EpiDz<E, true> ezt{};
+        if (vlen > full_v) {
+          stail = make_shape(w + (v0 + full_v) * ld_w, ld_w, vlen - full_v, hg, H, T, H);
+          stail.n_dev = count;
+          ezt = EpiDz<E, true>{dz + full_v, L.vc, vlen - full_v, v0 + full_v, g_c, lse_c, y_c, {}, {}, {}, {}, {}};
+        }
+        if (clk) hipLaunchKernelGGL(k_fill_i64, dim3(64), dim3(256), 0, st, clk, 8 * tm.clock_slots, int64_t{0});
+        hipLaunchKernelGGL(k_bwd_dz_pull<E>, dim3(static_cast<unsigned>(pull_grid())), dim3(kThreads), 0, st, sa,
+                           stail, ez, ezt, next + 8 * vb, clk, tm.clock_slots);
+        tail_done = true;
+      } else {
+        hipLaunchKernelGGL((k_bwd_dz<E, false>), dim3(gemm_grid(sa)), dim3(kThreads), 0, st, sa, ez, clk,
+                           tm.clock_slots);
+      }
       hook(vb, SAO_KERNEL_BACKWARD_DZ, true);
     }
-    if (vlen > full_v) {
+    if (vlen > full_v && !tail_done) {
       GemmShape sa = make_shape(w + (v0 + full_v) * ld_w, ld_w, vlen - full_v, hg, H, T, H);
       sa.n_dev = count;
       EpiDz<E, true> ez{dz + full_v, L.vc, vlen - full_v, v0 + full_v, g_c, lse_c, y_c, {}, {}, {}, {}, {}};

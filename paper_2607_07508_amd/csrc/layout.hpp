@@ -53,7 +53,7 @@ inline LogprobLayout logprob_layout(int64_t T, int64_t H, int64_t V, size_t esiz
 struct BackwardLayout {
   int64_t t_pad, n_count_blocks, vc, n_vblocks;
   int dh_pieces;   // K pieces of the dH product (each with its own fp32 accumulator)
-  size_t blk_counts, count, idx, pos, g_c, lse_c, y_c, hg, dh, dz, total;
+  size_t blk_counts, count, next, idx, pos, g_c, lse_c, y_c, hg, dh, dz, total;
 };
 
 // K pieces of the dH product: enough that its output tiles number at least 1024
@@ -116,6 +116,7 @@ inline BackwardLayout backward_layout(int64_t T, int64_t H, int64_t V, size_t es
   const size_t tp = static_cast<size_t>(L.t_pad);
   L.blk_counts = c.take(4 * static_cast<size_t>(L.n_count_blocks));
   L.count = c.take(4);
+  L.next = c.take(4 * 8 * static_cast<size_t>(L.n_vblocks));  // the recompute's tile counters
   L.idx = c.take(4 * tp);
   L.pos = c.take(4 * static_cast<size_t>(T));
   L.g_c = c.take(4 * tp);
