@@ -326,16 +326,17 @@ __global__ __launch_bounds__(256) void k_fill_i64(int64_t* p, int64_t n, int64_t
     p[i] = v;
 }
 
-// The head forward over the full vocabulary tiles, as a grid of workgroups (a
-// multiple of 8, normally one per CU) that pull tiles until none is left,
-// instead of one workgroup per tile. Workgroup b runs on XCD b % 8 and takes
-// the tiles of that XCD's vocabulary tiles (v with v % 8 == b % 8) from the
-// XCD's own counter next[b % 8] (zeroed before the launch), in groups of 4
-// vocabulary tiles x 8 token tiles, so that the 32 tiles an XCD runs at once
-// share 12 operand panels in its L2. Only valid token tiles (below the device
-// count) are enumerated, so no workgroup is dispatched for nothing, and a
-// workgroup takes its next tile as soon as it is free, whichever shader engine
-// it sits on. The timeline hook records tile (v, t) in slot v x n_tiles + t.
+// The head forward as a grid of workgroups (a multiple of 8, normally one per
+// CU) that pull tiles until none is left, instead of one workgroup per tile.
+// Workgroup b runs on XCD b % 8 and takes, from the XCD's own counter
+// next[b % 8] (zeroed before the launch), first the tiles of that XCD's full
+// vocabulary tiles (v with v % 8 == b % 8; order of pull_tile), then, when st
+// describes a partial last vocabulary tile (st.m > 0), that tile's token tiles
+// t with t % 8 == b % 8, with the masked epilogue. Only valid token tiles (below
+// the device count) are enumerated, so no workgroup is dispatched for nothing,
+// and a workgroup takes its next tile as soon as it is free, whichever shader
+// engine it sits on. The timeline hook records tile (v, t) in slot
+// v x n_tiles + t (the partial tile as v = s.m_tiles).
 template <class E>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_head_fwd_pull(GemmShape s, GemmShape st, float2* part, int64_t ldp, int32_t* next, int64_t* clk,
