@@ -832,12 +832,13 @@ static GemmShape make_shape(const void* a, int64_t lda, int64_t m, const void* b
   return s;
 }
 
-// Host-bound token tiles up to which the forward pulls its tiles
-// (k_head_fwd_pull) rather than launching one workgroup per tile of the host
-// bound. Measured per workload against the one-workgroup-per-tile raster: an
-// 8192-token chunk (32 host-bound tiles, about 16 with loss-mask rows) 7 %
-// faster; 32,768 tokens at H = 6144 (128 tiles) 4 % slower, 65,536 tokens
-// (256) 0.7 % slower.
+// Host-bound token tiles up to which the forward and the backward's logit
+// recompute pull their tiles (k_head_fwd_pull, k_bwd_dz_pull) rather than
+// launching one workgroup per tile of the host bound. Measured per workload
+// against the one-workgroup-per-tile raster: on an 8192-token chunk (32
+// host-bound tiles, about 16 with loss-mask rows) the forward 7 % faster and
+// the recompute 6 %; the forward at 32,768 tokens and H = 6144 (128 tiles) 4 %
+// slower, at 65,536 tokens (256) 0.7 % slower.
 constexpr int kPullMaxNTiles = 32;
 
 // Workgroups of a pulling launch: one per CU of the current device, rounded
