@@ -594,13 +594,15 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--vendor-gemm", action="store_true",
-                    help="also time torch.matmul (bf16) at the forward's shape, as context (allocates the T_act x V output)")
+                    help="also time torch.matmul (bf16) at the four head shapes (forward; dz, dH and dW of a full "
+                         "backward block), as context (allocates the T_act x V output)")
     ap.add_argument("--timeline", action="store_true",
                     help="also record the per-workgroup timelines of the head forward and the backward's three "
                          "products (first vocabulary block), one extra step each")
     ap.add_argument("--mfma-ceiling", action="store_true",
                     help="run only the MFMA probe loops (register operands: random, constant, refreshed; LDS-fed "
-                         "without and with the engine's copies), one line per mode")
+                         "without and with the engine's copies; both operands MN-major through the transposing read, "
+                         "without and with the copies), one line per mode")
     ap.add_argument("--epilogue-sweep", action="store_true",
                     help="HBM bandwidth of the scan and loss epilogue at T = 2^20 .. 2^26 (one line per size)")
     args = ap.parse_args()
